@@ -1,0 +1,230 @@
+"""fp64 CPU oracle of the VGGT-Prime routed global-attention layer.
+
+TEST INFRASTRUCTURE ONLY.  Imported by the tests, by the smoke check and by
+the benchmark's CPU-baseline leg; never by the GPU library or its binding.
+It shares no code with the GPU path (only the seeded input generators are
+common).  The arithmetic lives in ``vp_oracle.c`` (plain C, double precision,
+written from the paper's equations); this module loads it, composes the
+layer in the paper's order and adds the trivial MEAN broadcast.
+
+Pins (tests/test_oracle_pins.py) tie every function here to something other
+than itself: library routines (scaled-dot-product attention, softmax, erf),
+closed forms (planted key, zero queries, one-hot router rows), invariants
+(rows summing to one, token-permutation equivariance, S identical views) and
+a numpy brute force on tiny shapes.  The surrogate MLP's exact architecture is
+a reading of the paper (it gives only "a lightweight MLP" of hidden size 64):
+its structure is pinned by closed-form special cases, but no paper number
+fixes it -- parity unpinned as to the architecture itself.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "vp_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+MODE_MEAN, MODE_SURR, MODE_FULL = 0, 1, 2
+RULE_THRESHOLD, RULE_ARGMAX = 0, 1
+ACT_GELU, ACT_RELU = 0, 1
+TAU_LOW, TAU_HIGH = 0.01, 0.20   # Section 4.2 and implementation details
+
+
+def build(force: bool = False) -> str:
+    """Compile vp_oracle.c with gcc (strict IEEE double; no fast-math)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-o", tmp, _SRC,
+                               "-lm", "-lpthread"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            # VP_ORACLE_LIB names a prebuilt variant (the mutation tests plant
+            # mistakes in a copy of vp_oracle.c and check that the pins fail).
+            path = os.environ.get("VP_ORACLE_LIB")
+            if not path:
+                path = build()
+            lib = ctypes.CDLL(path)
+            P = ctypes.c_void_p
+            i64, i32, dbl, flt = ctypes.c_int64, ctypes.c_int, ctypes.c_double, ctypes.c_float
+            lib.or_router_pool.argtypes = [P, i64, i32, i32, i32, P, P, P, P, P, P, i32]
+            lib.or_router_route.argtypes = [P, P, i64, i32, i32, P, dbl, P, P, P, P, i32]
+            lib.or_router_logits.argtypes = [P, P, P, i32, i32, P]
+            lib.or_assign.argtypes = [P, i32, i32, flt, flt, P]
+            lib.or_full_rows.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, dbl, P, i32]
+            lib.or_surr_rows.argtypes = [P, i64, i32, i32, i32, i32, i32, P, P, P, P, P, P, P,
+                                         P, P, P, i64, P, i32]
+            lib.or_threads_used.argtypes = [i32]
+            lib.or_threads_used.restype = i32
+            _lib = lib
+    return _lib
+
+
+def as_f32(x) -> np.ndarray:
+    """Stored values as a C-contiguous float32 array (exact for bf16 and fp32)."""
+    if hasattr(x, "detach"):
+        x = x.detach().float().cpu().numpy()
+    return np.ascontiguousarray(x, dtype=np.float32)
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def threads_used(nthreads: int = 0) -> int:
+    return _load().or_threads_used(nthreads)
+
+
+# ------------------------------------------------------------------ steps
+
+def router_pool(Q, W, U, w, nthreads=0, want_weights=False):
+    """Eq.1-2: gated attention pooling.  Returns q_pool [H, d] (and a, alpha [H, N])."""
+    Q, W, U, w = as_f32(Q), as_f32(W), as_f32(U), as_f32(w)
+    N, H, d = Q.shape
+    L = W.shape[1]
+    qp = np.zeros((H, d), np.float64)
+    a = np.zeros((H, N), np.float64) if want_weights else None
+    al = np.zeros((H, N), np.float64) if want_weights else None
+    _load().or_router_pool(_p(Q), N, H, d, L, _p(W), _p(U), _p(w), _p(qp), _p(a), _p(al),
+                           nthreads)
+    return (qp, a, al) if want_weights else qp
+
+
+def router_route(K, V, q_pool, scale=None, nthreads=0, want_r=False):
+    """Eq.3 and Eq.5: single-query attention r_h, saliency s_h = max r_h,
+    context C_h = r_h V_h and value mean.  Returns (s [H], C [H,d], mean [H,d] [, r])."""
+    K, V = as_f32(K), as_f32(V)
+    N, H, d = K.shape
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    qp = np.ascontiguousarray(q_pool, dtype=np.float64)
+    s = np.zeros(H, np.float64)
+    C = np.zeros((H, d), np.float64)
+    mean = np.zeros((H, d), np.float64)
+    r = np.zeros((H, N), np.float64) if want_r else None
+    _load().or_router_route(_p(K), _p(V), N, H, d, _p(qp), float(scale), _p(r), _p(s), _p(C),
+                            _p(mean), nthreads)
+    return (s, C, mean, r) if want_r else (s, C, mean)
+
+
+def router_logits(u, Wr, br):
+    """Linear-logit mode router of the synthetic workloads: [H, 3] logits."""
+    u, Wr, br = as_f32(u), as_f32(Wr), as_f32(br)
+    R, Din = Wr.shape
+    out = np.zeros(R, np.float64)
+    _load().or_router_logits(_p(u), _p(Wr), _p(br), R, Din, _p(out))
+    return out.reshape(R // 3, 3)
+
+
+def assign(scores, rule, tau_low=TAU_LOW, tau_high=TAU_HIGH):
+    """Eq.4 (threshold on s_h) or first-argmax of per-head logits."""
+    sc = np.ascontiguousarray(scores, dtype=np.float64)
+    H = sc.shape[0]
+    modes = np.zeros(H, np.uint8)
+    _load().or_assign(_p(sc), H, int(rule), float(tau_low), float(tau_high), _p(modes))
+    return modes
+
+
+def buckets(modes):
+    """Counts per mode and head ids grouped by mode (MEAN, SURR, FULL), each
+    group in ascending head order."""
+    modes = np.asarray(modes)
+    counts = np.array([(modes == m).sum() for m in range(3)], np.int32)
+    lst = np.concatenate([np.nonzero(modes == m)[0] for m in range(3)]).astype(np.int32)
+    return counts, lst
+
+
+def full_rows(Q, K, V, h, rows=None, scale=None, nthreads=0):
+    """Algorithm 1 FULL branch for head h on the given query rows: [R, d]."""
+    Q, K, V = as_f32(Q), as_f32(K), as_f32(V)
+    N, H, d = Q.shape
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    if rows is None:
+        nr, rp = N, None
+    else:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        nr, rp = rows.shape[0], rows
+    Y = np.zeros((nr, d), np.float64)
+    _load().or_full_rows(_p(Q), _p(K), _p(V), N, H, d, int(h), _p(rp), nr, float(scale), _p(Y),
+                         nthreads)
+    return Y
+
+
+def surr_rows(V, C_h, surr, h, rows=None, act=ACT_GELU, nthreads=0):
+    """Eq.5-7 SURR branch for head h: [R, d].  ``surr`` holds the per-head
+    stacked weights g_w1 [H,L,2d], g_b1 [H,L], g_w2 [H,d,L], g_b2 [H,d], d_*."""
+    V = as_f32(V)
+    N, H, d = V.shape
+    wt = {k: np.ascontiguousarray(as_f32(v)[h]) for k, v in surr.items()}
+    L = wt["g_w1"].shape[0]
+    C_h = np.ascontiguousarray(C_h, dtype=np.float64)
+    if rows is None:
+        nr, rp = N, None
+    else:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        nr, rp = rows.shape[0], rows
+    Y = np.zeros((nr, d), np.float64)
+    _load().or_surr_rows(_p(V), N, H, d, int(h), L, int(act), _p(C_h), _p(wt["g_w1"]),
+                         _p(wt["g_b1"]), _p(wt["g_w2"]), _p(wt["g_b2"]), _p(wt["d_w1"]),
+                         _p(wt["d_b1"]), _p(wt["d_w2"]), _p(wt["d_b2"]), _p(rp), nr, _p(Y),
+                         nthreads)
+    return Y
+
+
+def routed_layer(Q, K, V, W, U, w, surr, u=None, Wr=None, br=None, rule=RULE_ARGMAX,
+                 tau_low=TAU_LOW, tau_high=TAU_HIGH, modes=None, rows=None, full_rows_sel=None,
+                 act=ACT_GELU, scale_router=None, scale_attn=None, nthreads=0):
+    """The routed global-attention layer (Algorithm 1 step 2, Eq.1-7), in order:
+    router pooling, single-query routing, mode assignment, per-head outputs,
+    concatenation over heads.
+
+    ``rows``: query rows at which Y is evaluated (all if None).
+    ``full_rows_sel``: for FULL heads only, evaluate these rows instead (the
+    row sample used at sizes where exact attention over every row is too slow);
+    the returned ``Y_full_rows`` then holds them.
+    ``modes``: explicit modes (bypasses the rule, e.g. to force every head FULL).
+    """
+    Q32 = as_f32(Q)
+    N, H, d = Q32.shape
+    q_pool = router_pool(Q32, W, U, w, nthreads)
+    s, C, mean = router_route(K, V, q_pool, scale_router, nthreads)
+    logits = None
+    if modes is None:
+        if rule == RULE_THRESHOLD:
+            modes = assign(s, RULE_THRESHOLD, tau_low, tau_high)
+        else:
+            if u is None:   # default router input: the pooled queries of all heads
+                u = q_pool.reshape(-1).astype(np.float32)
+            logits = router_logits(u, Wr, br)
+            modes = assign(logits, RULE_ARGMAX)
+    modes = np.asarray(modes, np.uint8)
+    nrow = N if rows is None else len(rows)
+    Y = np.zeros((nrow, H, d), np.float64)
+    Yf = {}
+    for h in range(H):
+        m = int(modes[h])
+        if m == MODE_FULL:
+            if full_rows_sel is not None:
+                Yf[h] = full_rows(Q32, K, V, h, full_rows_sel, scale_attn, nthreads)
+                Y[:, h, :] = np.nan
+            else:
+                Y[:, h, :] = full_rows(Q32, K, V, h, rows, scale_attn, nthreads)
+        elif m == MODE_SURR:
+            Y[:, h, :] = surr_rows(V, C[h], surr, h, rows, act, nthreads)
+        else:
+            Y[:, h, :] = mean[h][None, :]     # Algorithm 1: broadcast of the value mean
+    return dict(q_pool=q_pool, s=s, C=C, mean=mean, logits=logits, modes=modes, Y=Y,
+                Y_full_rows=Yf)

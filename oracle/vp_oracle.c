@@ -1,0 +1,365 @@
+/*
+ * vp_oracle.c -- fp64 CPU oracle of the VGGT-Prime routed global-attention
+ * layer.  TEST INFRASTRUCTURE ONLY: this code is the parity reference for the
+ * GPU library and is used only by the tests, the smoke check and the CPU
+ * baseline timing of the benchmark.  It shares no code with the GPU path.
+ *
+ * Everything is computed in double precision from the stored input values
+ * (fp32 arrays; bf16 inputs are widened exactly before they arrive here),
+ * straight from the definitions, with no tiling and no online softmax.
+ * Threads only split independent work (rows, heads); every reduction runs
+ * serially in index order, so results are deterministic.
+ *
+ * Layouts: Q, K, V are [N, H, d] row-major, N = S * P tokens of all views;
+ * the row of head h for token i starts at (i * H + h) * d.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+#define OR_MODE_MEAN 0
+#define OR_MODE_SURR 1
+#define OR_MODE_FULL 2
+
+/* ---------------------------------------------------------------- threads */
+
+typedef void (*or_body)(void *ctx, int64_t lo, int64_t hi);
+typedef struct {
+    or_body body;
+    void *ctx;
+    int64_t lo, hi;
+} or_chunk;
+
+static void *or_thread_main(void *p) {
+    or_chunk *c = (or_chunk *)p;
+    if (c->lo < c->hi) c->body(c->ctx, c->lo, c->hi);
+    return NULL;
+}
+
+static int or_nthreads(int requested) {
+    if (requested > 0) return requested;
+    long n = sysconf(_SC_NPROCESSORS_ONLN);
+    return n > 0 ? (int)n : 1;
+}
+
+/* Run body over [0, n) split into contiguous chunks, one per thread. */
+static void or_parallel_for(int64_t n, int nthreads, or_body body, void *ctx) {
+    int T = or_nthreads(nthreads);
+    if (T > n) T = (int)(n > 0 ? n : 1);
+    if (T <= 1) {
+        if (n > 0) body(ctx, 0, n);
+        return;
+    }
+    pthread_t *th = (pthread_t *)malloc(sizeof(pthread_t) * T);
+    or_chunk *ch = (or_chunk *)malloc(sizeof(or_chunk) * T);
+    for (int t = 0; t < T; ++t) {
+        ch[t].body = body;
+        ch[t].ctx = ctx;
+        ch[t].lo = n * t / T;
+        ch[t].hi = n * (t + 1) / T;
+        pthread_create(&th[t], NULL, or_thread_main, &ch[t]);
+    }
+    for (int t = 0; t < T; ++t) pthread_join(th[t], NULL);
+    free(th);
+    free(ch);
+}
+
+int or_threads_used(int requested) { return or_nthreads(requested); }
+
+static double sigmoid(double x) { return 1.0 / (1.0 + exp(-x)); }
+
+/* ------------------------------------------------ router pooling (Eq.1-2) */
+/*
+ * Gated attention pooling of the queries of head h (Section 4.1, Eq.1, a
+ * pooling module from attention-based multiple-instance learning):
+ *   a_{h,i} = sum_l w_h[l] * tanh((W_h q_{h,i})_l) * sigmoid((U_h q_{h,i})_l)
+ *   alpha_h = softmax over all N tokens of a_h
+ *   q_pool_h = sum_i alpha_{h,i} q_{h,i}                               (Eq.2)
+ * W_h, U_h are [L, d]; w_h is [L]; no biases appear in Eq.1.
+ */
+typedef struct {
+    const float *Q, *W, *U, *w;
+    int64_t N;
+    int H, d, L;
+    double *a; /* [H, N] */
+} pool_ctx;
+
+static void pool_logits_body(void *p, int64_t lo, int64_t hi) {
+    pool_ctx *c = (pool_ctx *)p;
+    for (int64_t idx = lo; idx < hi; ++idx) {
+        int h = (int)(idx / c->N);
+        int64_t i = idx % c->N;
+        const float *q = c->Q + (i * c->H + h) * (int64_t)c->d;
+        const float *Wh = c->W + (int64_t)h * c->L * c->d;
+        const float *Uh = c->U + (int64_t)h * c->L * c->d;
+        const float *wh = c->w + (int64_t)h * c->L;
+        double a = 0.0;
+        for (int l = 0; l < c->L; ++l) {
+            double x = 0.0, y = 0.0;
+            for (int k = 0; k < c->d; ++k) {
+                x += (double)Wh[l * c->d + k] * (double)q[k];
+                y += (double)Uh[l * c->d + k] * (double)q[k];
+            }
+            a += (double)wh[l] * tanh(x) * sigmoid(y);
+        }
+        c->a[(int64_t)h * c->N + i] = a;
+    }
+}
+
+/* q_pool [H, d]; optional a_out / alpha_out [H, N] (pre-softmax logits, weights). */
+void or_router_pool(const float *Q, int64_t N, int H, int d, int L, const float *W,
+                    const float *U, const float *w, double *q_pool, double *a_out,
+                    double *alpha_out, int nthreads) {
+    double *a = (double *)malloc(sizeof(double) * (size_t)N * H);
+    pool_ctx c = {Q, W, U, w, N, H, d, L, a};
+    or_parallel_for(N * H, nthreads, pool_logits_body, &c);
+    for (int h = 0; h < H; ++h) {
+        const double *ah = a + (int64_t)h * N;
+        double mx = -INFINITY;
+        for (int64_t i = 0; i < N; ++i)
+            if (ah[i] > mx) mx = ah[i];
+        double sum = 0.0;
+        for (int64_t i = 0; i < N; ++i) sum += exp(ah[i] - mx);
+        double *qp = q_pool + (int64_t)h * d;
+        for (int k = 0; k < d; ++k) qp[k] = 0.0;
+        for (int64_t i = 0; i < N; ++i) {
+            double alpha = exp(ah[i] - mx) / sum;
+            if (alpha_out) alpha_out[(int64_t)h * N + i] = alpha;
+            const float *q = Q + (i * H + h) * (int64_t)d;
+            for (int k = 0; k < d; ++k) qp[k] += alpha * (double)q[k];
+        }
+        if (a_out) memcpy(a_out + (int64_t)h * N, ah, sizeof(double) * N);
+    }
+    free(a);
+}
+
+/* --------------------------- single-query attention and saliency (Eq.3) */
+/*
+ * The pooled query attends over all N keys of all views (Section 4.1):
+ *   t_{h,j} = scale * (q_pool_h . k_{h,j}),   r_h = softmax_j(t_h)
+ *   s_h = max_j r_h(j)                                                 (Eq.3)
+ * and, reusing r_h (Section 4.3, Eq.5; Algorithm 1 mean branch):
+ *   C_h = r_h V_h,     mean_h = (1/N) sum_j v_{h,j}
+ */
+typedef struct {
+    const float *K, *V;
+    int64_t N;
+    int H, d;
+    const double *q_pool;
+    double scale;
+    double *r_out, *s, *C, *mean;
+} route_ctx;
+
+static void route_body(void *p, int64_t lo, int64_t hi) {
+    route_ctx *c = (route_ctx *)p;
+    int64_t N = c->N;
+    int H = c->H, d = c->d;
+    double *t = (double *)malloc(sizeof(double) * N);
+    for (int64_t h = lo; h < hi; ++h) {
+        const double *qp = c->q_pool + h * d;
+        for (int64_t j = 0; j < N; ++j) {
+            const float *k = c->K + (j * H + h) * (int64_t)d;
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e) dot += qp[e] * (double)k[e];
+            t[j] = c->scale * dot;
+        }
+        double mx = -INFINITY;
+        for (int64_t j = 0; j < N; ++j)
+            if (t[j] > mx) mx = t[j];
+        double sum = 0.0;
+        for (int64_t j = 0; j < N; ++j) sum += exp(t[j] - mx);
+        double smax = 0.0;
+        double *C = c->C + h * d, *mean = c->mean + h * d;
+        for (int e = 0; e < d; ++e) C[e] = mean[e] = 0.0;
+        for (int64_t j = 0; j < N; ++j) {
+            double r = exp(t[j] - mx) / sum;
+            if (c->r_out) c->r_out[h * N + j] = r;
+            if (r > smax) smax = r;
+            const float *v = c->V + (j * H + h) * (int64_t)d;
+            for (int e = 0; e < d; ++e) {
+                C[e] += r * (double)v[e];
+                mean[e] += (double)v[e];
+            }
+        }
+        for (int e = 0; e < d; ++e) mean[e] /= (double)N;
+        c->s[h] = smax;
+    }
+    free(t);
+}
+
+void or_router_route(const float *K, const float *V, int64_t N, int H, int d,
+                     const double *q_pool, double scale, double *r_out, double *s,
+                     double *C, double *mean, int nthreads) {
+    route_ctx c = {K, V, N, H, d, q_pool, scale, r_out, s, C, mean};
+    or_parallel_for(H, nthreads, route_body, &c);
+}
+
+/* ------------------------------------------------ linear-logit mode router */
+/*
+ * Mode router of the synthetic workloads (not a construct of the paper): a
+ * linear map of a 1024-vector to H*3 logits, logits[r] = W_r[r] . u + b_r[r],
+ * row r = h * 3 + m with m in (MEAN, SURR, FULL).
+ */
+void or_router_logits(const float *u, const float *Wr, const float *br, int R, int Din,
+                      double *logits) {
+    for (int r = 0; r < R; ++r) {
+        double acc = 0.0;
+        for (int c = 0; c < Din; ++c) acc += (double)Wr[(int64_t)r * Din + c] * (double)u[c];
+        logits[r] = acc + (double)br[r];
+    }
+}
+
+/* --------------------------------------------------- mode assignment (Eq.4) */
+/*
+ * rule 0 (threshold, Eq.4): FULL if s >= tau_high; MEAN if s <= tau_low;
+ *   SURR strictly between.  The thresholds arrive as fp32 and are widened.
+ * rule 1 (argmax over the three logits of a head): the first maximal index.
+ * A NaN score sends the head to FULL (the paper is silent; FULL is exact).
+ */
+void or_assign(const double *scores, int H, int rule, float tau_low, float tau_high,
+               uint8_t *modes) {
+    for (int h = 0; h < H; ++h) {
+        if (rule == 0) {
+            double s = scores[h];
+            if (isnan(s) || s >= (double)tau_high)
+                modes[h] = OR_MODE_FULL;
+            else if (s <= (double)tau_low)
+                modes[h] = OR_MODE_MEAN;
+            else
+                modes[h] = OR_MODE_SURR;
+        } else {
+            const double *lg = scores + (int64_t)h * 3;
+            int best = 0, bad = isnan(lg[0]);
+            for (int m = 1; m < 3; ++m) {
+                if (isnan(lg[m])) bad = 1;
+                if (lg[m] > lg[best]) best = m;
+            }
+            modes[h] = bad ? OR_MODE_FULL : (uint8_t)best;
+        }
+    }
+}
+
+/* --------------------------------------------- FULL mode (Algorithm 1, eq) */
+/*
+ * Exact softmax attention of head h over all N tokens of all views
+ * (Algorithm 1, first branch): for query row i,
+ *   l_j = (q_{h,i} . k_{h,j}) * scale,  p = softmax(l),  y_i = sum_j p_j v_{h,j}
+ * Two passes per row (max, then exponentials), scale = 1/sqrt(d).
+ */
+typedef struct {
+    const float *Q, *K, *V;
+    int64_t N;
+    int H, d, h;
+    const int64_t *rows;
+    double scale;
+    double *Y;
+} full_ctx;
+
+static void full_body(void *p, int64_t lo, int64_t hi) {
+    full_ctx *c = (full_ctx *)p;
+    int64_t N = c->N;
+    int H = c->H, d = c->d, h = c->h;
+    double *l = (double *)malloc(sizeof(double) * N);
+    for (int64_t r = lo; r < hi; ++r) {
+        int64_t i = c->rows ? c->rows[r] : r;
+        const float *q = c->Q + (i * H + h) * (int64_t)d;
+        double mx = -INFINITY;
+        for (int64_t j = 0; j < N; ++j) {
+            const float *k = c->K + (j * H + h) * (int64_t)d;
+            double dot = 0.0;
+            for (int e = 0; e < d; ++e) dot += (double)q[e] * (double)k[e];
+            l[j] = dot * c->scale;
+            if (l[j] > mx) mx = l[j];
+        }
+        double sum = 0.0;
+        double *y = c->Y + r * d;
+        for (int e = 0; e < d; ++e) y[e] = 0.0;
+        for (int64_t j = 0; j < N; ++j) {
+            double pj = exp(l[j] - mx);
+            sum += pj;
+            const float *v = c->V + (j * H + h) * (int64_t)d;
+            for (int e = 0; e < d; ++e) y[e] += pj * (double)v[e];
+        }
+        for (int e = 0; e < d; ++e) y[e] /= sum;
+    }
+    free(l);
+}
+
+/* Y [nrows, d]; rows == NULL means rows 0..nrows-1. */
+void or_full_rows(const float *Q, const float *K, const float *V, int64_t N, int H, int d,
+                  int h, const int64_t *rows, int64_t nrows, double scale, double *Y,
+                  int nthreads) {
+    full_ctx c = {Q, K, V, N, H, d, h, rows, scale, Y};
+    or_parallel_for(nrows, nthreads, full_body, &c);
+}
+
+/* --------------------------------------- SURR mode (Section 4.3, Eq.5-7) */
+/*
+ * Learned surrogate attention of head h for token i:
+ *   z = [v_{h,i}; C_h]                       (value first, then context)
+ *   gamma = sigmoid(MLP_gamma(z)),  delta = MLP_delta(z)               (Eq.6)
+ *   y_i = C_h + gamma (.) delta                                        (Eq.7)
+ * Each MLP is Linear(2d -> L) -> act -> Linear(L -> d), with biases;
+ * act 0 = GELU (erf form), act 1 = ReLU.  w1 is [L, 2d], w2 is [d, L].
+ */
+typedef struct {
+    const float *V;
+    int64_t N;
+    int H, d, h, L, act;
+    const double *C;
+    const float *gw1, *gb1, *gw2, *gb2, *dw1, *db1, *dw2, *db2;
+    const int64_t *rows;
+    double *Y;
+} surr_ctx;
+
+static double act_fn(double x, int act) {
+    if (act == 1) return x > 0.0 ? x : 0.0;
+    return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));
+}
+
+static void mlp(const double *z, int din, int L, int dout, const float *w1, const float *b1,
+                const float *w2, const float *b2, int act, double *hid, double *out) {
+    for (int l = 0; l < L; ++l) {
+        double acc = (double)b1[l];
+        for (int c = 0; c < din; ++c) acc += (double)w1[(int64_t)l * din + c] * z[c];
+        hid[l] = act_fn(acc, act);
+    }
+    for (int k = 0; k < dout; ++k) {
+        double acc = (double)b2[k];
+        for (int l = 0; l < L; ++l) acc += (double)w2[(int64_t)k * L + l] * hid[l];
+        out[k] = acc;
+    }
+}
+
+static void surr_body(void *p, int64_t lo, int64_t hi) {
+    surr_ctx *c = (surr_ctx *)p;
+    int d = c->d, L = c->L;
+    double *z = (double *)malloc(sizeof(double) * (2 * d + 2 * L + 2 * d));
+    double *hid = z + 2 * d, *g = hid + L, *dl = g + d;
+    for (int64_t r = lo; r < hi; ++r) {
+        int64_t i = c->rows ? c->rows[r] : r;
+        const float *v = c->V + (i * c->H + c->h) * (int64_t)d;
+        for (int e = 0; e < d; ++e) {
+            z[e] = (double)v[e];
+            z[d + e] = c->C[e];
+        }
+        mlp(z, 2 * d, L, d, c->gw1, c->gb1, c->gw2, c->gb2, c->act, hid, g);
+        mlp(z, 2 * d, L, d, c->dw1, c->db1, c->dw2, c->db2, c->act, hid, dl);
+        double *y = c->Y + r * d;
+        for (int e = 0; e < d; ++e) y[e] = c->C[e] + sigmoid(g[e]) * dl[e];
+    }
+    free(z);
+}
+
+/* Weights passed for head h only (already offset by the caller). */
+void or_surr_rows(const float *V, int64_t N, int H, int d, int h, int L, int act,
+                  const double *C_h, const float *gw1, const float *gb1, const float *gw2,
+                  const float *gb2, const float *dw1, const float *db1, const float *dw2,
+                  const float *db2, const int64_t *rows, int64_t nrows, double *Y,
+                  int nthreads) {
+    surr_ctx c = {V, N, H, d, h, L, act, C_h, gw1, gb1, gw2, gb2, dw1, db1, dw2, db2, rows, Y};
+    or_parallel_for(nrows, nthreads, surr_body, &c);
+}

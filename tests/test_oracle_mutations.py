@@ -1,0 +1,56 @@
+"""The oracle pins catch plausible mistakes.
+
+Each case plants one mistake in a copy of the oracle's C source (on the CPU),
+builds it, and runs the pin suite against that build: the suite must fail.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "vp_oracle.c")
+
+MUTANTS = {
+    "tanh_sigmoid_swapped": ("a += (double)wh[l] * tanh(x) * sigmoid(y);",
+                             "a += (double)wh[l] * sigmoid(x) * tanh(y);"),
+    "gate_weight_dropped": ("a += (double)wh[l] * tanh(x) * sigmoid(y);",
+                            "a += tanh(x) * sigmoid(y);"),
+    "U_replaced_by_W": ("y += (double)Uh[l * c->d + k] * (double)q[k];",
+                        "y += (double)Wh[l * c->d + k] * (double)q[k];"),
+    "router_scale_dropped": ("t[j] = c->scale * dot;", "t[j] = dot;"),
+    "saliency_not_max": ("if (r > smax) smax = r;", "smax += r / (double)N;"),
+    "mean_wrong_count": ("mean[e] /= (double)N;", "mean[e] /= (double)(N - 1 > 0 ? N - 1 : 1);"),
+    "attn_scale_dropped": ("l[j] = dot * c->scale;", "l[j] = dot;"),
+    "attn_not_normalised": ("for (int e = 0; e < d; ++e) y[e] /= sum;", "(void)sum;"),
+    "attn_wrong_head_keys": ("const float *k = c->K + (j * H + h) * (int64_t)d;\n            double dot = 0.0;\n            for (int e = 0; e < d; ++e) dot += (double)q[e]",
+                             "const float *k = c->K + (j * H + (h + 1) % H) * (int64_t)d;\n            double dot = 0.0;\n            for (int e = 0; e < d; ++e) dot += (double)q[e]"),
+    "concat_order_swapped": ("z[e] = (double)v[e];\n            z[d + e] = c->C[e];",
+                             "z[d + e] = (double)v[e];\n            z[e] = c->C[e];"),
+    "gate_sigmoid_dropped": ("y[e] = c->C[e] + sigmoid(g[e]) * dl[e];", "y[e] = c->C[e] + g[e] * dl[e];"),
+    "context_residual_dropped": ("y[e] = c->C[e] + sigmoid(g[e]) * dl[e];", "y[e] = sigmoid(g[e]) * dl[e];"),
+    "gelu_tanh_form": ("return 0.5 * x * (1.0 + erf(x / sqrt(2.0)));",
+                       "return 0.5 * x * (1.0 + tanh(0.7978845608 * (x + 0.044715 * x * x * x)));"),
+    "tau_high_exclusive": ("s >= (double)tau_high", "s > (double)tau_high"),
+    "tau_low_exclusive": ("s <= (double)tau_low", "s < (double)tau_low"),
+    "argmax_last_tie": ("if (lg[m] > lg[best]) best = m;", "if (lg[m] >= lg[best]) best = m;"),
+    "logit_bias_dropped": ("logits[r] = acc + (double)br[r];", "logits[r] = acc;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_mutant(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, "mutation anchor not found once: " + name
+    msrc = tmp_path / "mutant.c"
+    msrc.write_text(src.replace(old, new))
+    lib = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-o", str(lib),
+                           str(msrc), "-lm", "-lpthread"])
+    env = dict(os.environ, VP_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, "pins did not catch mutant %s:\n%s" % (name, r.stdout[-2000:])
