@@ -1,0 +1,188 @@
+"""Benchmark of the routed global-attention layer on one MI355X.
+
+A step is one pass of the whole layer on device-resident inputs:
+router_score -> router_logits -> assign_heads -> routed global attention
+(bucket gather, FULL-head attention, SURR/MEAN heads).  The headline
+workload is S = 100 views x 1374 tokens (N = 137,400), 16 heads x 64, bf16
+operands with fp32 accumulation, bf16 Y, 4 of 16 heads routed FULL by the
+seeded linear-logit mode router.  The JSON line also carries the latency of
+the other view counts and full-head counts (`by_workload`), the roofline of
+the FULL-head kernel, and the fp64 CPU oracle timed on a bounded sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "routed global-attn layer latency (ms) + TFLOP/s & % bf16 MFMA peak vs S"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+P_TOKENS = 1374
+HEADS, D, L = 16, 64, 64
+
+
+def flops_full(N, n_full):
+    """Algorithmic FULL-head work: QK^T and PV, 2 * N^2 * d each."""
+    return 4.0 * N * N * D * n_full
+
+
+def layer_flops(N, n_full, n_surr, n_mean):
+    """Algorithmic work of the whole layer (complexity terms of the paper's
+    appendix): FULL 4 N^2 d per head; router N H (4 d L + 2 L + 2 d) plus the
+    single-query pass 4 N H d; SURR 8 d L N per head; MEAN N d per head."""
+    router = N * HEADS * (4 * D * L + 2 * L + 2 * D) + 4 * N * HEADS * D
+    return flops_full(N, n_full) + router + 8 * D * L * N * n_surr + N * D * n_mean
+
+
+def measure(layer, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        layer.step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for k in range(steps):
+        layer.step(events=ev[k])
+    t1.record()
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / steps
+    full = sorted(a.elapsed_time(b) for a, b in ev)
+    return ms_step, sum(full) / len(full), full[len(full) // 2]
+
+
+def run_workload(S, n_full, steps, warmup, seed_key):
+    import torch
+    from paper_2609_23733_amd import synth, vp
+    x = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=n_full, key=seed_key,
+                         qkv_device="cuda")
+    layer = vp.RoutedLayer(x, y_dtype=torch.bfloat16)
+    ms_step, full_avg, full_med = measure(layer, steps, warmup)
+    modes = layer.modes.cpu().numpy()
+    counts = [int((modes == m).sum()) for m in range(3)]
+    assert counts[2] == n_full, "router did not produce the target FULL count"
+    N = S * P_TOKENS
+    fl = layer_flops(N, counts[2], counts[1], counts[0])
+    ff = flops_full(N, counts[2])
+    rec = dict(S=S, N=N, n_full=counts[2], n_surr=counts[1], n_mean=counts[0],
+               ms=round(ms_step, 4), tflops=round(fl / ms_step / 1e9, 2),
+               frac_bf16_peak=round(fl / ms_step / 1e9 / PEAK_BF16_TFLOPS, 4),
+               full_kernel_ms=round(full_avg, 4),
+               full_kernel_tflops=round(ff / full_avg / 1e9, 2) if ff else None,
+               full_kernel_frac=round(ff / full_avg / 1e9 / PEAK_BF16_TFLOPS, 4) if ff else None)
+    return rec, layer, x
+
+
+def cpu_baseline(x, rows_per_head=64):
+    """The fp64 oracle on a bounded sample of the same layer: the router over
+    all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
+    extrapolated linearly to all N rows (every row costs the same)."""
+    import numpy as np
+    import oracle
+    from paper_2609_23733_amd import synth
+    Q, K, V = oracle.as_f32(x.Q), oracle.as_f32(x.K), oracle.as_f32(x.V)
+    N = Q.shape[0]
+    t0 = time.perf_counter()
+    qp = oracle.router_pool(Q, x.W, x.U, x.w)
+    s, C, mean = oracle.router_route(K, V, qp)
+    lg = oracle.router_logits(x.u, x.Wr, x.br)
+    modes = oracle.assign(lg, oracle.RULE_ARGMAX)
+    t_router = time.perf_counter() - t0
+    rows = synth.sample_rows(N, rows_per_head, synth.derive_seed(500, 0, 20))
+    t_rows = 0.0
+    for h in range(Q.shape[1]):
+        t1 = time.perf_counter()
+        if modes[h] == 2:
+            oracle.full_rows(Q, K, V, h, rows)
+        elif modes[h] == 1:
+            oracle.surr_rows(V, C[h], x.surr, h, rows)
+        t_rows += time.perf_counter() - t1
+    total = t_router + t_rows * N / len(rows)
+    return dict(value=round(total * 1e3, 1), unit="ms", cores=oracle.threads_used(),
+                kind="oracle",
+                sample="router over all %d tokens (%.1f s) + %d sampled query rows per FULL and "
+                       "SURR head (%.1f s), extrapolated to %d rows; MEAN heads free"
+                       % (N, t_router, len(rows), t_rows, N),
+                measured_s=round(t_router + t_rows, 1))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--n-full", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    torch.cuda.set_device(0)
+    from paper_2609_23733_amd import vp
+    vp.load_library()
+
+    head, layer, x = run_workload(100, args.n_full, args.steps, args.warmup, (100, 0))
+    by = [head]
+    if not args.no_sweep:
+        del layer
+        for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16)):
+            r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 0))
+            by.append(r)
+            del lyr
+        torch.cuda.empty_cache()
+        ref16 = [r for r in by if r["S"] == 100 and r["n_full"] == 16]
+        if ref16:
+            for r in by:
+                if r["S"] == 100:
+                    r["speedup_vs_all_full"] = round(ref16[0]["ms"] / r["ms"], 3)
+                    r["ideal_speedup"] = round(16.0 / max(r["n_full"], 1), 3)
+
+    ff = flops_full(head["N"], head["n_full"])
+    achieved = ff / head["full_kernel_ms"] / 1e9
+    out = {
+        "metric": METRIC,
+        "value": head["ms"],
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms"],
+        "higher_is_better": False,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded iid N(0,1/64) Q/K/V, seeded router and surrogate weights)",
+        "config": {"workload": "S=100 views x 1374 tokens (N=137400), 16 heads x 64, bf16 "
+                               "operands, fp32 accumulate, bf16 Y, %d of 16 heads FULL"
+                               % head["n_full"],
+                   "S": 100, "P": P_TOKENS, "N": head["N"], "heads": HEADS, "head_dim": D,
+                   "n_full": head["n_full"], "n_surr": head["n_surr"], "n_mean": head["n_mean"],
+                   "layout": "Q/K/V [S*P, 16, 64] row-major"},
+        "tflops": head["tflops"],
+        "frac_bf16_peak": head["frac_bf16_peak"],
+        "roofline": {"kernel": "k_flash_bf16", "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "algorithmic_flop_per_launch": ff,
+                     "avg_launch_ms": round(head["full_kernel_ms"], 4)},
+        "by_workload": by,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(x)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

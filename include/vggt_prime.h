@@ -1,0 +1,190 @@
+/*
+ * vggt_prime.h -- C ABI of libvggtprime.so: the routed global-attention layer
+ * of VGGT-Prime (a compute-adaptive mixture of heads) on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The layer (Algorithm 1, step 2 "compute routed attention"; Sections 4.1-4.3):
+ * for every attention head h with per-head Q_h, K_h, V_h in R^{N x d} over all
+ * N = S * P tokens of all views,
+ *   1. a router pools the queries with gated attention (Eq.1-2), lets the
+ *      pooled query attend to all keys (routing vector r_h) and scores the
+ *      head by its largest routing weight s_h = max r_h (Eq.3);
+ *   2. each head is assigned one computation mode (Eq.4):
+ *        FULL  (s_h >= tau_high): exact softmax attention over all tokens,
+ *        SURR  (tau_low < s_h < tau_high): learned surrogate, Eq.5-7,
+ *        MEAN  (s_h <= tau_low): broadcast of the mean value token;
+ *   3. the head outputs are concatenated (Algorithm 1, step 3).
+ *
+ * Conventions for every entry point:
+ *   - Tensor arguments are DEVICE pointers owned by the caller.  The library
+ *     never allocates, frees or synchronises; each call only enqueues work on
+ *     `stream` (a hipStream_t passed as void*; NULL = the default stream) and
+ *     returns.  Calls are stateless and re-entrant.
+ *   - Struct arguments (vp_shape, vp_router_weights, ...) are HOST memory,
+ *     read during the call only; the pointers inside them are device pointers.
+ *   - Arguments are validated on the host before anything is enqueued; on an
+ *     error nothing is enqueued and a VP_ERR_* code is returned.  A HIP
+ *     launch error after enqueueing returns VP_ERR_HIP; vp_last_error() then
+ *     gives the message (thread-local).
+ *   - Q, K, V, Y are [N, H, d] row-major (token-major; the d values of one
+ *     head of one token are contiguous).  Supported: 1 <= H <= 16, d = 64,
+ *     router/surrogate hidden size L = 64, dtype fp32 or bf16 (fp32
+ *     accumulation everywhere).
+ *   - Numeric anomalies never fail a call: a NaN routing score sends its head
+ *     to FULL and sets bit 0 of the flags word of `buckets`.
+ */
+#ifndef VGGT_PRIME_H
+#define VGGT_PRIME_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    VP_OK = 0,
+    VP_ERR_INVALID_ARG = 1,  /* null pointer, bad size, misaligned pointer, bad enum */
+    VP_ERR_UNSUPPORTED = 2,  /* valid but unsupported shape (d != 64, H > 16, L != 64) */
+    VP_ERR_WORKSPACE = 3,    /* workspace smaller than vp_workspace_bytes() */
+    VP_ERR_HIP = 4           /* a HIP runtime error while enqueueing */
+} vp_status;
+
+typedef enum { VP_F32 = 0, VP_BF16 = 1 } vp_dtype;
+
+/* Computation modes, ordered by cost (Eq.4). */
+enum { VP_MODE_MEAN = 0, VP_MODE_SURR = 1, VP_MODE_FULL = 2, VP_NUM_MODES = 3 };
+
+typedef enum {
+    VP_ASSIGN_THRESHOLD = 0, /* Eq.4 on the saliency scores s_h */
+    VP_ASSIGN_ARGMAX = 1     /* first argmax over the three per-head logits */
+} vp_assign_rule;
+
+typedef enum { VP_ACT_GELU_ERF = 0, VP_ACT_RELU = 1 } vp_act;
+
+#define VP_MAX_HEADS 16
+#define VP_HEAD_DIM 64
+#define VP_HIDDEN 64
+/* Size in int32 of the `buckets` array: counts[3], head list[16], flags[1]. */
+#define VP_BUCKETS_LEN (VP_NUM_MODES + VP_MAX_HEADS + 1)
+#define VP_FLAG_NAN_SCORE 1u
+
+/* N = S * P tokens: S views of P tokens each (all views attend jointly). */
+typedef struct {
+    int64_t S, P;
+    int32_t H, d;
+    vp_dtype dtype; /* storage type of Q, K, V and of every weight matrix */
+} vp_shape;
+
+/* Gated attention pooling parameters (Eq.1): W, U are [H, L, d], w is [H, L],
+ * all in shape.dtype; no biases.  `scale` multiplies q_pool . k in the
+ * single-query attention (1/sqrt(d) when 0 is passed). */
+typedef struct {
+    const void *W, *U, *w;
+    int32_t L;
+    float scale;
+} vp_router_weights;
+
+/* Router outputs, device fp32, written by vp_router_score:
+ *   q_pool [H, d]  pooled query (Eq.2)
+ *   stats  [H, 2]  (m_h, l_h): m_h = max_j t_{h,j}, l_h = sum_j exp(t_{h,j} - m_h),
+ *                  t_{h,j} = scale * q_pool_h . k_{h,j}
+ *   score  [H]     s_h = max_j r_h(j) = 1 / l_h (Eq.3)
+ *   ctx    [H, d]  C_h = r_h V_h (Eq.5)
+ *   vmean  [H, d]  (1/N) sum_j v_{h,j} (Algorithm 1, mean branch) */
+typedef struct {
+    float *q_pool, *stats, *score, *ctx, *vmean;
+} vp_router_state;
+
+/* Surrogate MLPs (Eq.6), per head: Linear(2d -> L) -> act -> Linear(L -> d)
+ * acting on z = [v_{h,i}; C_h].  *_w1 [H, L, 2d] and *_w2 [H, d, L] in
+ * shape.dtype; biases *_b1 [H, L], *_b2 [H, d] fp32.  g_* is the gate MLP
+ * (gamma = sigmoid(MLP_gamma(z))), d_* the correction MLP (delta). */
+typedef struct {
+    const void *g_w1, *g_w2, *d_w1, *d_w2;
+    const float *g_b1, *g_b2, *d_b1, *d_b2;
+    int32_t L;
+    vp_act act;
+} vp_surrogate_weights;
+
+/* Bytes of device workspace that vp_router_score and
+ * vp_routed_global_attention need for `shape` (0 if the shape is invalid).
+ * The workspace holds router partial sums and the gathered values of FULL
+ * heads; it must be 256-byte aligned and may be reused across calls on one
+ * stream (calls on different streams need separate workspaces). */
+size_t vp_workspace_bytes(const vp_shape *shape);
+
+/* Router (Section 4.1, Eq.1-3; context Eq.5; value mean, Algorithm 1).
+ * Reads Q, K, V once each (HBM-bound); writes every field of `out`.
+ * Deterministic: partial sums are combined in a fixed order. */
+vp_status vp_router_score(const vp_shape *shape, const void *Q, const void *K, const void *V,
+                          const vp_router_weights *rw, vp_router_state *out, void *ws,
+                          size_t ws_bytes, void *stream);
+
+/* Linear-logit mode router of the synthetic workloads (not a construct of the
+ * paper): logits[r] = sum_c W_r[r, c] * u[c] + b_r[r] for r = h * 3 + m,
+ * m in (MEAN, SURR, FULL).  u: fp32 [Din]; W_r: [H * 3, Din] in w_dtype;
+ * b_r: fp32 [H * 3]; logits: fp32 [H, 3].  1 <= Din <= 65536. */
+vp_status vp_router_logits(const float *u, const void *W_r, const float *b_r, int32_t H,
+                           int32_t Din, vp_dtype w_dtype, float *logits, void *stream);
+
+/* Mode assignment (Eq.4).  THRESHOLD: scores = s_h [H]; FULL if s >= tau_high,
+ * MEAN if s <= tau_low, SURR otherwise (0 <= tau_low <= tau_high).  ARGMAX:
+ * scores = logits [H, 3]; the first maximal mode.  NaN -> FULL + flag.
+ * Writes modes [H] (uint8) and buckets [VP_BUCKETS_LEN] (int32):
+ *   buckets[0..2]   number of heads in MEAN, SURR, FULL;
+ *   buckets[3..3+H) head ids grouped by mode (MEAN, then SURR, then FULL),
+ *                   ascending within a group;
+ *   buckets[3+16]   flags (bit 0: a NaN score was seen). */
+vp_status vp_assign_heads(const float *scores, int32_t H, vp_assign_rule rule, float tau_low,
+                          float tau_high, uint8_t *modes, int32_t *buckets, void *stream);
+
+/* Routed global attention (Algorithm 1 step 2, Eq.5-7): writes Y [N, H, d] in
+ * y_dtype, every head in the mode vp_assign_heads gave it.  `modes` [H] and
+ * `buckets` are the device outputs of vp_assign_heads for the same call: the
+ * MEAN and SURR kernels read modes[h], the FULL kernels take the FULL head
+ * list from buckets; nothing is copied back to the host.
+ *   FULL heads: softmax(Q_h K_h^T / sqrt(d)) V_h over all N tokens;
+ *   SURR heads: C_h + gamma (.) delta with C_h = state->ctx (Eq.5-7);
+ *   MEAN heads: every row = state->vmean[h].
+ * `state` must hold the vp_router_score outputs for the same Q, K, V.
+ * `surr` must be non-NULL (its weights are read only for SURR heads).
+ * Every output element is written exactly once. */
+vp_status vp_routed_global_attention(const vp_shape *shape, const void *Q, const void *K,
+                                     const void *V, const uint8_t *modes,
+                                     const int32_t *buckets, const vp_router_state *state,
+                                     const vp_surrogate_weights *surr, void *Y,
+                                     vp_dtype y_dtype, void *ws, size_t ws_bytes,
+                                     void *stream);
+
+/* The three stages of vp_routed_global_attention, in the order it runs them,
+ * for callers that schedule or time them separately (same arguments and
+ * requirements as vp_routed_global_attention; run all three, in this order,
+ * on one stream, to obtain the same Y).
+ *   vp_gather_full_heads:   packs V of each FULL head (bf16 layers; no-op for
+ *                           fp32) into the workspace, tile-transposed;
+ *   vp_full_head_attention: exact softmax attention of every FULL head
+ *                           (Algorithm 1, first branch); reads the packed
+ *                           values the gather left in `ws`;
+ *   vp_linear_heads:        SURR (Eq.5-7) and MEAN heads. */
+vp_status vp_gather_full_heads(const vp_shape *shape, const void *V, const int32_t *buckets,
+                               void *ws, size_t ws_bytes, void *stream);
+vp_status vp_full_head_attention(const vp_shape *shape, const void *Q, const void *K,
+                                 const void *V, const int32_t *buckets, void *Y,
+                                 vp_dtype y_dtype, void *ws, size_t ws_bytes, void *stream);
+vp_status vp_linear_heads(const vp_shape *shape, const void *V, const uint8_t *modes,
+                          const vp_router_state *state, const vp_surrogate_weights *surr,
+                          void *Y, vp_dtype y_dtype, void *stream);
+
+/* Static description of a status code. */
+const char *vp_status_string(vp_status s);
+
+/* Message of the last VP_ERR_HIP on the calling thread ("" if none). */
+const char *vp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VGGT_PRIME_H */

@@ -79,12 +79,24 @@ def as_f32(x) -> np.ndarray:
     return np.ascontiguousarray(x, dtype=np.float32)
 
 
+def default_threads() -> int:
+    """Oracle worker threads: VP_ORACLE_THREADS, else min(16, CPU count)."""
+    env = os.environ.get("VP_ORACLE_THREADS")
+    if env:
+        return max(1, int(env))
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _nt(n):
+    return default_threads() if not n else int(n)
+
+
 def _p(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
 
 def threads_used(nthreads: int = 0) -> int:
-    return _load().or_threads_used(nthreads)
+    return _load().or_threads_used(_nt(nthreads))
 
 
 # ------------------------------------------------------------------ steps
@@ -98,7 +110,7 @@ def router_pool(Q, W, U, w, nthreads=0, want_weights=False):
     a = np.zeros((H, N), np.float64) if want_weights else None
     al = np.zeros((H, N), np.float64) if want_weights else None
     _load().or_router_pool(_p(Q), N, H, d, L, _p(W), _p(U), _p(w), _p(qp), _p(a), _p(al),
-                           nthreads)
+                           _nt(nthreads))
     return (qp, a, al) if want_weights else qp
 
 
@@ -115,7 +127,7 @@ def router_route(K, V, q_pool, scale=None, nthreads=0, want_r=False):
     mean = np.zeros((H, d), np.float64)
     r = np.zeros((H, N), np.float64) if want_r else None
     _load().or_router_route(_p(K), _p(V), N, H, d, _p(qp), float(scale), _p(r), _p(s), _p(C),
-                            _p(mean), nthreads)
+                            _p(mean), _nt(nthreads))
     return (s, C, mean, r) if want_r else (s, C, mean)
 
 
@@ -159,7 +171,7 @@ def full_rows(Q, K, V, h, rows=None, scale=None, nthreads=0):
         nr, rp = rows.shape[0], rows
     Y = np.zeros((nr, d), np.float64)
     _load().or_full_rows(_p(Q), _p(K), _p(V), N, H, d, int(h), _p(rp), nr, float(scale), _p(Y),
-                         nthreads)
+                         _nt(nthreads))
     return Y
 
 
@@ -180,7 +192,7 @@ def surr_rows(V, C_h, surr, h, rows=None, act=ACT_GELU, nthreads=0):
     _load().or_surr_rows(_p(V), N, H, d, int(h), L, int(act), _p(C_h), _p(wt["g_w1"]),
                          _p(wt["g_b1"]), _p(wt["g_w2"]), _p(wt["g_b2"]), _p(wt["d_w1"]),
                          _p(wt["d_b1"]), _p(wt["d_w2"]), _p(wt["d_b2"]), _p(rp), nr, _p(Y),
-                         nthreads)
+                         _nt(nthreads))
     return Y
 
 

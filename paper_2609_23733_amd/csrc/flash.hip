@@ -1,0 +1,434 @@
+// FULL-mode heads (Algorithm 1, first branch): exact softmax attention of a
+// head's queries over all N = S * P keys of all views, Y_h =
+// softmax(Q_h K_h^T / sqrt(d)) V_h, on MFMA with an online softmax over
+// 64-key tiles that are double-buffered through LDS.
+//
+// Work is taken from the FULL bucket that the mode assignment wrote on the
+// device: a grid sized for every head exits early past n_full * q_tiles, so
+// no mode is ever copied to the host.
+#include "vp_device.hpp"
+#include "vp_internal.hpp"
+
+namespace vp {
+
+constexpr int kBK = 64;       // keys per tile
+
+// Number of FULL heads in the bucket array written by the mode assignment,
+// 0 if the counts are inconsistent with H (never index past the head list).
+__device__ __forceinline__ int full_count(const int32_t* buckets, int H) {
+    const int c0 = buckets[0], c1 = buckets[1], c2 = buckets[2];
+    if (c0 < 0 || c1 < 0 || c2 < 0 || c0 + c1 + c2 != H) return 0;
+    return c2;
+}
+
+// Head id of FULL slot `slot` (< full_count), or -1 if out of range.
+__device__ __forceinline__ int full_head(const int32_t* buckets, int H, int slot) {
+    const int h = buckets[3 + buckets[0] + buckets[1] + slot];
+    return (h >= 0 && h < H) ? h : -1;
+}
+constexpr int kLdsRow = 72;   // bf16 LDS row stride (144 B: 16-B aligned, bank-staggered)
+
+// ------------------------------------------------------------------------
+// K5: bucket gather.  For each FULL head (slot s of the FULL bucket), copy V_h
+// into a packed, tile-transposed buffer Vt[s][tile][d][64 keys] (keys past N
+// are zero).  The attention kernel then reads V^T tiles as contiguous 8 KB
+// blocks whose rows feed the PV MFMA operand directly.
+// ------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ V,
+                                                   const int32_t* __restrict__ buckets, int64_t N,
+                                                   int H, int nkt, bf16* __restrict__ Vt) {
+    const int slot = blockIdx.y, tile = blockIdx.x;
+    const int nfull = full_count(buckets, H);
+    if (slot >= nfull) return;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    __shared__ __attribute__((aligned(16))) bf16 s[kD * kLdsRow];
+    const int t = threadIdx.x;
+    const int key = t >> 2, dseg = (t & 3) * 16;
+    const int64_t row = (int64_t)tile * kBK + key;
+    const bool ok = row < N;
+    const bf16* src = V + ((ok ? row : 0) * H + h) * kD + dseg;
+    bf16x8 a = load_bf16x8(src), b = load_bf16x8(src + 8);
+    if (!ok) a = b = zero_bf16x8();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        s[(dseg + j) * kLdsRow + key] = a[j];
+        s[(dseg + 8 + j) * kLdsRow + key] = b[j];
+    }
+    __syncthreads();
+    const int d = t >> 2, kseg = (t & 3) * 16;
+    bf16* dst = Vt + (((int64_t)slot * nkt + tile) * kD + d) * kBK + kseg;
+    *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(&s[d * kLdsRow + kseg]);
+    *reinterpret_cast<bf16x8*>(dst + 8) =
+        *reinterpret_cast<const bf16x8*>(&s[d * kLdsRow + kseg + 8]);
+}
+
+// ------------------------------------------------------------------------
+// K6 (bf16): one workgroup = 4 waves x 64 queries of one FULL head.
+// Per 64-key tile and wave:  S^T = K Q^T  (keys x queries, 2 x 2 blocks of
+// 32x32, 16 MFMAs), online softmax in registers, O^T += V^T P^T (d x queries,
+// 16 MFMAs).  Each lane owns one query column of every block, so softmax row
+// statistics stay in the lane plus one exchange with lane ^ 32.  K rows are
+// stored in LDS with index bits 2 and 3 swapped so that the S^T registers
+// hold eight consecutive keys per lane-half: they become the B operand of the
+// PV MFMA without any data movement.
+// ------------------------------------------------------------------------
+constexpr int kBQ16 = 256;
+
+__global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ Q,
+                                                       const bf16* __restrict__ K,
+                                                       const bf16* __restrict__ Vt,
+                                                       const int32_t* __restrict__ buckets,
+                                                       int64_t N, int H, int nqt, int nkt, float c,
+                                                       void* __restrict__ Y, int ydt) {
+    const int nfull = full_count(buckets, H);
+    const int active = nfull * nqt;
+    if ((int)blockIdx.x >= active) return;
+    const int L = xcd_remap(blockIdx.x, active);
+    const int slot = L / nqt, qt = L - slot * nqt;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+
+    __shared__ __attribute__((aligned(16))) bf16 sK[2][kBK * kLdsRow];
+    __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kLdsRow];
+
+    // Q^T operands of this wave's two 32-query blocks, kept in registers.
+    bf16x8 Qop[2][4];
+    int64_t qidx[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int64_t qi = (int64_t)qt * kBQ16 + wave * 64 + qb * 32 + n;
+        qidx[qb] = qi;
+        const bool ok = qi < N;
+        const bf16* qp = Q + ((ok ? qi : 0) * H + h) * kD + 8 * hh;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            Qop[qb][ks] = load_bf16x8(qp + 16 * ks);
+            if (!ok) Qop[qb][ks] = zero_bf16x8();
+        }
+    }
+
+    // Global -> LDS copy assignment: 64 rows x 4 segments of 16 elements.
+    const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
+    const bf16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
+    bf16x8 pk0, pk1, pv0, pv1;
+    auto gload = [&](int t) {
+        const int64_t key = (int64_t)t * kBK + lr;
+        const bool ok = key < N;
+        const bf16* kp = K + ((ok ? key : 0) * H + h) * kD + lc;
+        pk0 = load_bf16x8(kp);
+        pk1 = load_bf16x8(kp + 8);
+        if (!ok) pk0 = pk1 = zero_bf16x8();
+        const bf16* vp = Vth + ((int64_t)t * kD + lr) * kBK + lc;
+        pv0 = load_bf16x8(vp);
+        pv1 = load_bf16x8(vp + 8);
+    };
+    auto lstore = [&](int buf) {
+        bf16* kd = &sK[buf][swap23(lr) * kLdsRow + lc];
+        *reinterpret_cast<bf16x8*>(kd) = pk0;
+        *reinterpret_cast<bf16x8*>(kd + 8) = pk1;
+        bf16* vd = &sV[buf][lr * kLdsRow + lc];
+        *reinterpret_cast<bf16x8*>(vd) = pv0;
+        *reinterpret_cast<bf16x8*>(vd + 8) = pv1;
+    };
+
+    f32x16 O[2][2];
+    float m[2], l[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        O[qb][0] = O[qb][1] = zero_f32x16();
+        m[qb] = -INFINITY;
+        l[qb] = 0.f;
+    }
+
+    gload(0);
+    lstore(0);
+    __syncthreads();
+
+    for (int t = 0; t < nkt; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < nkt) gload(t + 1);
+
+        // S^T = K Q^T
+        f32x16 S[2][2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) S[qb][0] = S[qb][1] = zero_f32x16();
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                    &sK[buf][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) S[qb][kb] = mfma_bf16(a, Qop[qb][ks], S[qb][kb]);
+            }
+
+        if ((int64_t)(t + 1) * kBK > N) {   // ragged last tile: mask keys >= N
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t key =
+                        (int64_t)t * kBK + kb * 32 + 16 * (r >> 3) + 8 * hh + (r & 7);
+                    if (key >= N) {
+                        S[0][kb][r] = -INFINITY;
+                        S[1][kb][r] = -INFINITY;
+                    }
+                }
+        }
+
+        // Online softmax (base 2; c = log2(e) / sqrt(d)), P packed to bf16.
+        bf16x8 P[2][2][2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[qb][kb][r]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float mn = fmaxf(m[qb], mx * c);
+            const float al = exp2f_fast(m[qb] - mn);
+            m[qb] = mn;
+            l[qb] *= al;
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) O[qb][db][r] *= al;
+            float ls = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const float p = exp2f_fast(fmaf(S[qb][kb][r], c, -mn));
+                    S[qb][kb][r] = p;
+                    ls += p;
+                }
+            l[qb] += ls;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+                    P[qb][kb][b] = pack_bf16x8(S[qb][kb][8 * b], S[qb][kb][8 * b + 1],
+                                               S[qb][kb][8 * b + 2], S[qb][kb][8 * b + 3],
+                                               S[qb][kb][8 * b + 4], S[qb][kb][8 * b + 5],
+                                               S[qb][kb][8 * b + 6], S[qb][kb][8 * b + 7]);
+        }
+
+        // O^T += V^T P^T
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                        &sV[buf][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
+#pragma unroll
+                    for (int qb = 0; qb < 2; ++qb) O[qb][db] = mfma_bf16(a, P[qb][kb][b], O[qb][db]);
+                }
+
+        if (t + 1 < nkt) lstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    // Y[q, h, d] = O / l; lane holds d = 32 db + 8 g + 4 hh + i for i = 0..3.
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float lt = l[qb] + __shfl_xor(l[qb], 32);
+        const float inv = 1.f / lt;
+        const int64_t qi = qidx[qb];
+        if (qi < N) {
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int64_t off = (qi * H + h) * kD + db * 32 + 8 * g + 4 * hh;
+                    const float y0 = O[qb][db][4 * g] * inv, y1 = O[qb][db][4 * g + 1] * inv;
+                    const float y2 = O[qb][db][4 * g + 2] * inv, y3 = O[qb][db][4 * g + 3] * inv;
+                    if (ydt == DT_BF16) {
+                        bf16x4 v;
+                        v[0] = (bf16)y0; v[1] = (bf16)y1; v[2] = (bf16)y2; v[3] = (bf16)y3;
+                        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + off) = v;
+                    } else {
+                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off) =
+                            make_float4(y0, y1, y2, y3);
+                    }
+                }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------
+// K6 (fp32): one workgroup = 4 waves x 32 queries; 32x32x2 fp32 MFMA.  S^T
+// output register r of lane-half hh holds key 8 (r / 4) + 4 hh + (r % 4) of
+// its 32-key block; the PV MFMA consumes one register per step, reading the
+// matching V row from LDS.
+// ------------------------------------------------------------------------
+constexpr int kBQ32 = 128;
+constexpr int kKRow32 = 65;   // odd stride: column reads are bank-conflict free
+
+__global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ Q,
+                                                      const float* __restrict__ K,
+                                                      const float* __restrict__ V,
+                                                      const int32_t* __restrict__ buckets,
+                                                      int64_t N, int H, int nqt, int nkt, float c,
+                                                      void* __restrict__ Y, int ydt) {
+    const int nfull = full_count(buckets, H);
+    const int active = nfull * nqt;
+    if ((int)blockIdx.x >= active) return;
+    const int L = xcd_remap(blockIdx.x, active);
+    const int slot = L / nqt, qt = L - slot * nqt;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+
+    __shared__ float sK[2][kBK * kKRow32];
+    __shared__ __attribute__((aligned(16))) float sV[2][kBK * kD];
+
+    const int64_t qi = (int64_t)qt * kBQ32 + wave * 32 + n;
+    const bool qok = qi < N;
+    float Qf[32];
+    {
+        const float* qp = Q + ((qok ? qi : 0) * H + h) * kD + hh;
+#pragma unroll
+        for (int ks = 0; ks < 32; ++ks) Qf[ks] = qok ? qp[2 * ks] : 0.f;
+    }
+
+    const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
+    float4 pk[4], pv[4];
+    auto gload = [&](int t) {
+        const int64_t key = (int64_t)t * kBK + lr;
+        const bool ok = key < N;
+        const float4* kp = reinterpret_cast<const float4*>(K + ((ok ? key : 0) * H + h) * kD + lc);
+        const float4* vp = reinterpret_cast<const float4*>(V + ((ok ? key : 0) * H + h) * kD + lc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            pk[i] = kp[i];
+            pv[i] = vp[i];
+            if (!ok) {   // component-wise: a whole-float4 select here crashes hipcc 7.2
+                pk[i].x = 0.f; pk[i].y = 0.f; pk[i].z = 0.f; pk[i].w = 0.f;
+                pv[i].x = 0.f; pv[i].y = 0.f; pv[i].z = 0.f; pv[i].w = 0.f;
+            }
+        }
+    };
+    auto lstore = [&](int buf) {
+        float* kd = &sK[buf][lr * kKRow32 + lc];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            kd[4 * i] = pk[i].x; kd[4 * i + 1] = pk[i].y;
+            kd[4 * i + 2] = pk[i].z; kd[4 * i + 3] = pk[i].w;
+            *reinterpret_cast<float4*>(&sV[buf][lr * kD + lc + 4 * i]) = pv[i];
+        }
+    };
+
+    f32x16 O[2] = {zero_f32x16(), zero_f32x16()};
+    float m = -INFINITY, l = 0.f;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+
+    for (int t = 0; t < nkt; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < nkt) gload(t + 1);
+        f32x16 S[2] = {zero_f32x16(), zero_f32x16()};
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < 32; ++ks)
+                S[kb] = mfma_f32(sK[buf][(kb * 32 + n) * kKRow32 + 2 * ks + hh], Qf[ks], S[kb]);
+        if ((int64_t)(t + 1) * kBK > N) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t key = (int64_t)t * kBK + kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                    if (key >= N) S[kb][r] = -INFINITY;
+                }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[kb][r]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mn = fmaxf(m, mx * c);
+        const float al = exp2f_fast(m - mn);
+        m = mn;
+        l *= al;
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) O[db][r] *= al;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const float p = exp2f_fast(fmaf(S[kb][r], c, -mn));
+                S[kb][r] = p;
+                l += p;
+            }
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+                    O[db] = mfma_f32(sV[buf][key * kD + db * 32 + n], S[kb][r], O[db]);
+                }
+        if (t + 1 < nkt) lstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    const float lt = l + __shfl_xor(l, 32);
+    const float inv = 1.f / lt;
+    if (qok) {
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int64_t off = (qi * H + h) * kD + db * 32 + 8 * g + 4 * hh;
+                const float y0 = O[db][4 * g] * inv, y1 = O[db][4 * g + 1] * inv;
+                const float y2 = O[db][4 * g + 2] * inv, y3 = O[db][4 * g + 3] * inv;
+                if (ydt == DT_BF16) {
+                    bf16x4 v;
+                    v[0] = (bf16)y0; v[1] = (bf16)y1; v[2] = (bf16)y2; v[3] = (bf16)y3;
+                    *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + off) = v;
+                } else {
+                    *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off) =
+                        make_float4(y0, y1, y2, y3);
+                }
+            }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+
+int flash_q_tile(int dtype) { return dtype == DT_BF16 ? kBQ16 : kBQ32; }
+
+void launch_gather(const AttnArgs& a, hipStream_t st) {
+    const int nkt = (int)((a.N + kBK - 1) / kBK);
+    hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.V,
+                       a.buckets, a.N, a.H, nkt, (bf16*)a.vt);
+}
+
+void launch_flash(const AttnArgs& a, hipStream_t st) {
+    const int nkt = (int)((a.N + kBK - 1) / kBK);
+    const float c = kLog2e / sqrtf((float)kD);
+    const int bq = flash_q_tile(a.dtype);
+    const int nqt = (int)((a.N + bq - 1) / bq);
+    if (a.dtype == DT_BF16)
+        hipLaunchKernelGGL(k_flash_bf16, dim3(nqt * a.H), dim3(256), 0, st, (const bf16*)a.Q,
+                           (const bf16*)a.K, (const bf16*)a.vt, a.buckets, a.N, a.H, nqt, nkt, c,
+                           a.Y, a.ydt);
+    else
+        hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
+                           (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,
+                           c, a.Y, a.ydt);
+}
+
+}  // namespace vp

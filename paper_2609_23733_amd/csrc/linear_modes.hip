@@ -1,0 +1,284 @@
+// The two linear-cost modes of the routed layer:
+//   SURR (Section 4.3, Eq.5-7): y_i = C_h + gamma_i (.) delta_i with
+//        gamma_i = sigmoid(MLP_gamma([v_i; C_h])), delta_i = MLP_delta([v_i; C_h]);
+//   MEAN (Algorithm 1, third branch): y_i = (1/N) sum_j v_j for every token.
+// Each kernel runs over (token block, head) and exits unless modes[h] is its
+// mode.
+//
+// The first MLP layer splits z = [v; C] into W1 = [W1_v | W1_C]: the context
+// half W1_C C_h + b1 is the same for every token of a head and is computed
+// once per workgroup, leaving a 64 x 64 product per token.
+#include "vp_device.hpp"
+#include "vp_internal.hpp"
+
+namespace vp {
+
+__device__ __forceinline__ float act_fn(float x, int act) {
+    if (act == 1) return fmaxf(x, 0.f);
+    return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
+}
+
+__device__ __forceinline__ float sigmoid_fast(float x) {
+    return rcp_fast(1.f + exp2f_fast(-kLog2e * x));
+}
+
+constexpr int kSurrRows = 512;   // tokens per workgroup
+constexpr int kW = 72;           // bf16 LDS row stride
+
+// ------------------------------------------------------------------------
+// K7 (bf16): per wave and 32 tokens, H1^T = W1_v V^T (128 x 32: rows 0-63
+// gamma hidden, 64-127 delta hidden; 16 MFMAs), activation, then
+// G^T = W2_gamma H_gamma^T and D^T = W2_delta H_delta^T (64 x 32 each,
+// 8 MFMAs each).  W1 rows sit in LDS with index bits 2,3 swapped so that
+// hidden units arrive eight-consecutive per lane-half, the K order of the
+// second MFMA.
+// ------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_surrogate_bf16(
+    const bf16* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
+    const bf16* __restrict__ gw1, const float* __restrict__ gb1, const bf16* __restrict__ gw2,
+    const float* __restrict__ gb2, const bf16* __restrict__ dw1, const float* __restrict__ db1,
+    const bf16* __restrict__ dw2, const float* __restrict__ db2, int act, int64_t N, int H,
+    void* __restrict__ Y, int ydt) {
+    const int h = blockIdx.y;
+    if (modes[h] != MODE_SURR) return;
+    const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
+    const int64_t t1 = (t0 + kSurrRows < N) ? t0 + kSurrRows : N;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = lane & 31, hh = lane >> 5;
+
+    __shared__ __attribute__((aligned(16))) bf16 sW1[128 * kW];   // [hidden (permuted)][d]
+    __shared__ __attribute__((aligned(16))) bf16 sW2[2][64 * kW]; // [gamma|delta][d][hidden]
+    __shared__ __attribute__((aligned(16))) float sC[kD], sB2g[kD], sB2d[kD], sC1[128];
+
+    const float* C = ctx + h * kD;
+    if (tid < kD) {
+        sC[tid] = C[tid];
+        sB2g[tid] = gb2[h * kD + tid];
+        sB2d[tid] = db2[h * kD + tid];
+    }
+    // Context half of layer 1 plus bias: c1[u] = b1[u] + sum_c W1[u][64 + c] C[c].
+    if (tid < 128) {
+        const int u = tid & 63;
+        const bf16* w1 = (tid < 64 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD;
+        float acc = (tid < 64 ? gb1 : db1)[h * kL + u];
+        for (int cc = 0; cc < kD; ++cc) acc = fmaf(bf16_to_f32(w1[kD + cc]), C[cc], acc);
+        sC1[tid] = acc;
+    }
+    // W1_v rows (value half) into LDS, rows permuted within 32-blocks.
+    for (int i = tid; i < 128 * 8; i += 256) {
+        const int u = i >> 3, seg = (i & 7) * 8;
+        const bf16* w1 = (u < 64 ? gw1 : dw1) + ((int64_t)h * kL + (u & 63)) * 2 * kD + seg;
+        *reinterpret_cast<bf16x8*>(&sW1[swap23(u & 31) * kW + (u & ~31) * kW + seg]) =
+            load_bf16x8(w1);
+    }
+    for (int i = tid; i < 2 * 64 * 8; i += 256) {
+        const int which = i >> 9, r = (i >> 3) & 63, seg = (i & 7) * 8;
+        const bf16* w2 = (which == 0 ? gw2 : dw2) + ((int64_t)h * kD + r) * kL + seg;
+        *reinterpret_cast<bf16x8*>(&sW2[which][r * kW + seg]) = load_bf16x8(w2);
+    }
+    __syncthreads();
+
+    // c1 values this lane needs: hidden u = 32 mb + 16 (r / 8) + 8 hh + r % 8.
+    float c1[4][16];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) c1[mb][r] = sC1[32 * mb + 16 * (r >> 3) + 8 * hh + (r & 7)];
+
+    for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
+        const int64_t tok = tb + n;
+        const bool ok = tok < t1;
+        const bf16* vr = V + ((ok ? tok : t0) * H + h) * kD + 8 * hh;
+        bf16x8 B[4];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) B[ks] = load_bf16x8(vr + 16 * ks);
+        f32x16 A1[4];
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+            A1[mb] = zero_f32x16();
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const bf16x8 a =
+                    *reinterpret_cast<const bf16x8*>(&sW1[(32 * mb + n) * kW + 16 * ks + 8 * hh]);
+                A1[mb] = mfma_bf16(a, B[ks], A1[mb]);
+            }
+        }
+        bf16x8 Hop[2][4];   // [gamma|delta][k-step over hidden]
+#pragma unroll
+        for (int which = 0; which < 2; ++which)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const int mb = 2 * which + (ks >> 1), r0 = 8 * (ks & 1);
+                float hv[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) hv[j] = act_fn(A1[mb][r0 + j] + c1[mb][r0 + j], act);
+                Hop[which][ks] = pack_bf16x8(hv[0], hv[1], hv[2], hv[3], hv[4], hv[5], hv[6], hv[7]);
+            }
+        f32x16 G[2], D[2];
+#pragma unroll
+        for (int db = 0; db < 2; ++db) {
+            G[db] = zero_f32x16();
+            D[db] = zero_f32x16();
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const bf16x8 ag = *reinterpret_cast<const bf16x8*>(
+                    &sW2[0][(32 * db + n) * kW + 16 * ks + 8 * hh]);
+                const bf16x8 ad = *reinterpret_cast<const bf16x8*>(
+                    &sW2[1][(32 * db + n) * kW + 16 * ks + 8 * hh]);
+                G[db] = mfma_bf16(ag, Hop[0][ks], G[db]);
+                D[db] = mfma_bf16(ad, Hop[1][ks], D[db]);
+            }
+        }
+        if (ok) {
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int d0 = 32 * db + 8 * g + 4 * hh;
+                    float y[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int d = d0 + i;
+                        const float gam = sigmoid_fast(G[db][4 * g + i] + sB2g[d]);
+                        y[i] = sC[d] + gam * (D[db][4 * g + i] + sB2d[d]);
+                    }
+                    const int64_t off = (tok * H + h) * kD + d0;
+                    if (ydt == DT_BF16) {
+                        bf16x4 v;
+                        v[0] = (bf16)y[0]; v[1] = (bf16)y[1]; v[2] = (bf16)y[2]; v[3] = (bf16)y[3];
+                        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + off) = v;
+                    } else {
+                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off) =
+                            make_float4(y[0], y[1], y[2], y[3]);
+                    }
+                }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------
+// K7 (fp32): one token per thread, weights in LDS, plain FMAs in fp32.
+// ------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_surrogate_f32(
+    const float* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
+    const float* __restrict__ gw1, const float* __restrict__ gb1, const float* __restrict__ gw2,
+    const float* __restrict__ gb2, const float* __restrict__ dw1, const float* __restrict__ db1,
+    const float* __restrict__ dw2, const float* __restrict__ db2, int act, int64_t N, int H,
+    void* __restrict__ Y, int ydt) {
+    const int h = blockIdx.y;
+    if (modes[h] != MODE_SURR) return;
+    const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
+    const int64_t t1 = (t0 + kSurrRows < N) ? t0 + kSurrRows : N;
+    const int tid = threadIdx.x;
+    __shared__ float sW1v[2][kL][kD + 1];   // value half of layer 1, [gamma|delta][u][c]
+    __shared__ float sW2t[2][kL][kD];       // layer 2 transposed: [which][u][d]
+    __shared__ float sC1[2][kL], sC[kD], sB2[2][kD];
+    const float* C = ctx + h * kD;
+    for (int i = tid; i < 2 * kL * kD; i += 256) {
+        const int which = i / (kL * kD), u = (i / kD) % kL, cc = i % kD;
+        const float* w1 = (which == 0 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD;
+        sW1v[which][u][cc] = w1[cc];
+        const float* w2 = (which == 0 ? gw2 : dw2) + (int64_t)h * kD * kL;
+        // sW2t[which][u][d] = W2[d][u]; here (u, cc) runs over (hidden, d)
+        sW2t[which][u][cc] = w2[(int64_t)cc * kL + u];
+    }
+    if (tid < 128) {
+        const int which = tid >> 6, u = tid & 63;
+        const float* w1 = (which == 0 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD;
+        float acc = (which == 0 ? gb1 : db1)[h * kL + u];
+        for (int cc = 0; cc < kD; ++cc) acc = fmaf(w1[kD + cc], C[cc], acc);
+        sC1[which][u] = acc;
+    }
+    if (tid < kD) {
+        sC[tid] = C[tid];
+        sB2[0][tid] = gb2[h * kD + tid];
+        sB2[1][tid] = db2[h * kD + tid];
+    }
+    __syncthreads();
+    for (int64_t tok = t0 + tid; tok < t1; tok += 256) {
+        float v[kD], og[kD], od[kD];
+        const float* vr = V + (tok * H + h) * kD;
+#pragma unroll
+        for (int k = 0; k < kD; ++k) {
+            v[k] = vr[k];
+            og[k] = sB2[0][k];
+            od[k] = sB2[1][k];
+        }
+        for (int u = 0; u < kL; ++u) {
+            float ag = sC1[0][u], ad = sC1[1][u];
+#pragma unroll
+            for (int k = 0; k < kD; ++k) {
+                ag = fmaf(sW1v[0][u][k], v[k], ag);
+                ad = fmaf(sW1v[1][u][k], v[k], ad);
+            }
+            const float hg = act_fn(ag, act), hd = act_fn(ad, act);
+#pragma unroll
+            for (int k = 0; k < kD; ++k) {
+                og[k] = fmaf(sW2t[0][u][k], hg, og[k]);
+                od[k] = fmaf(sW2t[1][u][k], hd, od[k]);
+            }
+        }
+        const int64_t off = (tok * H + h) * kD;
+#pragma unroll
+        for (int k = 0; k < kD; ++k) {
+            const float y = sC[k] + sigmoid_fast(og[k]) * od[k];
+            if (ydt == DT_BF16)
+                reinterpret_cast<bf16*>(Y)[off + k] = (bf16)y;
+            else
+                reinterpret_cast<float*>(Y)[off + k] = y;
+        }
+    }
+}
+
+// ------------------------------------------------------------------------
+// K8: MEAN heads, a write-only stream of the head's value mean.
+// 8 lanes per row (8 values each); a workgroup covers 32 rows per step.
+// ------------------------------------------------------------------------
+constexpr int kMeanRows = 1024;
+
+__global__ __launch_bounds__(256) void k_mean_heads(const uint8_t* __restrict__ modes,
+                                                    const float* __restrict__ vmean, int64_t N,
+                                                    int H, void* __restrict__ Y, int ydt) {
+    const int h = blockIdx.y;
+    if (modes[h] != MODE_MEAN) return;
+    const int64_t t0 = (int64_t)blockIdx.x * kMeanRows;
+    const int64_t t1 = (t0 + kMeanRows < N) ? t0 + kMeanRows : N;
+    const int seg = (threadIdx.x & 7) * 8, rr = threadIdx.x >> 3;
+    float mv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mv[j] = vmean[h * kD + seg + j];
+    if (ydt == DT_BF16) {
+        const bf16x8 v = pack_bf16x8(mv[0], mv[1], mv[2], mv[3], mv[4], mv[5], mv[6], mv[7]);
+        for (int64_t row = t0 + rr; row < t1; row += 32)
+            *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + (row * H + h) * kD + seg) = v;
+    } else {
+        const float4 a = make_float4(mv[0], mv[1], mv[2], mv[3]);
+        const float4 b = make_float4(mv[4], mv[5], mv[6], mv[7]);
+        for (int64_t row = t0 + rr; row < t1; row += 32) {
+            float4* p = reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + (row * H + h) * kD + seg);
+            p[0] = a;
+            p[1] = b;
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+
+void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
+    const unsigned nbs = (unsigned)((a.N + kSurrRows - 1) / kSurrRows);
+    if (a.dtype == DT_BF16)
+        hipLaunchKernelGGL(k_surrogate_bf16, dim3(nbs, a.H), dim3(256), 0, st, (const bf16*)a.V,
+                           a.modes, a.ctx, (const bf16*)a.g_w1, a.g_b1, (const bf16*)a.g_w2,
+                           a.g_b2, (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2,
+                           a.act, a.N, a.H, a.Y, a.ydt);
+    else
+        hipLaunchKernelGGL(k_surrogate_f32, dim3(nbs, a.H), dim3(256), 0, st, (const float*)a.V,
+                           a.modes, a.ctx, (const float*)a.g_w1, a.g_b1, (const float*)a.g_w2,
+                           a.g_b2, (const float*)a.d_w1, a.d_b1, (const float*)a.d_w2, a.d_b2,
+                           a.act, a.N, a.H, a.Y, a.ydt);
+    const unsigned nbm = (unsigned)((a.N + kMeanRows - 1) / kMeanRows);
+    hipLaunchKernelGGL(k_mean_heads, dim3(nbm, a.H), dim3(256), 0, st, a.modes, a.vmean, a.N,
+                       a.H, a.Y, a.ydt);
+}
+
+}  // namespace vp

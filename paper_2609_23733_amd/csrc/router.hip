@@ -1,0 +1,492 @@
+// Router of the routed global-attention layer (Section 4.1, Eq.1-3), the
+// context/mean reductions that reuse its routing weights (Eq.5; Algorithm 1
+// mean branch), the linear-logit mode router of the synthetic workloads and
+// the mode assignment (Eq.4).
+//
+// Every reduction over tokens is split into fixed token chunks whose partial
+// results are combined in chunk order by a second kernel: no float atomics,
+// so results are bitwise reproducible run to run.
+#include "vp_device.hpp"
+#include "vp_internal.hpp"
+
+namespace vp {
+
+// tanh(x) * sigmoid(y) = (1 - e^{-2x}) / ((1 + e^{-2x}) (1 + e^{-y})), with x
+// clamped to +-15 (tanh is +-1 to fp32 precision there) so that no inf/inf
+// arises.  Two exponentials and one reciprocal.
+__device__ __forceinline__ float tanh_times_sigmoid(float x, float y) {
+    x = fminf(fmaxf(x, -15.f), 15.f);
+    float e1 = exp2f_fast(-2.f * kLog2e * x);
+    float e2 = exp2f_fast(-kLog2e * y);
+    return (1.f - e1) * rcp_fast((1.f + e1) * (1.f + e2));
+}
+
+// ------------------------------------------------------------------------
+// K1: gated attention pooling, partial sums per (token chunk, head).
+// part1[c][h] = (m, l, acc[64]) with m = max_i a_i (log2 units: a * log2 e),
+// l = sum_i 2^(a_i - m), acc = sum_i 2^(a_i - m) q_i over the chunk's tokens.
+// ------------------------------------------------------------------------
+
+// bf16: per head, [W_h; U_h] (128 x 64) times Q_h^T (64 x 32 tokens) on MFMA.
+// The four 32-row blocks of A are W rows 0-31, W rows 32-63, U rows 0-31,
+// U rows 32-63, so W and U results for one hidden unit l land in the same
+// lane and register.
+__global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restrict__ Q,
+                                                           const bf16* __restrict__ W,
+                                                           const bf16* __restrict__ U,
+                                                           const bf16* __restrict__ w,
+                                                           int64_t N, int H, int64_t chunk,
+                                                           float* __restrict__ part) {
+    const int h = blockIdx.y, c = blockIdx.x;
+    const int64_t t0 = (int64_t)c * chunk;
+    const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+
+    bf16x8 Wop[2][4], Uop[2][4];
+    const bf16* Wh = W + (int64_t)h * kL * kD;
+    const bf16* Uh = U + (int64_t)h * kL * kD;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            Wop[mb][ks] = load_bf16x8(Wh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
+            Uop[mb][ks] = load_bf16x8(Uh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
+        }
+    float wv[2][16];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            wv[mb][r] = bf16_to_f32(w[(int64_t)h * kL + 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+
+    float m = -INFINITY, l = 0.f;
+    float acc[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) acc[i] = 0.f;
+
+    for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
+        const int64_t tok = tb + n;
+        const bool valid = tok < t1;
+        bf16x8 B[4];
+        // Tail lanes read a valid row (the chunk's first) and zero it afterwards.
+        const bf16* qrow = Q + ((valid ? tok : t0) * H + h) * kD;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            B[ks] = load_bf16x8(qrow + 16 * ks + 8 * hh);
+            if (!valid) B[ks] = zero_bf16x8();
+        }
+        f32x16 aW[2], aU[2];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            aW[mb] = zero_f32x16();
+            aU[mb] = zero_f32x16();
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                aW[mb] = mfma_bf16(Wop[mb][ks], B[ks], aW[mb]);
+                aU[mb] = mfma_bf16(Uop[mb][ks], B[ks], aU[mb]);
+            }
+        }
+        float pa = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) pa += wv[mb][r] * tanh_times_sigmoid(aW[mb][r], aU[mb][r]);
+        float a = (pa + __shfl_xor(pa, 32)) * kLog2e;
+        if (!valid) a = -INFINITY;
+        float bm = a;
+#pragma unroll
+        for (int o = 16; o >= 1; o >>= 1) bm = fmaxf(bm, __shfl_xor(bm, o));
+        const float mn = fmaxf(m, bm);
+        const float al = exp2f_fast(m - mn);
+        const float p = valid ? exp2f_fast(a - mn) : 0.f;
+        l = l * al + (hh == 0 ? p : 0.f);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[8 * ks + j] = acc[8 * ks + j] * al + p * bf16_to_f32(B[ks][j]);
+        m = mn;
+    }
+
+    // Combine lanes (same hh share a d set) and waves through LDS.
+    __shared__ float s_acc[4][64][33];
+    __shared__ float s_ml[4][2];
+    const float lw = wave_sum(l);
+#pragma unroll
+    for (int i = 0; i < 32; ++i) s_acc[wave][lane][i] = acc[i];
+    if (lane == 0) {
+        s_ml[wave][0] = m;
+        s_ml[wave][1] = lw;
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int d = threadIdx.x;
+        const int ks = d >> 4, dh = (d >> 3) & 1, j = d & 7;
+        float M = -INFINITY;
+        for (int wv2 = 0; wv2 < 4; ++wv2) M = fmaxf(M, s_ml[wv2][0]);
+        float L = 0.f, A = 0.f;
+        for (int wv2 = 0; wv2 < 4; ++wv2) {
+            const float mw = s_ml[wv2][0];
+            const float sc = (mw == -INFINITY) ? 0.f : exp2f_fast(mw - M);
+            L += s_ml[wv2][1] * sc;
+            float sa = 0.f;
+            for (int nn = 0; nn < 32; ++nn) sa += s_acc[wv2][32 * dh + nn][8 * ks + j];
+            A += sa * sc;
+        }
+        float* o = part + ((int64_t)c * H + h) * (2 + kD);
+        if (d == 0) {
+            o[0] = M;
+            o[1] = L;
+        }
+        o[2 + d] = A;
+    }
+}
+
+// fp32: one token per thread, weights in LDS, plain FMAs.
+__global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restrict__ Q,
+                                                          const float* __restrict__ W,
+                                                          const float* __restrict__ U,
+                                                          const float* __restrict__ w,
+                                                          int64_t N, int H, int64_t chunk,
+                                                          float* __restrict__ part) {
+    const int h = blockIdx.y, c = blockIdx.x;
+    const int64_t t0 = (int64_t)c * chunk;
+    const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
+    __shared__ float sW[kL * kD], sU[kL * kD], sw[kL];
+    __shared__ float s_red[4][2 + kD];
+    for (int i = threadIdx.x; i < kL * kD; i += 256) {
+        sW[i] = W[(int64_t)h * kL * kD + i];
+        sU[i] = U[(int64_t)h * kL * kD + i];
+    }
+    if (threadIdx.x < kL) sw[threadIdx.x] = w[(int64_t)h * kL + threadIdx.x];
+    __syncthreads();
+
+    float m = -INFINITY, l = 0.f;
+    float acc[kD];
+#pragma unroll
+    for (int k = 0; k < kD; ++k) acc[k] = 0.f;
+    for (int64_t tok = t0 + threadIdx.x; tok < t1; tok += 256) {
+        float q[kD];
+        const float4* qr = reinterpret_cast<const float4*>(Q + (tok * H + h) * kD);
+#pragma unroll
+        for (int k = 0; k < kD / 4; ++k) {
+            float4 v = qr[k];
+            q[4 * k] = v.x; q[4 * k + 1] = v.y; q[4 * k + 2] = v.z; q[4 * k + 3] = v.w;
+        }
+        float a = 0.f;
+        for (int li = 0; li < kL; ++li) {
+            float x = 0.f, y = 0.f;
+#pragma unroll
+            for (int k = 0; k < kD; ++k) {
+                x = fmaf(sW[li * kD + k], q[k], x);
+                y = fmaf(sU[li * kD + k], q[k], y);
+            }
+            a = fmaf(sw[li], tanh_times_sigmoid(x, y), a);
+        }
+        a *= kLog2e;
+        const float mn = fmaxf(m, a);
+        const float al = exp2f_fast(m - mn);
+        const float p = exp2f_fast(a - mn);
+        l = l * al + p;
+#pragma unroll
+        for (int k = 0; k < kD; ++k) acc[k] = acc[k] * al + p * q[k];
+        m = mn;
+    }
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const float M = wave_max(m);
+    const float sc = (m == -INFINITY) ? 0.f : exp2f_fast(m - M);
+    const float lw = wave_sum(l * sc);
+#pragma unroll
+    for (int k = 0; k < kD; ++k) {
+        const float v = wave_sum(acc[k] * sc);
+        if (lane == 0) s_red[wave][2 + k] = v;
+    }
+    if (lane == 0) {
+        s_red[wave][0] = M;
+        s_red[wave][1] = lw;
+    }
+    __syncthreads();
+    if (threadIdx.x < kD) {
+        const int d = threadIdx.x;
+        float MM = -INFINITY;
+        for (int wv = 0; wv < 4; ++wv) MM = fmaxf(MM, s_red[wv][0]);
+        float L = 0.f, A = 0.f;
+        for (int wv = 0; wv < 4; ++wv) {
+            const float mw = s_red[wv][0];
+            const float s2 = (mw == -INFINITY) ? 0.f : exp2f_fast(mw - MM);
+            L += s_red[wv][1] * s2;
+            A += s_red[wv][2 + d] * s2;
+        }
+        float* o = part + ((int64_t)c * H + h) * (2 + kD);
+        if (d == 0) {
+            o[0] = MM;
+            o[1] = L;
+        }
+        o[2 + d] = A;
+    }
+}
+
+// K9a: q_pool_h = (sum_c 2^(m_c - M) acc_c) / (sum_c 2^(m_c - M) l_c), chunks in order.
+__global__ __launch_bounds__(64) void k_pool_combine(const float* __restrict__ part, int nchunks,
+                                                     int H, float* __restrict__ q_pool) {
+    const int h = blockIdx.x, d = threadIdx.x;
+    float M = -INFINITY;
+    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, part[((int64_t)c * H + h) * (2 + kD)]);
+    float L = 0.f, A = 0.f;
+    for (int c = 0; c < nchunks; ++c) {
+        const float* p = part + ((int64_t)c * H + h) * (2 + kD);
+        const float sc = (p[0] == -INFINITY) ? 0.f : exp2f_fast(p[0] - M);
+        L += p[1] * sc;
+        A += p[2 + d] * sc;
+    }
+    q_pool[h * kD + d] = A / L;
+}
+
+// ------------------------------------------------------------------------
+// K2: single-query attention of q_pool over all keys, fused with the context
+// C_h = r_h V_h and the value sum, partial per token chunk, all heads.
+// part2[c][h] = (m, l, C[64], sumv[64]); m in log2 units of t = scale q.k.
+// Thread layout: 8 lanes per (token, head) row, each owning 8 of the 64
+// values; a workgroup streams whole token rows ([H, 64] contiguous).
+// ------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ Kp,
+                                                       const void* __restrict__ Vp,
+                                                       const float* __restrict__ q_pool,
+                                                       float scale, int64_t N, int H,
+                                                       int64_t chunk, float* __restrict__ part) {
+    const int c = blockIdx.x;
+    const int64_t t0 = (int64_t)c * chunk;
+    const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
+    const int tpr = H * 8;
+    const int rpi = 256 / tpr;
+    const int t = threadIdx.x;
+    const int rr = t / tpr, hs = t % tpr, h = hs >> 3, seg = hs & 7;
+    const bool active = rr < rpi;
+
+    float qp[8];
+    const float cs = scale * kLog2e;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) qp[j] = active ? q_pool[h * kD + seg * 8 + j] * cs : 0.f;
+    float m = -INFINITY, l = 0.f, C[8], sv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) C[j] = sv[j] = 0.f;
+
+    if (active) {
+        for (int64_t row = t0 + rr; row < t1; row += rpi) {
+            float kv[8], vv[8];
+            const int64_t off = (row * H + h) * kD + seg * 8;
+            if (DT == DT_BF16) {
+                bf16x8 k8 = load_bf16x8(reinterpret_cast<const bf16*>(Kp) + off);
+                bf16x8 v8 = load_bf16x8(reinterpret_cast<const bf16*>(Vp) + off);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    kv[j] = bf16_to_f32(k8[j]);
+                    vv[j] = bf16_to_f32(v8[j]);
+                }
+            } else {
+                const float4* kq = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(Kp) + off);
+                const float4* vq = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(Vp) + off);
+                float4 a0 = kq[0], a1 = kq[1], b0 = vq[0], b1 = vq[1];
+                kv[0] = a0.x; kv[1] = a0.y; kv[2] = a0.z; kv[3] = a0.w;
+                kv[4] = a1.x; kv[5] = a1.y; kv[6] = a1.z; kv[7] = a1.w;
+                vv[0] = b0.x; vv[1] = b0.y; vv[2] = b0.z; vv[3] = b0.w;
+                vv[4] = b1.x; vv[5] = b1.y; vv[6] = b1.z; vv[7] = b1.w;
+            }
+            float dot = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) dot = fmaf(qp[j], kv[j], dot);
+            dot += __shfl_xor(dot, 1);
+            dot += __shfl_xor(dot, 2);
+            dot += __shfl_xor(dot, 4);
+            const float mn = fmaxf(m, dot);
+            const float al = exp2f_fast(m - mn);
+            const float p = exp2f_fast(dot - mn);
+            l = l * al + p;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                C[j] = C[j] * al + p * vv[j];
+                sv[j] += vv[j];
+            }
+            m = mn;
+        }
+    }
+    // Combine the rpi row phases of each (head, segment) in order.
+    __shared__ float s_m[256], s_l[256], s_C[256][9], s_s[256][9];
+    s_m[t] = m;
+    s_l[t] = l;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        s_C[t][j] = C[j];
+        s_s[t][j] = sv[j];
+    }
+    __syncthreads();
+    if (rr == 0) {
+        float M = -INFINITY;
+        for (int q = 0; q < rpi; ++q) M = fmaxf(M, s_m[q * tpr + hs]);
+        float L = 0.f, CC[8], SS[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) CC[j] = SS[j] = 0.f;
+        for (int q = 0; q < rpi; ++q) {
+            const int src = q * tpr + hs;
+            const float mq = s_m[src];
+            const float sc = (mq == -INFINITY) ? 0.f : exp2f_fast(mq - M);
+            L += s_l[src] * sc;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                CC[j] += s_C[src][j] * sc;
+                SS[j] += s_s[src][j];
+            }
+        }
+        float* o = part + ((int64_t)c * H + h) * (2 + 2 * kD);
+        if (seg == 0) {
+            o[0] = M;
+            o[1] = L;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            o[2 + seg * 8 + j] = CC[j];
+            o[2 + kD + seg * 8 + j] = SS[j];
+        }
+    }
+}
+
+// K9b: per head, combine chunks in order; write stats, score, ctx, vmean.
+__global__ __launch_bounds__(64) void k_route_combine(const float* __restrict__ part, int nchunks,
+                                                      int H, int64_t N, float* __restrict__ stats,
+                                                      float* __restrict__ score,
+                                                      float* __restrict__ ctx,
+                                                      float* __restrict__ vmean) {
+    const int h = blockIdx.x, d = threadIdx.x;
+    const int stride = 2 + 2 * kD;
+    float M = -INFINITY;
+    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, part[((int64_t)c * H + h) * stride]);
+    float L = 0.f, C = 0.f, Sv = 0.f;
+    for (int c = 0; c < nchunks; ++c) {
+        const float* p = part + ((int64_t)c * H + h) * stride;
+        const float sc = (p[0] == -INFINITY) ? 0.f : exp2f_fast(p[0] - M);
+        L += p[1] * sc;
+        C += p[2 + d] * sc;
+        Sv += p[2 + kD + d];
+    }
+    ctx[h * kD + d] = C / L;
+    vmean[h * kD + d] = Sv / (float)N;
+    if (d == 0) {
+        stats[2 * h] = M * kLn2;
+        stats[2 * h + 1] = L;
+        score[h] = 1.f / L;
+    }
+}
+
+// ------------------------------------------------------------------------
+// K3: linear-logit mode router, one workgroup per output row, fixed-order
+// tree reduction.
+// ------------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(256) void k_router_logits(const float* __restrict__ u,
+                                                       const void* __restrict__ Wr,
+                                                       const float* __restrict__ br, int Din,
+                                                       float* __restrict__ logits) {
+    const int r = blockIdx.x, t = threadIdx.x;
+    float acc = 0.f;
+    for (int c = t; c < Din; c += 256) {
+        const float wv = (DT == DT_BF16)
+                             ? bf16_to_f32(reinterpret_cast<const bf16*>(Wr)[(int64_t)r * Din + c])
+                             : reinterpret_cast<const float*>(Wr)[(int64_t)r * Din + c];
+        acc = fmaf(wv, u[c], acc);
+    }
+    acc = wave_sum(acc);
+    __shared__ float s[4];
+    if ((t & 63) == 0) s[t >> 6] = acc;
+    __syncthreads();
+    if (t == 0) logits[r] = ((s[0] + s[1]) + (s[2] + s[3])) + br[r];
+}
+
+// ------------------------------------------------------------------------
+// K4: mode per head (Eq.4 or first argmax) and the grouped head lists.
+// ------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_assign(const float* __restrict__ scores, int H, int rule,
+                                               float tau_low, float tau_high,
+                                               uint8_t* __restrict__ modes,
+                                               int32_t* __restrict__ buckets) {
+    __shared__ int s_mode[kMaxHeads];
+    __shared__ int s_nan[kMaxHeads];
+    const int h = threadIdx.x;
+    if (h < H) {
+        int md, bad = 0;
+        if (rule == 0) {
+            const float s = scores[h];
+            bad = isnan(s);
+            md = (bad || s >= tau_high) ? MODE_FULL : (s <= tau_low ? MODE_MEAN : MODE_SURR);
+        } else {
+            const float* lg = scores + 3 * h;
+            bad = isnan(lg[0]) || isnan(lg[1]) || isnan(lg[2]);
+            md = 0;
+            if (lg[1] > lg[md]) md = 1;
+            if (lg[2] > lg[md]) md = 2;
+            if (bad) md = MODE_FULL;
+        }
+        s_mode[h] = md;
+        s_nan[h] = bad;
+        modes[h] = (uint8_t)md;
+    }
+    __syncthreads();
+    if (h == 0) {
+        int cnt[3] = {0, 0, 0}, flags = 0;
+        for (int i = 0; i < H; ++i) {
+            cnt[s_mode[i]]++;
+            flags |= s_nan[i];
+        }
+        int pos = 3;
+        for (int md = 0; md < 3; ++md)
+            for (int i = 0; i < H; ++i)
+                if (s_mode[i] == md) buckets[pos++] = i;
+        for (; pos < 3 + kMaxHeads; ++pos) buckets[pos] = -1;
+        buckets[0] = cnt[0];
+        buckets[1] = cnt[1];
+        buckets[2] = cnt[2];
+        buckets[3 + kMaxHeads] = flags;
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+
+void launch_router(const RouterArgs& a, hipStream_t st) {
+    const dim3 g1((unsigned)a.n1, (unsigned)a.H);
+    if (a.dtype == DT_BF16)
+        hipLaunchKernelGGL(k_pool_partial_bf16, g1, dim3(256), 0, st, (const bf16*)a.Q,
+                           (const bf16*)a.W, (const bf16*)a.U, (const bf16*)a.w, a.N, a.H,
+                           a.chunk1, a.part1);
+    else
+        hipLaunchKernelGGL(k_pool_partial_f32, g1, dim3(256), 0, st, (const float*)a.Q,
+                           (const float*)a.W, (const float*)a.U, (const float*)a.w, a.N, a.H,
+                           a.chunk1, a.part1);
+    hipLaunchKernelGGL(k_pool_combine, dim3(a.H), dim3(64), 0, st, a.part1, (int)a.n1, a.H,
+                       a.q_pool);
+    if (a.dtype == DT_BF16)
+        hipLaunchKernelGGL(k_route_partial<DT_BF16>, dim3((unsigned)a.n2), dim3(256), 0, st, a.K,
+                           a.V, a.q_pool, a.scale, a.N, a.H, a.chunk2, a.part2);
+    else
+        hipLaunchKernelGGL(k_route_partial<DT_F32>, dim3((unsigned)a.n2), dim3(256), 0, st, a.K,
+                           a.V, a.q_pool, a.scale, a.N, a.H, a.chunk2, a.part2);
+    hipLaunchKernelGGL(k_route_combine, dim3(a.H), dim3(64), 0, st, a.part2, (int)a.n2, a.H, a.N,
+                       a.stats, a.score, a.ctx, a.vmean);
+}
+
+void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,
+                          int dtype, float* logits, hipStream_t st) {
+    if (dtype == DT_BF16)
+        hipLaunchKernelGGL(k_router_logits<DT_BF16>, dim3(R), dim3(256), 0, st, u, Wr, br, Din,
+                           logits);
+    else
+        hipLaunchKernelGGL(k_router_logits<DT_F32>, dim3(R), dim3(256), 0, st, u, Wr, br, Din,
+                           logits);
+}
+
+void launch_assign(const float* scores, int H, int rule, float tl, float th, uint8_t* modes,
+                   int32_t* buckets, hipStream_t st) {
+    hipLaunchKernelGGL(k_assign, dim3(1), dim3(64), 0, st, scores, H, rule, tl, th, modes,
+                       buckets);
+}
+
+}  // namespace vp

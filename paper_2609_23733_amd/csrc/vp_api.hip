@@ -1,0 +1,299 @@
+// C ABI of libvggtprime.so (declared in include/vggt_prime.h): argument
+// validation, workspace layout and launch sequencing on the caller's stream.
+// Validation runs entirely on the host before anything is enqueued.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/vggt_prime.h"
+#include "vp_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+constexpr int64_t kMaxTokens = (int64_t)1 << 28;   // 268M tokens: int32-safe grids
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct Layout {
+    int64_t N;
+    int64_t n1, chunk1, n2, chunk2, nkt;
+    size_t off_part1, off_part2, off_vt, total;
+};
+
+// Chunking of the router reductions and the workspace carve-up; a pure
+// function of the shape, shared by vp_workspace_bytes and the launches.
+bool make_layout(const vp_shape* s, Layout* L) {
+    if (!s) return false;
+    if (s->S < 1 || s->P < 1 || s->S > kMaxTokens || s->P > kMaxTokens) return false;
+    if (s->S * s->P > kMaxTokens) return false;
+    if (s->H < 1 || s->H > VP_MAX_HEADS || s->d != VP_HEAD_DIM) return false;
+    if (s->dtype != VP_F32 && s->dtype != VP_BF16) return false;
+    const int64_t N = s->S * s->P;
+    L->N = N;
+    int64_t c1 = cdiv(N, 64);
+    c1 = c1 < 256 ? 256 : cdiv(c1, 128) * 128;
+    L->chunk1 = c1;
+    L->n1 = cdiv(N, c1);
+    int64_t c2 = cdiv(N, 1024);
+    L->chunk2 = c2 < 64 ? 64 : c2;
+    L->n2 = cdiv(N, L->chunk2);
+    L->nkt = cdiv(N, 64);
+    size_t off = kAlign;   // first 256 bytes reserved
+    L->off_part1 = off;
+    off = align_up(off + (size_t)L->n1 * s->H * (2 + VP_HEAD_DIM) * sizeof(float));
+    L->off_part2 = off;
+    off = align_up(off + (size_t)L->n2 * s->H * (2 + 2 * VP_HEAD_DIM) * sizeof(float));
+    L->off_vt = off;
+    if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * 64 * 64 * 2);
+    L->total = off;
+    return true;
+}
+
+vp_status shape_status(const vp_shape* s) {
+    if (!s) return VP_ERR_INVALID_ARG;
+    if (s->S < 1 || s->P < 1 || s->H < 1) return VP_ERR_INVALID_ARG;
+    if (s->dtype != VP_F32 && s->dtype != VP_BF16) return VP_ERR_INVALID_ARG;
+    if (s->S > kMaxTokens || s->P > kMaxTokens || s->S * s->P > kMaxTokens)
+        return VP_ERR_UNSUPPORTED;
+    if (s->H > VP_MAX_HEADS || s->d != VP_HEAD_DIM) return VP_ERR_UNSUPPORTED;
+    return VP_OK;
+}
+
+vp_status check_ws(const vp_shape* s, void* ws, size_t ws_bytes, Layout* L) {
+    if (!make_layout(s, L)) return VP_ERR_INVALID_ARG;
+    if (!ws || ((uintptr_t)ws & (kAlign - 1))) return VP_ERR_INVALID_ARG;
+    if (ws_bytes < L->total) return VP_ERR_WORKSPACE;
+    return VP_OK;
+}
+
+vp_status hip_status(const char* where) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        snprintf(g_err, sizeof(g_err), "%s: %s", where, hipGetErrorString(e));
+        return VP_ERR_HIP;
+    }
+    return VP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* vp_status_string(vp_status s) {
+    switch (s) {
+        case VP_OK: return "ok";
+        case VP_ERR_INVALID_ARG: return "invalid argument";
+        case VP_ERR_UNSUPPORTED: return "unsupported shape";
+        case VP_ERR_WORKSPACE: return "workspace too small";
+        case VP_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* vp_last_error(void) { return g_err; }
+
+size_t vp_workspace_bytes(const vp_shape* shape) {
+    Layout L;
+    return make_layout(shape, &L) ? L.total : 0;
+}
+
+vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, const void* V,
+                          const vp_router_weights* rw, vp_router_state* out, void* ws,
+                          size_t ws_bytes, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (!Q || !K || !V || !rw || !out) return VP_ERR_INVALID_ARG;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V)) return VP_ERR_INVALID_ARG;
+    if (!rw->W || !rw->U || !rw->w || !aligned16(rw->W) || !aligned16(rw->U) || !aligned16(rw->w))
+        return VP_ERR_INVALID_ARG;
+    if (rw->L != VP_HIDDEN) return VP_ERR_UNSUPPORTED;
+    if (!isfinite(rw->scale) || rw->scale < 0.f) return VP_ERR_INVALID_ARG;
+    if (!out->q_pool || !out->stats || !out->score || !out->ctx || !out->vmean)
+        return VP_ERR_INVALID_ARG;
+    if (!aligned16(out->q_pool) || !aligned16(out->ctx) || !aligned16(out->vmean))
+        return VP_ERR_INVALID_ARG;
+    Layout L;
+    if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+
+    (void)hipGetLastError();
+    vp::RouterArgs a;
+    a.dtype = shape->dtype == VP_BF16 ? 1 : 0;
+    a.Q = Q; a.K = K; a.V = V;
+    a.W = rw->W; a.U = rw->U; a.w = rw->w;
+    a.N = L.N;
+    a.H = shape->H;
+    a.n1 = L.n1; a.chunk1 = L.chunk1;
+    a.part1 = (float*)((char*)ws + L.off_part1);
+    a.n2 = L.n2; a.chunk2 = L.chunk2;
+    a.part2 = (float*)((char*)ws + L.off_part2);
+    a.scale = rw->scale > 0.f ? rw->scale : 1.f / sqrtf((float)shape->d);
+    a.q_pool = out->q_pool; a.stats = out->stats; a.score = out->score;
+    a.ctx = out->ctx; a.vmean = out->vmean;
+    vp::launch_router(a, (hipStream_t)stream);
+    return hip_status("vp_router_score");
+}
+
+vp_status vp_router_logits(const float* u, const void* W_r, const float* b_r, int32_t H,
+                           int32_t Din, vp_dtype w_dtype, float* logits, void* stream) {
+    if (!u || !W_r || !b_r || !logits) return VP_ERR_INVALID_ARG;
+    if (H < 1 || Din < 1 || Din > 65536) return VP_ERR_INVALID_ARG;
+    if (H > VP_MAX_HEADS) return VP_ERR_UNSUPPORTED;
+    if (w_dtype != VP_F32 && w_dtype != VP_BF16) return VP_ERR_INVALID_ARG;
+    if (((uintptr_t)u & 3u) || ((uintptr_t)b_r & 3u) || ((uintptr_t)logits & 3u) ||
+        ((uintptr_t)W_r & (w_dtype == VP_BF16 ? 1u : 3u)))
+        return VP_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    vp::launch_router_logits(u, W_r, b_r, H * VP_NUM_MODES, Din, w_dtype == VP_BF16 ? 1 : 0,
+                             logits, (hipStream_t)stream);
+    return hip_status("vp_router_logits");
+}
+
+vp_status vp_assign_heads(const float* scores, int32_t H, vp_assign_rule rule, float tau_low,
+                          float tau_high, uint8_t* modes, int32_t* buckets, void* stream) {
+    if (!scores || !modes || !buckets) return VP_ERR_INVALID_ARG;
+    if (H < 1) return VP_ERR_INVALID_ARG;
+    if (H > VP_MAX_HEADS) return VP_ERR_UNSUPPORTED;
+    if (rule != VP_ASSIGN_THRESHOLD && rule != VP_ASSIGN_ARGMAX) return VP_ERR_INVALID_ARG;
+    if (rule == VP_ASSIGN_THRESHOLD &&
+        (!isfinite(tau_low) || !isfinite(tau_high) || tau_low < 0.f || tau_low > tau_high))
+        return VP_ERR_INVALID_ARG;
+    if (((uintptr_t)scores & 3u) || ((uintptr_t)buckets & 3u)) return VP_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    vp::launch_assign(scores, H, (int)rule, tau_low, tau_high, modes, buckets,
+                      (hipStream_t)stream);
+    return hip_status("vp_assign_heads");
+}
+
+namespace {
+
+vp_status check_attn_common(const vp_shape* shape, const void* V, const void* Y,
+                            vp_dtype y_dtype) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (!V || !Y || !aligned16(V) || !aligned16(Y)) return VP_ERR_INVALID_ARG;
+    if (y_dtype != VP_F32 && y_dtype != VP_BF16) return VP_ERR_INVALID_ARG;
+    return VP_OK;
+}
+
+vp_status check_linear(const vp_shape* shape, const void* V, const uint8_t* modes,
+                       const vp_router_state* state, const vp_surrogate_weights* surr,
+                       const void* Y, vp_dtype y_dtype) {
+    vp_status st = check_attn_common(shape, V, Y, y_dtype);
+    if (st != VP_OK) return st;
+    if (!modes || !state || !surr) return VP_ERR_INVALID_ARG;
+    if (!state->ctx || !state->vmean || ((uintptr_t)state->ctx & 3u) ||
+        ((uintptr_t)state->vmean & 3u))
+        return VP_ERR_INVALID_ARG;
+    if (!surr->g_w1 || !surr->g_w2 || !surr->d_w1 || !surr->d_w2 || !surr->g_b1 ||
+        !surr->g_b2 || !surr->d_b1 || !surr->d_b2)
+        return VP_ERR_INVALID_ARG;
+    if (!aligned16(surr->g_w1) || !aligned16(surr->g_w2) || !aligned16(surr->d_w1) ||
+        !aligned16(surr->d_w2))
+        return VP_ERR_INVALID_ARG;
+    if (((uintptr_t)surr->g_b1 & 3u) || ((uintptr_t)surr->g_b2 & 3u) ||
+        ((uintptr_t)surr->d_b1 & 3u) || ((uintptr_t)surr->d_b2 & 3u))
+        return VP_ERR_INVALID_ARG;
+    if (surr->L != VP_HIDDEN) return VP_ERR_UNSUPPORTED;
+    if (surr->act != VP_ACT_GELU_ERF && surr->act != VP_ACT_RELU) return VP_ERR_INVALID_ARG;
+    return VP_OK;
+}
+
+vp::AttnArgs attn_args(const vp_shape* shape, const Layout& L, const void* Q, const void* K,
+                       const void* V, const uint8_t* modes, const int32_t* buckets, void* Y,
+                       vp_dtype y_dtype, void* ws) {
+    vp::AttnArgs a;
+    memset(&a, 0, sizeof(a));
+    a.dtype = shape->dtype == VP_BF16 ? 1 : 0;
+    a.ydt = y_dtype == VP_BF16 ? 1 : 0;
+    a.Q = Q; a.K = K; a.V = V;
+    a.modes = modes;
+    a.buckets = buckets;
+    a.N = L.N;
+    a.H = shape->H;
+    a.vt = ws ? (char*)ws + L.off_vt : nullptr;
+    a.Y = Y;
+    return a;
+}
+
+void set_linear(vp::AttnArgs& a, const vp_router_state* state, const vp_surrogate_weights* surr) {
+    a.ctx = state->ctx;
+    a.vmean = state->vmean;
+    a.g_w1 = surr->g_w1; a.g_w2 = surr->g_w2; a.d_w1 = surr->d_w1; a.d_w2 = surr->d_w2;
+    a.g_b1 = surr->g_b1; a.g_b2 = surr->g_b2; a.d_b1 = surr->d_b1; a.d_b2 = surr->d_b2;
+    a.act = (int)surr->act;
+}
+
+}  // namespace
+
+vp_status vp_gather_full_heads(const vp_shape* shape, const void* V, const int32_t* buckets,
+                               void* ws, size_t ws_bytes, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (!V || !aligned16(V) || !buckets || ((uintptr_t)buckets & 3u)) return VP_ERR_INVALID_ARG;
+    Layout L;
+    if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+    if (shape->dtype != VP_BF16) return VP_OK;
+    (void)hipGetLastError();
+    vp::AttnArgs a = attn_args(shape, L, nullptr, nullptr, V, nullptr, buckets, nullptr, VP_F32, ws);
+    vp::launch_gather(a, (hipStream_t)stream);
+    return hip_status("vp_gather_full_heads");
+}
+
+vp_status vp_full_head_attention(const vp_shape* shape, const void* Q, const void* K,
+                                 const void* V, const int32_t* buckets, void* Y,
+                                 vp_dtype y_dtype, void* ws, size_t ws_bytes, void* stream) {
+    vp_status st = check_attn_common(shape, V, Y, y_dtype);
+    if (st != VP_OK) return st;
+    if (!Q || !K || !aligned16(Q) || !aligned16(K)) return VP_ERR_INVALID_ARG;
+    if (!buckets || ((uintptr_t)buckets & 3u)) return VP_ERR_INVALID_ARG;
+    Layout L;
+    if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+    (void)hipGetLastError();
+    vp::AttnArgs a = attn_args(shape, L, Q, K, V, nullptr, buckets, Y, y_dtype, ws);
+    vp::launch_flash(a, (hipStream_t)stream);
+    return hip_status("vp_full_head_attention");
+}
+
+vp_status vp_linear_heads(const vp_shape* shape, const void* V, const uint8_t* modes,
+                          const vp_router_state* state, const vp_surrogate_weights* surr,
+                          void* Y, vp_dtype y_dtype, void* stream) {
+    vp_status st = check_linear(shape, V, modes, state, surr, Y, y_dtype);
+    if (st != VP_OK) return st;
+    Layout L;
+    make_layout(shape, &L);
+    (void)hipGetLastError();
+    vp::AttnArgs a = attn_args(shape, L, nullptr, nullptr, V, modes, nullptr, Y, y_dtype, nullptr);
+    set_linear(a, state, surr);
+    vp::launch_linear_heads(a, (hipStream_t)stream);
+    return hip_status("vp_linear_heads");
+}
+
+vp_status vp_routed_global_attention(const vp_shape* shape, const void* Q, const void* K,
+                                     const void* V, const uint8_t* modes,
+                                     const int32_t* buckets, const vp_router_state* state,
+                                     const vp_surrogate_weights* surr, void* Y, vp_dtype y_dtype,
+                                     void* ws, size_t ws_bytes, void* stream) {
+    vp_status st = check_linear(shape, V, modes, state, surr, Y, y_dtype);
+    if (st != VP_OK) return st;
+    if (!Q || !K || !aligned16(Q) || !aligned16(K)) return VP_ERR_INVALID_ARG;
+    if (!buckets || ((uintptr_t)buckets & 3u)) return VP_ERR_INVALID_ARG;
+    Layout L;
+    if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+    (void)hipGetLastError();
+    vp::AttnArgs a = attn_args(shape, L, Q, K, V, modes, buckets, Y, y_dtype, ws);
+    set_linear(a, state, surr);
+    hipStream_t s = (hipStream_t)stream;
+    if (a.dtype == 1) vp::launch_gather(a, s);
+    vp::launch_flash(a, s);
+    vp::launch_linear_heads(a, s);
+    return hip_status("vp_routed_global_attention");
+}
+
+}  // extern "C"

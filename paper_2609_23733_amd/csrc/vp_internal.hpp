@@ -1,0 +1,48 @@
+// Host-side launcher interface between the C ABI (vp_api.hip) and the kernel
+// files.  Everything here is internal to libvggtprime.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vp {
+
+struct RouterArgs {
+    int dtype;
+    const void *Q, *K, *V, *W, *U, *w;
+    int64_t N;
+    int H;
+    int64_t n1, chunk1;   // pooling chunks
+    float* part1;
+    int64_t n2, chunk2;   // routing chunks
+    float* part2;
+    float scale;
+    float *q_pool, *stats, *score, *ctx, *vmean;
+};
+
+struct AttnArgs {
+    int dtype, ydt;
+    const void *Q, *K, *V;
+    const uint8_t* modes;
+    const int32_t* buckets;
+    int64_t N;
+    int H;
+    void* vt;   // packed V^T of FULL heads (bf16 only)
+    void* Y;
+    const float *ctx, *vmean;
+    const void *g_w1, *g_w2, *d_w1, *d_w2;
+    const float *g_b1, *g_b2, *d_b1, *d_b2;
+    int act;
+};
+
+void launch_router(const RouterArgs& a, hipStream_t st);
+void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,
+                          int dtype, float* logits, hipStream_t st);
+void launch_assign(const float* scores, int H, int rule, float tl, float th, uint8_t* modes,
+                   int32_t* buckets, hipStream_t st);
+void launch_gather(const AttnArgs& a, hipStream_t st);
+void launch_flash(const AttnArgs& a, hipStream_t st);
+void launch_linear_heads(const AttnArgs& a, hipStream_t st);
+int flash_q_tile(int dtype);
+
+}  // namespace vp

@@ -1,0 +1,357 @@
+"""Python binding of libvggtprime.so (include/vggt_prime.h).
+
+Argument marshalling only: every step of the layer runs in the HIP kernels of
+the library.  Tensors are torch CUDA (HIP) tensors; each call enqueues on the
+current torch stream and returns without synchronising.  There is no CPU
+fallback: if the library is not built, loading fails with an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libvggtprime.so")
+
+VP_OK, VP_ERR_INVALID_ARG, VP_ERR_UNSUPPORTED, VP_ERR_WORKSPACE, VP_ERR_HIP = range(5)
+VP_F32, VP_BF16 = 0, 1
+MODE_MEAN, MODE_SURR, MODE_FULL = 0, 1, 2
+RULE_THRESHOLD, RULE_ARGMAX = 0, 1
+ACT_GELU_ERF, ACT_RELU = 0, 1
+MAX_HEADS, HEAD_DIM, HIDDEN = 16, 64, 64
+BUCKETS_LEN = 3 + MAX_HEADS + 1
+TAU_LOW, TAU_HIGH = 0.01, 0.20
+
+EXPORTS = ("vp_workspace_bytes", "vp_router_score", "vp_router_logits", "vp_assign_heads",
+           "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
+           "vp_linear_heads", "vp_status_string", "vp_last_error")
+
+
+class vp_shape(ctypes.Structure):
+    _fields_ = [("S", ctypes.c_int64), ("P", ctypes.c_int64), ("H", ctypes.c_int32),
+                ("d", ctypes.c_int32), ("dtype", ctypes.c_int)]
+
+
+class vp_router_weights(ctypes.Structure):
+    _fields_ = [("W", ctypes.c_void_p), ("U", ctypes.c_void_p), ("w", ctypes.c_void_p),
+                ("L", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class vp_router_state(ctypes.Structure):
+    _fields_ = [("q_pool", ctypes.c_void_p), ("stats", ctypes.c_void_p),
+                ("score", ctypes.c_void_p), ("ctx", ctypes.c_void_p), ("vmean", ctypes.c_void_p)]
+
+
+class vp_surrogate_weights(ctypes.Structure):
+    _fields_ = [("g_w1", ctypes.c_void_p), ("g_w2", ctypes.c_void_p), ("d_w1", ctypes.c_void_p),
+                ("d_w2", ctypes.c_void_p), ("g_b1", ctypes.c_void_p), ("g_b2", ctypes.c_void_p),
+                ("d_b1", ctypes.c_void_p), ("d_b2", ctypes.c_void_p), ("L", ctypes.c_int32),
+                ("act", ctypes.c_int)]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libvggtprime.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError("libvggtprime.so is not built (%s); run "
+                           "`python -c 'import __graft_entry__ as g; g.build()'`" % path)
+    lib = ctypes.CDLL(path)
+    P, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    lib.vp_workspace_bytes.argtypes = [ctypes.POINTER(vp_shape)]
+    lib.vp_workspace_bytes.restype = ctypes.c_size_t
+    lib.vp_router_score.argtypes = [ctypes.POINTER(vp_shape), P, P, P,
+                                    ctypes.POINTER(vp_router_weights),
+                                    ctypes.POINTER(vp_router_state), P, ctypes.c_size_t, P]
+    lib.vp_router_logits.argtypes = [P, P, P, i32, i32, ctypes.c_int, P, P]
+    lib.vp_assign_heads.argtypes = [P, i32, ctypes.c_int, f32, f32, P, P, P]
+    lib.vp_routed_global_attention.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P,
+                                               ctypes.POINTER(vp_router_state),
+                                               ctypes.POINTER(vp_surrogate_weights), P,
+                                               ctypes.c_int, P, ctypes.c_size_t, P]
+    lib.vp_gather_full_heads.argtypes = [ctypes.POINTER(vp_shape), P, P, P, ctypes.c_size_t, P]
+    lib.vp_full_head_attention.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P, ctypes.c_int,
+                                           P, ctypes.c_size_t, P]
+    lib.vp_linear_heads.argtypes = [ctypes.POINTER(vp_shape), P, P,
+                                    ctypes.POINTER(vp_router_state),
+                                    ctypes.POINTER(vp_surrogate_weights), P, ctypes.c_int, P]
+    for f in ("vp_router_score", "vp_router_logits", "vp_assign_heads",
+              "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
+              "vp_linear_heads"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.vp_status_string.argtypes = [ctypes.c_int]
+    lib.vp_status_string.restype = ctypes.c_char_p
+    lib.vp_last_error.argtypes = []
+    lib.vp_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+class VPError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        lib = load_library()
+        msg = lib.vp_status_string(code).decode()
+        if code == VP_ERR_HIP:
+            msg += ": " + lib.vp_last_error().decode()
+        super().__init__("%s failed: %s (status %d)" % (where, msg, code))
+        self.code = code
+
+
+def _check(code: int, where: str):
+    if code != VP_OK:
+        raise VPError(code, where)
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return VP_BF16
+    if t.dtype == torch.float32:
+        return VP_F32
+    raise TypeError("unsupported dtype %s" % t.dtype)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, shape=None, dtype=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a tensor" % name)
+    if not t.is_cuda:
+        raise ValueError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+
+
+def make_shape(S: int, P: int, H: int, dtype: torch.dtype) -> vp_shape:
+    return vp_shape(S, P, H, HEAD_DIM, VP_BF16 if dtype == torch.bfloat16 else VP_F32)
+
+
+def workspace_bytes(S: int, P: int, H: int = MAX_HEADS, dtype=torch.bfloat16) -> int:
+    n = load_library().vp_workspace_bytes(ctypes.byref(make_shape(S, P, H, dtype)))
+    if n == 0:
+        raise ValueError("invalid shape")
+    return int(n)
+
+
+def alloc_workspace(S: int, P: int, H: int = MAX_HEADS, dtype=torch.bfloat16,
+                    device="cuda") -> torch.Tensor:
+    # torch's caching allocator returns 512-byte aligned blocks
+    return torch.empty(workspace_bytes(S, P, H, dtype), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class RouterState:
+    q_pool: torch.Tensor   # [H, d]
+    stats: torch.Tensor    # [H, 2]  (m, l)
+    score: torch.Tensor    # [H]
+    ctx: torch.Tensor      # [H, d]
+    vmean: torch.Tensor    # [H, d]
+
+    @staticmethod
+    def empty(H: int, device="cuda") -> "RouterState":
+        f = lambda *s: torch.empty(*s, dtype=torch.float32, device=device)
+        return RouterState(f(H, HEAD_DIM), f(H, 2), f(H), f(H, HEAD_DIM), f(H, HEAD_DIM))
+
+    def c(self) -> vp_router_state:
+        return vp_router_state(self.q_pool.data_ptr(), self.stats.data_ptr(),
+                               self.score.data_ptr(), self.ctx.data_ptr(), self.vmean.data_ptr())
+
+
+def router_score(Q, K, V, W, U, w, S: int, P: int, ws: torch.Tensor, scale: float = 0.0,
+                 out: Optional[RouterState] = None) -> RouterState:
+    """Router (Eq.1-3) plus context and value mean: see vp_router_score."""
+    N, H = S * P, Q.shape[1]
+    for t, nm in ((Q, "Q"), (K, "K"), (V, "V")):
+        _need(t, nm, (N, H, HEAD_DIM), Q.dtype)
+    _need(W, "W", (H, HIDDEN, HEAD_DIM), Q.dtype)
+    _need(U, "U", (H, HIDDEN, HEAD_DIM), Q.dtype)
+    _need(w, "w", (H, HIDDEN), Q.dtype)
+    _need(ws, "ws")
+    if out is None:
+        out = RouterState.empty(H, Q.device)
+    rw = vp_router_weights(W.data_ptr(), U.data_ptr(), w.data_ptr(), HIDDEN, float(scale))
+    shp = make_shape(S, P, H, Q.dtype)
+    st = out.c()
+    _check(load_library().vp_router_score(ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V),
+                                          ctypes.byref(rw), ctypes.byref(st), _ptr(ws),
+                                          ws.numel() * ws.element_size(), _stream()),
+           "vp_router_score")
+    return out
+
+
+def router_logits(u, Wr, br, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Linear-logit mode router of the synthetic workloads: [H, 3] fp32."""
+    R, Din = Wr.shape
+    H = R // 3
+    _need(u, "u", (Din,), torch.float32)
+    _need(Wr, "Wr")
+    _need(br, "br", (R,), torch.float32)
+    if out is None:
+        out = torch.empty(H, 3, dtype=torch.float32, device=u.device)
+    _need(out, "logits", (H, 3), torch.float32)
+    _check(load_library().vp_router_logits(_ptr(u), _ptr(Wr), _ptr(br), H, Din, _dt(Wr),
+                                           _ptr(out), _stream()), "vp_router_logits")
+    return out
+
+
+def assign_heads(scores, rule: int, tau_low: float = TAU_LOW, tau_high: float = TAU_HIGH,
+                 modes: Optional[torch.Tensor] = None, buckets: Optional[torch.Tensor] = None):
+    """Mode assignment (Eq.4 / argmax).  Returns (modes uint8 [H], buckets int32 [20])."""
+    H = scores.shape[0]
+    _need(scores, "scores", None, torch.float32)
+    if modes is None:
+        modes = torch.empty(H, dtype=torch.uint8, device=scores.device)
+    if buckets is None:
+        buckets = torch.empty(BUCKETS_LEN, dtype=torch.int32, device=scores.device)
+    _need(modes, "modes", (H,), torch.uint8)
+    _need(buckets, "buckets", (BUCKETS_LEN,), torch.int32)
+    _check(load_library().vp_assign_heads(_ptr(scores), H, int(rule), float(tau_low),
+                                          float(tau_high), _ptr(modes), _ptr(buckets),
+                                          _stream()), "vp_assign_heads")
+    return modes, buckets
+
+
+def _surr_struct(surr, H, dtype, act):
+    for k in ("g_w1", "d_w1"):
+        _need(surr[k], k, (H, HIDDEN, 2 * HEAD_DIM), dtype)
+    for k in ("g_w2", "d_w2"):
+        _need(surr[k], k, (H, HEAD_DIM, HIDDEN), dtype)
+    for k in ("g_b1", "d_b1"):
+        _need(surr[k], k, (H, HIDDEN), torch.float32)
+    for k in ("g_b2", "d_b2"):
+        _need(surr[k], k, (H, HEAD_DIM), torch.float32)
+    return vp_surrogate_weights(*(surr[k].data_ptr() for k in
+                                  ("g_w1", "g_w2", "d_w1", "d_w2", "g_b1", "g_b2", "d_b1",
+                                   "d_b2")), HIDDEN, int(act))
+
+
+def _qkv(Q, K, V, S, P):
+    N, H = S * P, Q.shape[1]
+    for t, nm in ((Q, "Q"), (K, "K"), (V, "V")):
+        _need(t, nm, (N, H, HEAD_DIM), Q.dtype)
+    return N, H
+
+
+def routed_global_attention(Q, K, V, modes, buckets, state: RouterState,
+                            surr: Dict[str, torch.Tensor], S: int, P: int, ws: torch.Tensor,
+                            y_dtype=None, act: int = ACT_GELU_ERF,
+                            Y: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Routed global attention (Algorithm 1 step 2): Y [N, H, d]."""
+    N, H = _qkv(Q, K, V, S, P)
+    _need(modes, "modes", (H,), torch.uint8)
+    _need(buckets, "buckets", (BUCKETS_LEN,), torch.int32)
+    if y_dtype is None:
+        y_dtype = Q.dtype
+    if Y is None:
+        Y = torch.empty(N, H, HEAD_DIM, dtype=y_dtype, device=Q.device)
+    _need(Y, "Y", (N, H, HEAD_DIM), y_dtype)
+    sw = _surr_struct(surr, H, Q.dtype, act)
+    shp = make_shape(S, P, H, Q.dtype)
+    st = state.c()
+    _check(load_library().vp_routed_global_attention(
+        ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V), _ptr(modes), _ptr(buckets),
+        ctypes.byref(st), ctypes.byref(sw), _ptr(Y), _dt(Y), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream()), "vp_routed_global_attention")
+    return Y
+
+
+def gather_full_heads(V, buckets, S: int, P: int, ws: torch.Tensor):
+    """Stage 1 of routed_global_attention: pack V of the FULL heads."""
+    N, H = S * P, V.shape[1]
+    _need(V, "V", (N, H, HEAD_DIM))
+    _need(buckets, "buckets", (BUCKETS_LEN,), torch.int32)
+    shp = make_shape(S, P, H, V.dtype)
+    _check(load_library().vp_gather_full_heads(ctypes.byref(shp), _ptr(V), _ptr(buckets),
+                                               _ptr(ws), ws.numel() * ws.element_size(),
+                                               _stream()), "vp_gather_full_heads")
+
+
+def full_head_attention(Q, K, V, buckets, S: int, P: int, ws: torch.Tensor, Y: torch.Tensor):
+    """Stage 2: exact softmax attention of every FULL head into Y."""
+    N, H = _qkv(Q, K, V, S, P)
+    _need(buckets, "buckets", (BUCKETS_LEN,), torch.int32)
+    _need(Y, "Y", (N, H, HEAD_DIM))
+    shp = make_shape(S, P, H, Q.dtype)
+    _check(load_library().vp_full_head_attention(ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V),
+                                                 _ptr(buckets), _ptr(Y), _dt(Y), _ptr(ws),
+                                                 ws.numel() * ws.element_size(), _stream()),
+           "vp_full_head_attention")
+
+
+def linear_heads(V, modes, state: RouterState, surr, S: int, P: int, Y: torch.Tensor,
+                 act: int = ACT_GELU_ERF):
+    """Stage 3: SURR and MEAN heads into Y."""
+    N, H = S * P, V.shape[1]
+    _need(V, "V", (N, H, HEAD_DIM))
+    _need(modes, "modes", (H,), torch.uint8)
+    _need(Y, "Y", (N, H, HEAD_DIM))
+    sw = _surr_struct(surr, H, V.dtype, act)
+    shp = make_shape(S, P, H, V.dtype)
+    st = state.c()
+    _check(load_library().vp_linear_heads(ctypes.byref(shp), _ptr(V), _ptr(modes),
+                                          ctypes.byref(st), ctypes.byref(sw), _ptr(Y), _dt(Y),
+                                          _stream()), "vp_linear_heads")
+
+
+class RoutedLayer:
+    """One routed global-attention layer on the GPU: holds the weights, the
+    router state and the workspace, and runs the four library calls in order
+    (router_score, [router_logits], assign_heads, routed_global_attention)."""
+
+    def __init__(self, inp, rule: int = RULE_ARGMAX, y_dtype=None, act: int = ACT_GELU_ERF,
+                 tau_low: float = TAU_LOW, tau_high: float = TAU_HIGH, device="cuda"):
+        x = inp.to(device)
+        self.x = x
+        self.S, self.P, self.H = x.S, x.P, x.H
+        self.rule, self.act = rule, act
+        self.tau_low, self.tau_high = tau_low, tau_high
+        self.y_dtype = y_dtype if y_dtype is not None else x.Q.dtype
+        self.ws = alloc_workspace(x.S, x.P, x.H, x.Q.dtype, device)
+        self.state = RouterState.empty(x.H, device)
+        self.logits = torch.empty(x.H, 3, dtype=torch.float32, device=device)
+        self.modes = torch.empty(x.H, dtype=torch.uint8, device=device)
+        self.buckets = torch.empty(BUCKETS_LEN, dtype=torch.int32, device=device)
+        self.Y = torch.empty(x.N, x.H, HEAD_DIM, dtype=self.y_dtype, device=device)
+
+    def step(self, Q=None, K=None, V=None, events=None) -> torch.Tensor:
+        """One pass of the layer; ``events`` = (start, end) torch.cuda.Events
+        recorded around the FULL-head attention kernel on the current stream."""
+        x = self.x
+        Q = x.Q if Q is None else Q
+        K = x.K if K is None else K
+        V = x.V if V is None else V
+        router_score(Q, K, V, x.W, x.U, x.w, self.S, self.P, self.ws, out=self.state)
+        if self.rule == RULE_ARGMAX:
+            router_logits(x.u, x.Wr, x.br, out=self.logits)
+            scores = self.logits
+        else:
+            scores = self.state.score
+        assign_heads(scores, self.rule, self.tau_low, self.tau_high, self.modes, self.buckets)
+        if events is None:
+            routed_global_attention(Q, K, V, self.modes, self.buckets, self.state, x.surr,
+                                    self.S, self.P, self.ws, self.y_dtype, self.act, self.Y)
+        else:
+            # the same three stages, with events bracketing the FULL-head kernel
+            gather_full_heads(V, self.buckets, self.S, self.P, self.ws)
+            events[0].record()
+            full_head_attention(Q, K, V, self.buckets, self.S, self.P, self.ws, self.Y)
+            events[1].record()
+            linear_heads(V, self.modes, self.state, x.surr, self.S, self.P, self.Y, self.act)
+        return self.Y

@@ -1,0 +1,159 @@
+"""The C-ABI library loads, exports every symbol the header declares, and
+rejects bad arguments on the host before anything is enqueued (CPU only:
+every call here fails validation, so no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2609_23733_amd import vp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vggt_prime.h")
+
+FAKE = 0x10000          # 256-byte aligned fake device address (never dereferenced)
+FAKE_ODD = 0x10002      # misaligned
+
+
+def header_functions():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(vp_\w+)\s*\(", txt, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return vp.load_library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert set(names) == set(vp.EXPORTS)
+    for n in names:
+        assert getattr(lib, n) is not None
+
+
+def test_status_strings(lib):
+    for code in range(5):
+        assert lib.vp_status_string(code)
+    assert lib.vp_last_error() == b""
+
+
+def shape(S=2, P=1374, H=16, d=64, dt=vp.VP_BF16):
+    return vp.vp_shape(S, P, H, d, dt)
+
+
+def test_workspace_bytes(lib):
+    f = lambda s: lib.vp_workspace_bytes(ctypes.byref(s))
+    assert f(shape(S=0)) == 0
+    assert f(shape(H=17)) == 0
+    assert f(shape(d=32)) == 0
+    assert f(shape(dt=7)) == 0
+    a, b = f(shape(S=2)), f(shape(S=8))
+    assert 0 < a < b
+    assert a % 256 == 0
+    # bf16 needs room for the packed values of up to H FULL heads
+    assert f(shape(dt=vp.VP_BF16)) > f(shape(dt=vp.VP_F32))
+
+
+def rw(L=64, W=FAKE, scale=0.0):
+    return vp.vp_router_weights(W, FAKE, FAKE, L, scale)
+
+
+def rs(q=FAKE):
+    return vp.vp_router_state(q, FAKE, FAKE, FAKE, FAKE)
+
+
+def call_score(lib, shp=None, Q=FAKE, w=None, st=None, ws=FAKE, ws_bytes=1 << 40):
+    shp = shp or shape()
+    w = w or rw()
+    st = st or rs()
+    return lib.vp_router_score(ctypes.byref(shp), Q, FAKE, FAKE, ctypes.byref(w), ctypes.byref(st),
+                               ws, ws_bytes, None)
+
+
+def test_router_score_validation(lib):
+    assert call_score(lib, shp=shape(S=0)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, shp=shape(H=0)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, shp=shape(H=17)) == vp.VP_ERR_UNSUPPORTED
+    assert call_score(lib, shp=shape(d=128)) == vp.VP_ERR_UNSUPPORTED
+    assert call_score(lib, shp=shape(S=1 << 20, P=1 << 10)) == vp.VP_ERR_UNSUPPORTED
+    assert call_score(lib, shp=shape(dt=5)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, Q=None) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, Q=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, w=rw(W=None)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, w=rw(L=32)) == vp.VP_ERR_UNSUPPORTED
+    assert call_score(lib, w=rw(scale=float("nan"))) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, st=rs(q=None)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, ws=None) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, ws=FAKE + 64) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, ws_bytes=1024) == vp.VP_ERR_WORKSPACE
+    assert lib.vp_router_score(None, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None) == \
+        vp.VP_ERR_INVALID_ARG
+
+
+def test_router_logits_validation(lib):
+    f = lib.vp_router_logits
+    assert f(None, FAKE, FAKE, 16, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, None, FAKE, 16, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 0, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 17, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, 16, 0, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 16, 1 << 20, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 16, 1024, 9, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE + 1, FAKE, FAKE, 16, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+
+
+def test_assign_validation(lib):
+    f = lib.vp_assign_heads
+    assert f(None, 16, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 0, 0.01, 0.2, None, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 0, 0.01, 0.2, FAKE, None, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 0, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 17, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, 16, 2, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 0, 0.3, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 0, -0.1, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 0, float("nan"), 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE + 2, 16, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+
+
+def sw(L=64, act=0, g_w1=FAKE):
+    return vp.vp_surrogate_weights(g_w1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, L, act)
+
+
+def call_attn(lib, shp=None, Q=FAKE, modes=FAKE, st=None, s=None, Y=FAKE, ydt=vp.VP_BF16,
+              ws=FAKE, ws_bytes=1 << 40):
+    shp = shp or shape()
+    st = st or rs()
+    s = s or sw()
+    return lib.vp_routed_global_attention(ctypes.byref(shp), Q, FAKE, FAKE, modes, FAKE,
+                                          ctypes.byref(st), ctypes.byref(s), Y, ydt, ws, ws_bytes,
+                                          None)
+
+
+def test_routed_attention_validation(lib):
+    assert call_attn(lib, shp=shape(P=0)) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, shp=shape(H=20)) == vp.VP_ERR_UNSUPPORTED
+    assert call_attn(lib, Q=None) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, modes=None) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, Y=None) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, Y=FAKE + 8) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, ydt=3) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, s=sw(L=16)) == vp.VP_ERR_UNSUPPORTED
+    assert call_attn(lib, s=sw(act=7)) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, s=sw(g_w1=None)) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, ws_bytes=10) == vp.VP_ERR_WORKSPACE
+    assert lib.vp_routed_global_attention(ctypes.byref(shape()), FAKE, FAKE, FAKE, FAKE, FAKE,
+                                          None, ctypes.byref(sw()), FAKE, 1, FAKE, 1 << 40,
+                                          None) == vp.VP_ERR_INVALID_ARG
+
+
+def test_binding_rejects_cpu_tensors():
+    x = torch.zeros(4, 16, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        vp.router_score(x, x, x, torch.zeros(16, 64, 64, dtype=torch.bfloat16),
+                        torch.zeros(16, 64, 64, dtype=torch.bfloat16),
+                        torch.zeros(16, 64, dtype=torch.bfloat16), 1, 4,
+                        torch.zeros(10, dtype=torch.uint8))

@@ -1,0 +1,275 @@
+"""GPU parity of the routed global-attention layer against the fp64 oracle.
+
+Every test runs the HIP path through the C ABI (paper_2609_23733_amd.vp) and
+the oracle on the same seeded inputs, then compares:
+  - mode-router logits: |diff| <= 1e-5 (fp32 GEMV of 1024 terms);
+  - modes and buckets: bit-exact (inputs are generated with logit margins
+    >= 1e-3, or planted saliencies >= 1e-3 away from the thresholds);
+  - router outputs q_pool, s, C, mean: max |diff| <= 1e-4 * RMS;
+  - Y per head h: max |Y - Y_oracle| <= tol * RMS(Y_oracle[:, h]) with
+    tol = 1e-4 for fp32 operands and 2e-2 for bf16 operands; when Y is
+    stored as bf16 the bound adds the half-ulp of round-to-nearest-even,
+    2^-8 |Y_oracle|, elementwise.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_23733_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def log(msg):
+    sys.stdout.write("[gpu-case] %s\n" % msg)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_23733_amd import vp
+    vp.load_library()
+
+
+def run_gpu(x, rule=oracle.RULE_ARGMAX, y_dtype=None, act=0):
+    from paper_2609_23733_amd import vp
+    layer = vp.RoutedLayer(x, rule=rule, y_dtype=y_dtype, act=act)
+    layer.step()
+    torch.cuda.synchronize()
+    return layer
+
+
+def rms(a):
+    return float(np.sqrt(np.mean(np.square(a))))
+
+
+def check_router(layer, ref, rule):
+    st = layer.state
+    for name, g, r in (("q_pool", st.q_pool, ref["q_pool"]), ("ctx", st.ctx, ref["C"]),
+                       ("vmean", st.vmean, ref["mean"])):
+        g = g.cpu().numpy().astype(np.float64)
+        for h in range(g.shape[0]):
+            err = np.abs(g[h] - r[h]).max()
+            assert err <= 1e-4 * max(rms(r[h]), 1e-30), (name, h, err, rms(r[h]))
+    s = st.score.cpu().numpy().astype(np.float64)
+    np.testing.assert_allclose(s, ref["s"], rtol=1e-4)
+    if rule == oracle.RULE_ARGMAX and ref["logits"] is not None:
+        lg = layer.logits.cpu().numpy().astype(np.float64)
+        assert np.abs(lg - ref["logits"]).max() <= 1e-5
+    modes = layer.modes.cpu().numpy()
+    np.testing.assert_array_equal(modes, ref["modes"])
+    counts, lst = oracle.buckets(ref["modes"])
+    b = layer.buckets.cpu().numpy()
+    np.testing.assert_array_equal(b[:3], counts)
+    np.testing.assert_array_equal(b[3:3 + len(lst)], lst)
+    assert b[19] == 0
+
+
+def check_y(Yg, Yo, dtype, y_bf16, heads=None, label=""):
+    """Yg: GPU rows [R, H, d] (float64); Yo: oracle rows [R, H, d]."""
+    tol = TOL[dtype]
+    H = Yo.shape[1]
+    worst = 0.0
+    for h in (range(H) if heads is None else heads):
+        r = Yo[:, h, :]
+        bound = tol * rms(r) + (2.0 ** -8 * np.abs(r) if y_bf16 else 0.0)
+        err = np.abs(Yg[:, h, :] - r)
+        ratio = float((err / np.maximum(bound, 1e-300)).max())
+        worst = max(worst, ratio)
+        assert (err <= bound).all(), "%s head %d: max err %.3e, rms %.3e, ratio %.3f" % (
+            label, h, err.max(), rms(r), ratio)
+    log("%s worst err/bound = %.3f" % (label, worst))
+
+
+def oracle_layer(x, rule=oracle.RULE_ARGMAX, rows=None, full_rows_sel=None, act=0):
+    return oracle.routed_layer(x.Q, x.K, x.V, x.W, x.U, x.w, x.surr, u=x.u, Wr=x.Wr, br=x.br,
+                               rule=rule, rows=rows, full_rows_sel=full_rows_sel, act=act)
+
+
+# ------------------------------------------------------------- small layers
+
+@pytest.mark.parametrize("wl", ["s2_f32", "s8_bf16"])
+def test_workload_layer_parity(wl):
+    cfg = synth.WORKLOADS[wl]
+    log("workload %s" % wl)
+    x = synth.make_layer(cfg["S"], dtype=cfg["dtype"], n_full=cfg["n_full"], key=(1, 0),
+                         qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.float32)
+    rows = None if cfg["S"] <= 2 else synth.sample_rows(x.N, 768, synth.derive_seed(1, 0, 20))
+    ref = oracle_layer(x, rows=rows)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    Yg = layer.Y.double().cpu().numpy()
+    if rows is not None:
+        Yg = Yg[rows]
+    check_y(Yg, ref["Y"], cfg["dtype"], False, label=wl)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("P", [1, 2, 63, 64, 65, 255, 257, 1000])
+def test_ragged_token_counts(dtype, P):
+    """Token counts around the 64-key and 256/128-query tiles, sharp inputs
+    (attention far from uniform), every mode present."""
+    log("ragged P=%d %s" % (P, dtype))
+    modes = np.array([2, 1, 0, 2, 2, 1, 0, 0, 1, 2, 0, 1, 2, 0, 1, 2], np.uint8)
+    x = synth.make_layer(1, P, dtype=dtype, key=(2, P), sharp=True, modes=modes,
+                         qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], dtype, False, label="P=%d" % P)
+
+
+@pytest.mark.parametrize("H", [1, 3, 5, 8])
+def test_fewer_heads(H):
+    log("H=%d" % H)
+    modes = np.array(([2, 1, 0] * 6)[:H], np.uint8)
+    x = synth.make_layer(2, 150, dtype="bf16", key=(3, H), sharp=True, H=H, modes=modes,
+                         qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="H=%d" % H)
+
+
+def test_bf16_output_and_relu():
+    log("bf16 output, relu")
+    x = synth.make_layer(2, 700, dtype="bf16", key=(4, 0), sharp=True, n_full=6,
+                         qkv_device="cuda")
+    for act in (0, 1):
+        layer = run_gpu(x, y_dtype=torch.bfloat16, act=act)
+        ref = oracle_layer(x, act=act)
+        check_router(layer, ref, oracle.RULE_ARGMAX)
+        check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", True, label="act=%d" % act)
+
+
+def test_single_token():
+    """N = 1: FULL returns v, MEAN returns v, s = 1 (every head FULL under Eq.4)."""
+    log("N=1")
+    x = synth.make_layer(1, 1, dtype="f32", key=(5, 0), n_full=16, qkv_device="cuda")
+    layer = run_gpu(x, rule=oracle.RULE_THRESHOLD, y_dtype=torch.float32)
+    np.testing.assert_array_equal(layer.modes.cpu().numpy(), np.full(16, 2, np.uint8))
+    np.testing.assert_allclose(layer.Y.cpu().numpy(), x.V.cpu().numpy(), rtol=1e-6, atol=1e-7)
+    np.testing.assert_allclose(layer.state.score.cpu().numpy(), 1.0, rtol=1e-6)
+
+
+# --------------------------------------------------- threshold rule (Eq.4)
+
+def planted_inputs(N, targets, dtype, seed=0):
+    """All queries equal within a head (q_pool = q), one planted key per head
+    with logit L_h chosen so that s_h = targets[h]; see the oracle pins."""
+    H = len(targets)
+    rng = np.random.default_rng(seed)
+    Q = np.zeros((N, H, 64), np.float32)
+    Q[:, :, 0] = 1.0
+    K = (rng.normal(size=(N, H, 64)) * 0.125).astype(np.float32)
+    K[:, :, 0] = 0.0
+    V = (rng.normal(size=(N, H, 64)) * 0.125).astype(np.float32)
+    for h, s in enumerate(targets):
+        L = math.log(s * (N - 1) / (1.0 - s))
+        K[(h * 97) % N, h, 0] = 8.0 * L
+    x = synth.make_layer(1, N, dtype=dtype, key=(6, N), H=H, n_full=0)
+    td = synth.torch_dtype(dtype)
+    x.Q = torch.from_numpy(Q).to(td)
+    x.K = torch.from_numpy(K).to(td)
+    x.V = torch.from_numpy(V).to(td)
+    return x
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_threshold_rule_planted_saliency(dtype):
+    N = 2748
+    log("threshold planted %s" % dtype)
+    # at least 4e-3 from tau_low and 2e-2 from tau_high before rounding, so
+    # that bf16 rounding of the planted key (<= 3e-3 in s) keeps 1e-3
+    targets = [0.22, 0.18, 0.014, 0.006, 0.6, 0.05, 0.1, 0.3,
+               0.015, 0.005, 0.25, 0.12, 0.9, 0.02, 0.17, 0.23]
+    x = planted_inputs(N, targets, dtype)
+    ref = oracle_layer(x, rule=oracle.RULE_THRESHOLD)
+    # margins after rounding to the stored dtype
+    assert (np.minimum(np.abs(ref["s"] - 0.2), np.abs(ref["s"] - 0.01)) >= 1e-3).all()
+    layer = run_gpu(x.to("cuda"), rule=oracle.RULE_THRESHOLD, y_dtype=torch.float32)
+    check_router(layer, ref, oracle.RULE_THRESHOLD)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], dtype, False, label="planted")
+
+
+def test_assign_boundaries_and_nan():
+    from paper_2609_23733_amd import vp
+    log("assign boundaries")
+    tl, th = np.float32(0.01), np.float32(0.2)
+    s = np.array([th, tl, np.nextafter(th, 0), np.nextafter(tl, 1), 1.0, 0.0, np.nan, 0.05],
+                 np.float32)
+    modes, buckets = vp.assign_heads(torch.from_numpy(s).cuda(), vp.RULE_THRESHOLD)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(modes.cpu().numpy(), [2, 0, 1, 1, 2, 0, 2, 1])
+    b = buckets.cpu().numpy()
+    np.testing.assert_array_equal(b[:3], [2, 3, 3])
+    np.testing.assert_array_equal(b[3:11], [1, 5, 2, 3, 7, 0, 4, 6])
+    assert b[19] & 1
+    lg = np.array([[1, 1, 0], [0, 2, 2], [3, 3, 3], [0, 0, 1], [np.nan, 0, 0], [-1, -2, -3]],
+                  np.float32)
+    modes, buckets = vp.assign_heads(torch.from_numpy(lg).cuda(), vp.RULE_ARGMAX)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(modes.cpu().numpy(), oracle.assign(lg.astype(np.float64), 1))
+
+
+# ---------------------------------------------------- robustness and order
+
+def test_deterministic_bitwise():
+    log("determinism")
+    x = synth.make_layer(4, 1374, dtype="bf16", key=(7, 0), n_full=6, qkv_device="cuda")
+    a = run_gpu(x)
+    Y1 = a.Y.clone()
+    q1 = a.state.q_pool.clone()
+    a.step()
+    torch.cuda.synchronize()
+    assert torch.equal(Y1, a.Y)
+    assert torch.equal(q1, a.state.q_pool)
+
+
+def test_permutation_equivariance_gpu():
+    log("permutation")
+    modes = np.array([2, 1, 0, 2] * 4, np.uint8)
+    x = synth.make_layer(2, 300, dtype="f32", key=(8, 0), sharp=True, modes=modes,
+                         qkv_device="cuda")
+    a = run_gpu(x, y_dtype=torch.float32)
+    Ya = a.Y.double().cpu().numpy()
+    pi = torch.from_numpy(np.random.default_rng(0).permutation(x.N)).cuda()
+    xp = synth.make_layer(2, 300, dtype="f32", key=(8, 0), sharp=True, modes=modes,
+                          qkv_device="cuda")
+    xp.Q, xp.K, xp.V = x.Q[pi].contiguous(), x.K[pi].contiguous(), x.V[pi].contiguous()
+    b = run_gpu(xp, y_dtype=torch.float32)
+    Yb = b.Y.double().cpu().numpy()
+    ref = Ya[pi.cpu().numpy()]
+    for h in range(16):
+        assert np.abs(Yb[:, h] - ref[:, h]).max() <= 1e-4 * rms(ref[:, h])
+
+
+# ------------------------------------------------- full-size workloads
+
+@pytest.mark.parametrize("wl,n_full", [("s32_bf16", 4), ("s32_bf16", 16), ("s100_bf16", 4),
+                                       ("s100_bf16", 16)])
+def test_full_size_sampled(wl, n_full):
+    """The benchmark workloads at full size, in the benchmark's launch
+    configuration (bf16 operands, bf16 Y): router and modes on all tokens,
+    SURR and MEAN heads on every row, FULL heads on sampled query rows."""
+    cfg = synth.WORKLOADS[wl]
+    log("full size %s n_full=%d" % (wl, n_full))
+    x = synth.make_layer(cfg["S"], dtype="bf16", n_full=n_full, key=(cfg["S"], 0),
+                         qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.bfloat16)
+    rows = synth.sample_rows(x.N, 96, synth.derive_seed(cfg["S"], 0, 20))
+    ref = oracle_layer(x, rows=rows, full_rows_sel=rows)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    Yg = layer.Y[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    full = [h for h in range(16) if ref["modes"][h] == 2]
+    for h in full:
+        ref["Y"][:, h, :] = ref["Y_full_rows"][h]
+    check_y(Yg, ref["Y"], "bf16", True, label="%s/%d" % (wl, n_full))
