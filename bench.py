@@ -81,7 +81,7 @@ def run_workload(S, n_full, steps, warmup, seed_key):
     return rec, layer, x
 
 
-def cpu_baseline(x, rows_per_head=64):
+def cpu_baseline(x, rows_per_head=640):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
     extrapolated linearly to all N rows (every row costs the same)."""

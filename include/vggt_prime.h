@@ -163,13 +163,14 @@ vp_status vp_routed_global_attention(const vp_shape *shape, const void *Q, const
  * requirements as vp_routed_global_attention; run all three, in this order,
  * on one stream, to obtain the same Y).
  *   vp_gather_full_heads:   packs V of each FULL head (bf16 layers; no-op for
- *                           fp32) into the workspace, tile-transposed;
+ *                           fp32) into the workspace, tile-transposed, and
+ *                           records the largest key norm of every 64-key tile;
  *   vp_full_head_attention: exact softmax attention of every FULL head
  *                           (Algorithm 1, first branch); reads the packed
  *                           values the gather left in `ws`;
  *   vp_linear_heads:        SURR (Eq.5-7) and MEAN heads. */
-vp_status vp_gather_full_heads(const vp_shape *shape, const void *V, const int32_t *buckets,
-                               void *ws, size_t ws_bytes, void *stream);
+vp_status vp_gather_full_heads(const vp_shape *shape, const void *K, const void *V,
+                               const int32_t *buckets, void *ws, size_t ws_bytes, void *stream);
 vp_status vp_full_head_attention(const vp_shape *shape, const void *Q, const void *K,
                                  const void *V, const int32_t *buckets, void *Y,
                                  vp_dtype y_dtype, void *ws, size_t ws_bytes, void *stream);

@@ -31,31 +31,49 @@ constexpr int kLdsRow = 72;   // bf16 LDS row stride (144 B: 16-B aligned, bank-
 // ------------------------------------------------------------------------
 // K5: bucket gather.  For each FULL head (slot s of the FULL bucket), copy V_h
 // into a packed, tile-transposed buffer Vt[s][tile][d][64 keys] (keys past N
-// are zero).  The attention kernel then reads V^T tiles as contiguous 8 KB
-// blocks whose rows feed the PV MFMA operand directly.
+// are zero), and record kmax[s][tile] = max |k_j| over the tile's keys.  The
+// attention kernel reads V^T tiles as contiguous 8 KB blocks whose rows feed
+// the PV MFMA operand directly, and uses kmax to bound the tile's logits.
 // ------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ V,
+__global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
+                                                   const bf16* __restrict__ V,
                                                    const int32_t* __restrict__ buckets, int64_t N,
-                                                   int H, int nkt, bf16* __restrict__ Vt) {
+                                                   int H, int nkt, bf16* __restrict__ Vt,
+                                                   float* __restrict__ kmax) {
     const int slot = blockIdx.y, tile = blockIdx.x;
     const int nfull = full_count(buckets, H);
     if (slot >= nfull) return;
     const int h = full_head(buckets, H, slot);
     if (h < 0) return;
     __shared__ __attribute__((aligned(16))) bf16 s[kD * kLdsRow];
+    __shared__ float s_norm[4];
     const int t = threadIdx.x;
     const int key = t >> 2, dseg = (t & 3) * 16;
     const int64_t row = (int64_t)tile * kBK + key;
     const bool ok = row < N;
-    const bf16* src = V + ((ok ? row : 0) * H + h) * kD + dseg;
-    bf16x8 a = load_bf16x8(src), b = load_bf16x8(src + 8);
-    if (!ok) a = b = zero_bf16x8();
+    const int64_t off = ((ok ? row : 0) * H + h) * kD + dseg;
+    bf16x8 a = load_bf16x8(V + off), b = load_bf16x8(V + off + 8);
+    bf16x8 ka = load_bf16x8(K + off), kb = load_bf16x8(K + off + 8);
+    if (!ok) a = b = ka = kb = zero_bf16x8();
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         s[(dseg + j) * kLdsRow + key] = a[j];
         s[(dseg + 8 + j) * kLdsRow + key] = b[j];
     }
+    float n2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const float x = bf16_to_f32(ka[j]), y = bf16_to_f32(kb[j]);
+        n2 = fmaf(x, x, fmaf(y, y, n2));
+    }
+    n2 += __shfl_xor(n2, 1);
+    n2 += __shfl_xor(n2, 2);
+    n2 = wave_max(n2);
+    if ((t & 63) == 0) s_norm[t >> 6] = n2;
     __syncthreads();
+    if (t == 0)
+        kmax[(int64_t)slot * nkt + tile] =
+            sqrtf(fmaxf(fmaxf(s_norm[0], s_norm[1]), fmaxf(s_norm[2], s_norm[3])));
     const int d = t >> 2, kseg = (t & 3) * 16;
     bf16* dst = Vt + (((int64_t)slot * nkt + tile) * kD + d) * kBK + kseg;
     *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(&s[d * kLdsRow + kseg]);
@@ -72,12 +90,28 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ V,
 // stored in LDS with index bits 2 and 3 swapped so that the S^T registers
 // hold eight consecutive keys per lane-half: they become the B operand of the
 // PV MFMA without any data movement.
+//
+// Softmax work per score is one FMA, one exp2, half a bf16 pack and half a
+// dot2 (row sums of the packed P).  The running maximum m is a reference
+// point, not necessarily the exact maximum: a tile whose logits provably stay
+// below m + 8 (in log2 units; Cauchy-Schwarz, |q . k| c <= |q| c max|k|) is
+// exponentiated against m directly, so p <= 2^8.  Only otherwise is the tile
+// maximum computed, and m moves (rescaling O and l) only when the tile
+// exceeds m + 8.  O / l is unchanged by the choice of reference point.
 // ------------------------------------------------------------------------
 constexpr int kBQ16 = 256;
+constexpr float kSlack = 8.f;   // log2 headroom above the reference point
+
+__device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
+    const bf16x2 v = __builtin_bit_cast(bf16x2, pair);
+    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
+}
 
 __global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ Q,
                                                        const bf16* __restrict__ K,
                                                        const bf16* __restrict__ Vt,
+                                                       const float* __restrict__ kmax,
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        void* __restrict__ Y, int ydt) {
@@ -94,25 +128,36 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ 
     __shared__ __attribute__((aligned(16))) bf16 sK[2][kBK * kLdsRow];
     __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kLdsRow];
 
-    // Q^T operands of this wave's two 32-query blocks, kept in registers.
+    // Q^T operands of this wave's two 32-query blocks, kept in registers,
+    // and |q| * c per query for the logit bound.
     bf16x8 Qop[2][4];
     int64_t qidx[2];
+    float qnc[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const int64_t qi = (int64_t)qt * kBQ16 + wave * 64 + qb * 32 + n;
         qidx[qb] = qi;
         const bool ok = qi < N;
         const bf16* qp = Q + ((ok ? qi : 0) * H + h) * kD + 8 * hh;
+        float n2 = 0.f;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
             Qop[qb][ks] = load_bf16x8(qp + 16 * ks);
             if (!ok) Qop[qb][ks] = zero_bf16x8();
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float x = bf16_to_f32(Qop[qb][ks][j]);
+                n2 = fmaf(x, x, n2);
+            }
         }
+        n2 += __shfl_xor(n2, 32);
+        qnc[qb] = sqrtf(n2) * c;
     }
 
     // Global -> LDS copy assignment: 64 rows x 4 segments of 16 elements.
     const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
     const bf16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
+    const float* kmx = kmax + (int64_t)slot * nkt;
     bf16x8 pk0, pk1, pv0, pv1;
     auto gload = [&](int t) {
         const int64_t key = (int64_t)t * kBK + lr;
@@ -149,72 +194,74 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ 
 
     for (int t = 0; t < nkt; ++t) {
         const int buf = t & 1;
+        const float kbound = kmx[t];
         if (t + 1 < nkt) gload(t + 1);
 
-        // S^T = K Q^T
-        f32x16 S[2][2];
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) S[qb][0] = S[qb][1] = zero_f32x16();
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                    &sK[buf][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
-#pragma unroll
-                for (int qb = 0; qb < 2; ++qb) S[qb][kb] = mfma_bf16(a, Qop[qb][ks], S[qb][kb]);
-            }
-
-        if ((int64_t)(t + 1) * kBK > N) {   // ragged last tile: mask keys >= N
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int64_t key =
-                        (int64_t)t * kBK + kb * 32 + 16 * (r >> 3) + 8 * hh + (r & 7);
-                    if (key >= N) {
-                        S[0][kb][r] = -INFINITY;
-                        S[1][kb][r] = -INFINITY;
-                    }
-                }
-        }
-
-        // Online softmax (base 2; c = log2(e) / sqrt(d)), P packed to bf16.
+        // Per 32-query block: S^T = K Q^T, then its probabilities.  Blocks are
+        // done one after the other to keep one S^T live (the K operand is
+        // re-read from LDS for the second block).
+        const bool last = (int64_t)(t + 1) * kBK > N;
         bf16x8 P[2][2][2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-            float mx = -INFINITY;
+            f32x16 S[2];
+            S[0] = S[1] = zero_f32x16();
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[qb][kb][r]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float mn = fmaxf(m[qb], mx * c);
-            const float al = exp2f_fast(m[qb] - mn);
-            m[qb] = mn;
-            l[qb] *= al;
-#pragma unroll
-            for (int db = 0; db < 2; ++db)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) O[qb][db][r] *= al;
-            float ls = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const float p = exp2f_fast(fmaf(S[qb][kb][r], c, -mn));
-                    S[qb][kb][r] = p;
-                    ls += p;
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                        &sK[buf][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
+                    S[kb] = mfma_bf16(a, Qop[qb][ks], S[kb]);
                 }
-            l[qb] += ls;
+            if (last) {   // ragged last tile: mask keys >= N
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int64_t key =
+                            (int64_t)t * kBK + kb * 32 + 16 * (r >> 3) + 8 * hh + (r & 7);
+                        if (key >= N) S[kb][r] = -INFINITY;
+                    }
+            }
+            // Reference point: keep m unless the bound cannot rule out a
+            // logit above m + kSlack for some query of this block.
+            if (__builtin_amdgcn_ballot_w64(qnc[qb] * kbound > m[qb] + kSlack) != 0) {
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[kb][r]);
+                mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+                const bool move = mx > m[qb] + kSlack;
+                const float mn = move ? mx : m[qb];
+                const float al = move ? exp2f_fast(m[qb] - mn) : 1.f;
+                m[qb] = mn;
+                l[qb] *= al;
+#pragma unroll
+                for (int db = 0; db < 2; ++db)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) O[qb][db][r] *= al;
+            }
+            // p = 2^(s c - m), packed to bf16; row sums from the packed values.
+            const float nm = -m[qb];
+            float ls = l[qb];
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    P[qb][kb][b] = pack_bf16x8(S[qb][kb][8 * b], S[qb][kb][8 * b + 1],
-                                               S[qb][kb][8 * b + 2], S[qb][kb][8 * b + 3],
-                                               S[qb][kb][8 * b + 4], S[qb][kb][8 * b + 5],
-                                               S[qb][kb][8 * b + 6], S[qb][kb][8 * b + 7]);
+                for (int b = 0; b < 2; ++b) {
+                    u32x4 pk;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        f32x2 e;
+                        e[0] = exp2f_fast(fmaf(S[kb][8 * b + 2 * j], c, nm));
+                        e[1] = exp2f_fast(fmaf(S[kb][8 * b + 2 * j + 1], c, nm));
+                        pk[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, bf16x2));
+                        ls = dot2_ones(pk[j], ls);
+                    }
+                    P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
+                }
+            l[qb] = ls;
         }
 
         // O^T += V^T P^T
@@ -412,8 +459,8 @@ int flash_q_tile(int dtype) { return dtype == DT_BF16 ? kBQ16 : kBQ32; }
 
 void launch_gather(const AttnArgs& a, hipStream_t st) {
     const int nkt = (int)((a.N + kBK - 1) / kBK);
-    hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.V,
-                       a.buckets, a.N, a.H, nkt, (bf16*)a.vt);
+    hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.K,
+                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (bf16*)a.vt, a.kmax);
 }
 
 void launch_flash(const AttnArgs& a, hipStream_t st) {
@@ -423,8 +470,8 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
     const int nqt = (int)((a.N + bq - 1) / bq);
     if (a.dtype == DT_BF16)
         hipLaunchKernelGGL(k_flash_bf16, dim3(nqt * a.H), dim3(256), 0, st, (const bf16*)a.Q,
-                           (const bf16*)a.K, (const bf16*)a.vt, a.buckets, a.N, a.H, nqt, nkt, c,
-                           a.Y, a.ydt);
+                           (const bf16*)a.K, (const bf16*)a.vt, (const float*)a.kmax, a.buckets,
+                           a.N, a.H, nqt, nkt, c, a.Y, a.ydt);
     else
         hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,

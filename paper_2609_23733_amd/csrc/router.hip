@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
             for (int nn = 0; nn < 32; ++nn) sa += s_acc[wv2][32 * dh + nn][8 * ks + j];
             A += sa * sc;
         }
-        float* o = part + ((int64_t)c * H + h) * (2 + kD);
+        float* o = part + ((int64_t)h * gridDim.x + c) * (2 + kD);
         if (d == 0) {
             o[0] = M;
             o[1] = L;
@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restric
             L += s_red[wv][1] * s2;
             A += s_red[wv][2 + d] * s2;
         }
-        float* o = part + ((int64_t)c * H + h) * (2 + kD);
+        float* o = part + ((int64_t)h * gridDim.x + c) * (2 + kD);
         if (d == 0) {
             o[0] = MM;
             o[1] = L;
@@ -226,20 +226,69 @@ __global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restric
     }
 }
 
-// K9a: q_pool_h = (sum_c 2^(m_c - M) acc_c) / (sum_c 2^(m_c - M) l_c), chunks in order.
-__global__ __launch_bounds__(64) void k_pool_combine(const float* __restrict__ part, int nchunks,
-                                                     int H, float* __restrict__ q_pool) {
-    const int h = blockIdx.x, d = threadIdx.x;
+// Combine of per-chunk online-softmax partials (m_c, l_c, a_c[...]) of one
+// head: M = max_c m_c, w_c = 2^(m_c - M), L = sum_c w_c l_c,
+// A = sum_c w_c a_c (and, when `plain` is set, an unweighted sum of a second
+// vector).  256 threads: thread (d, g) sums the g-th quarter of the chunks in
+// order for feature d; quarters and the L partials are then added in a fixed
+// order, so the result does not depend on scheduling.
+struct Combined {
+    float M, L;
+};
+
+template <int NV>
+__device__ Combined combine_chunks(const float* __restrict__ part, int nchunks, int stride,
+                                   float (&acc)[NV]) {
+    __shared__ float s_w[1024];
+    __shared__ float s_red[4][kD * NV];
+    __shared__ float s_ml[8];
+    const int t = threadIdx.x, d = t & 63, g = t >> 6;
     float M = -INFINITY;
-    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, part[((int64_t)c * H + h) * (2 + kD)]);
-    float L = 0.f, A = 0.f;
-    for (int c = 0; c < nchunks; ++c) {
-        const float* p = part + ((int64_t)c * H + h) * (2 + kD);
-        const float sc = (p[0] == -INFINITY) ? 0.f : exp2f_fast(p[0] - M);
-        L += p[1] * sc;
-        A += p[2 + d] * sc;
+    for (int c = t; c < nchunks; c += 256) M = fmaxf(M, part[(int64_t)c * stride]);
+    M = wave_max(M);
+    if ((t & 63) == 0) s_ml[t >> 6] = M;
+    __syncthreads();
+    M = fmaxf(fmaxf(s_ml[0], s_ml[1]), fmaxf(s_ml[2], s_ml[3]));
+    for (int c = t; c < nchunks; c += 256) {
+        const float mc = part[(int64_t)c * stride];
+        s_w[c] = (mc == -INFINITY) ? 0.f : exp2f_fast(mc - M);
     }
-    q_pool[h * kD + d] = A / L;
+    __syncthreads();
+    const int q = (nchunks + 3) >> 2;
+    const int c0 = g * q, c1 = (c0 + q < nchunks) ? c0 + q : nchunks;
+    float a[NV], lsum = 0.f;
+#pragma unroll
+    for (int v = 0; v < NV; ++v) a[v] = 0.f;
+#pragma unroll 4
+    for (int c = c0; c < c1; ++c) {
+        const float* p = part + (int64_t)c * stride;
+        const float w = s_w[c];
+        if (d == 0) lsum = fmaf(p[1], w, lsum);
+        a[0] = fmaf(p[2 + d], w, a[0]);
+        if (NV > 1) a[NV - 1] += p[2 + kD + d];
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v) s_red[g][v * kD + d] = a[v];
+    if (d == 0) s_ml[4 + g] = lsum;
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+        acc[v] = ((s_red[0][v * kD + d] + s_red[1][v * kD + d]) + s_red[2][v * kD + d]) +
+                 s_red[3][v * kD + d];
+    Combined r;
+    r.M = M;
+    r.L = ((s_ml[4] + s_ml[5]) + s_ml[6]) + s_ml[7];
+    return r;
+}
+
+// K9a: q_pool_h = (sum_c w_c acc_c) / (sum_c w_c l_c).
+__global__ __launch_bounds__(256) void k_pool_combine(const float* __restrict__ part, int nchunks,
+                                                      float* __restrict__ q_pool) {
+    const int h = blockIdx.x;
+    float acc[1];
+    const Combined r =
+        combine_chunks<1>(part + (int64_t)h * nchunks * (2 + kD), nchunks, 2 + kD, acc);
+    if (threadIdx.x < kD) q_pool[h * kD + threadIdx.x] = acc[0] / r.L;
 }
 
 // ------------------------------------------------------------------------
@@ -338,7 +387,7 @@ __global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ 
                 SS[j] += s_s[src][j];
             }
         }
-        float* o = part + ((int64_t)c * H + h) * (2 + 2 * kD);
+        float* o = part + ((int64_t)h * gridDim.x + c) * (2 + 2 * kD);
         if (seg == 0) {
             o[0] = M;
             o[1] = L;
@@ -351,30 +400,24 @@ __global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ 
     }
 }
 
-// K9b: per head, combine chunks in order; write stats, score, ctx, vmean.
-__global__ __launch_bounds__(64) void k_route_combine(const float* __restrict__ part, int nchunks,
-                                                      int H, int64_t N, float* __restrict__ stats,
-                                                      float* __restrict__ score,
-                                                      float* __restrict__ ctx,
-                                                      float* __restrict__ vmean) {
+// K9b: per head, combine the routing partials; write stats, score, ctx, vmean.
+__global__ __launch_bounds__(256) void k_route_combine(const float* __restrict__ part, int nchunks,
+                                                       int64_t N, float* __restrict__ stats,
+                                                       float* __restrict__ score,
+                                                       float* __restrict__ ctx,
+                                                       float* __restrict__ vmean) {
     const int h = blockIdx.x, d = threadIdx.x;
-    const int stride = 2 + 2 * kD;
-    float M = -INFINITY;
-    for (int c = 0; c < nchunks; ++c) M = fmaxf(M, part[((int64_t)c * H + h) * stride]);
-    float L = 0.f, C = 0.f, Sv = 0.f;
-    for (int c = 0; c < nchunks; ++c) {
-        const float* p = part + ((int64_t)c * H + h) * stride;
-        const float sc = (p[0] == -INFINITY) ? 0.f : exp2f_fast(p[0] - M);
-        L += p[1] * sc;
-        C += p[2 + d] * sc;
-        Sv += p[2 + kD + d];
+    float acc[2];
+    const Combined r = combine_chunks<2>(part + (int64_t)h * nchunks * (2 + 2 * kD), nchunks,
+                                         2 + 2 * kD, acc);
+    if (d < kD) {
+        ctx[h * kD + d] = acc[0] / r.L;
+        vmean[h * kD + d] = acc[1] / (float)N;
     }
-    ctx[h * kD + d] = C / L;
-    vmean[h * kD + d] = Sv / (float)N;
     if (d == 0) {
-        stats[2 * h] = M * kLn2;
-        stats[2 * h + 1] = L;
-        score[h] = 1.f / L;
+        stats[2 * h] = r.M * kLn2;
+        stats[2 * h + 1] = r.L;
+        score[h] = 1.f / r.L;
     }
 }
 
@@ -461,7 +504,7 @@ void launch_router(const RouterArgs& a, hipStream_t st) {
         hipLaunchKernelGGL(k_pool_partial_f32, g1, dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.W, (const float*)a.U, (const float*)a.w, a.N, a.H,
                            a.chunk1, a.part1);
-    hipLaunchKernelGGL(k_pool_combine, dim3(a.H), dim3(64), 0, st, a.part1, (int)a.n1, a.H,
+    hipLaunchKernelGGL(k_pool_combine, dim3(a.H), dim3(256), 0, st, a.part1, (int)a.n1,
                        a.q_pool);
     if (a.dtype == DT_BF16)
         hipLaunchKernelGGL(k_route_partial<DT_BF16>, dim3((unsigned)a.n2), dim3(256), 0, st, a.K,
@@ -469,7 +512,7 @@ void launch_router(const RouterArgs& a, hipStream_t st) {
     else
         hipLaunchKernelGGL(k_route_partial<DT_F32>, dim3((unsigned)a.n2), dim3(256), 0, st, a.K,
                            a.V, a.q_pool, a.scale, a.N, a.H, a.chunk2, a.part2);
-    hipLaunchKernelGGL(k_route_combine, dim3(a.H), dim3(64), 0, st, a.part2, (int)a.n2, a.H, a.N,
+    hipLaunchKernelGGL(k_route_combine, dim3(a.H), dim3(256), 0, st, a.part2, (int)a.n2, a.N,
                        a.stats, a.score, a.ctx, a.vmean);
 }
 

@@ -24,7 +24,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 struct Layout {
     int64_t N;
     int64_t n1, chunk1, n2, chunk2, nkt;
-    size_t off_part1, off_part2, off_vt, total;
+    size_t off_part1, off_part2, off_vt, off_kmax, total;
 };
 
 // Chunking of the router reductions and the workspace carve-up; a pure
@@ -41,7 +41,7 @@ bool make_layout(const vp_shape* s, Layout* L) {
     c1 = c1 < 256 ? 256 : cdiv(c1, 128) * 128;
     L->chunk1 = c1;
     L->n1 = cdiv(N, c1);
-    int64_t c2 = cdiv(N, 1024);
+    int64_t c2 = cdiv(N, 512);
     L->chunk2 = c2 < 64 ? 64 : c2;
     L->n2 = cdiv(N, L->chunk2);
     L->nkt = cdiv(N, 64);
@@ -52,6 +52,8 @@ bool make_layout(const vp_shape* s, Layout* L) {
     off = align_up(off + (size_t)L->n2 * s->H * (2 + 2 * VP_HEAD_DIM) * sizeof(float));
     L->off_vt = off;
     if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * 64 * 64 * 2);
+    L->off_kmax = off;
+    if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * sizeof(float));
     L->total = off;
     return true;
 }
@@ -218,6 +220,7 @@ vp::AttnArgs attn_args(const vp_shape* shape, const Layout& L, const void* Q, co
     a.N = L.N;
     a.H = shape->H;
     a.vt = ws ? (char*)ws + L.off_vt : nullptr;
+    a.kmax = ws ? (float*)((char*)ws + L.off_kmax) : nullptr;
     a.Y = Y;
     return a;
 }
@@ -232,16 +235,17 @@ void set_linear(vp::AttnArgs& a, const vp_router_state* state, const vp_surrogat
 
 }  // namespace
 
-vp_status vp_gather_full_heads(const vp_shape* shape, const void* V, const int32_t* buckets,
-                               void* ws, size_t ws_bytes, void* stream) {
+vp_status vp_gather_full_heads(const vp_shape* shape, const void* K, const void* V,
+                               const int32_t* buckets, void* ws, size_t ws_bytes, void* stream) {
     vp_status st = shape_status(shape);
     if (st != VP_OK) return st;
-    if (!V || !aligned16(V) || !buckets || ((uintptr_t)buckets & 3u)) return VP_ERR_INVALID_ARG;
+    if (!K || !V || !aligned16(K) || !aligned16(V) || !buckets || ((uintptr_t)buckets & 3u))
+        return VP_ERR_INVALID_ARG;
     Layout L;
     if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
     if (shape->dtype != VP_BF16) return VP_OK;
     (void)hipGetLastError();
-    vp::AttnArgs a = attn_args(shape, L, nullptr, nullptr, V, nullptr, buckets, nullptr, VP_F32, ws);
+    vp::AttnArgs a = attn_args(shape, L, nullptr, K, V, nullptr, buckets, nullptr, VP_F32, ws);
     vp::launch_gather(a, (hipStream_t)stream);
     return hip_status("vp_gather_full_heads");
 }

@@ -77,7 +77,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                                ctypes.POINTER(vp_router_state),
                                                ctypes.POINTER(vp_surrogate_weights), P,
                                                ctypes.c_int, P, ctypes.c_size_t, P]
-    lib.vp_gather_full_heads.argtypes = [ctypes.POINTER(vp_shape), P, P, P, ctypes.c_size_t, P]
+    lib.vp_gather_full_heads.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, ctypes.c_size_t,
+                                         P]
     lib.vp_full_head_attention.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P, ctypes.c_int,
                                            P, ctypes.c_size_t, P]
     lib.vp_linear_heads.argtypes = [ctypes.POINTER(vp_shape), P, P,
@@ -272,13 +273,14 @@ def routed_global_attention(Q, K, V, modes, buckets, state: RouterState,
     return Y
 
 
-def gather_full_heads(V, buckets, S: int, P: int, ws: torch.Tensor):
+def gather_full_heads(K, V, buckets, S: int, P: int, ws: torch.Tensor):
     """Stage 1 of routed_global_attention: pack V of the FULL heads."""
     N, H = S * P, V.shape[1]
+    _need(K, "K", (N, H, HEAD_DIM), V.dtype)
     _need(V, "V", (N, H, HEAD_DIM))
     _need(buckets, "buckets", (BUCKETS_LEN,), torch.int32)
     shp = make_shape(S, P, H, V.dtype)
-    _check(load_library().vp_gather_full_heads(ctypes.byref(shp), _ptr(V), _ptr(buckets),
+    _check(load_library().vp_gather_full_heads(ctypes.byref(shp), _ptr(K), _ptr(V), _ptr(buckets),
                                                _ptr(ws), ws.numel() * ws.element_size(),
                                                _stream()), "vp_gather_full_heads")
 
@@ -349,7 +351,7 @@ class RoutedLayer:
                                     self.S, self.P, self.ws, self.y_dtype, self.act, self.Y)
         else:
             # the same three stages, with events bracketing the FULL-head kernel
-            gather_full_heads(V, self.buckets, self.S, self.P, self.ws)
+            gather_full_heads(K, V, self.buckets, self.S, self.P, self.ws)
             events[0].record()
             full_head_attention(Q, K, V, self.buckets, self.S, self.P, self.ws, self.Y)
             events[1].record()
