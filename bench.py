@@ -26,6 +26,34 @@ PEAK_HBM_GBS = 8000.0
 P_TOKENS = 1374
 HEADS, D, L = 16, 64, 64
 
+# HBM traffic of k_flash_bf16 on the headline workload (S=100, 4 FULL heads),
+# from two rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per
+# dispatch) over this bench, each scaled by the same counter on a plain 1 GiB
+# device-to-device copy (bench.py --copy-calibration): the copy reads FETCH_SIZE
+# = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
+# written (x1.0).  Valid only for the kernel source it was measured on.
+FLASH_TRAFFIC = {
+    "source_sha256": "e8848f67b40c8667626bc4b6166341cd77d438cbf8cdf94fa7f7183a15748a78",
+    "S": 100, "n_full": 4,
+    "fetch_kib": 1309327, "write_kib": 68700,
+    "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
+}
+
+
+def flash_traffic(S, n_full):
+    """Measured HBM bytes per launch of the FULL-head kernel, or None when the
+    kernel source or the workload differs from the measured one."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2609_23733_amd", "csrc", "flash.hip")
+    t = FLASH_TRAFFIC
+    if (S, n_full) != (t["S"], t["n_full"]):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != t["source_sha256"]:
+        return None
+    fetch = t["fetch_kib"] * 1024 * t["copy_bytes"] / (t["copy_fetch_kib"] * 1024)
+    write = t["write_kib"] * 1024 * t["copy_bytes"] / (t["copy_write_kib"] * 1024)
+    return int(round(fetch + write))
+
 
 def flops_full(N, n_full):
     """Algorithmic FULL-head work: QK^T and PV, 2 * N^2 * d each."""
@@ -122,6 +150,9 @@ def main():
     ap.add_argument("--n-full", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy three times (the "
+                         "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -130,6 +161,14 @@ def main():
 
     import torch
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": 1 << 30, "launches": 3}))
+        return
     from paper_2609_23733_amd import vp
     vp.load_library()
 
@@ -174,7 +213,8 @@ def main():
         "frac_bf16_peak": head["frac_bf16_peak"],
         "roofline": {"kernel": "k_flash_bf16", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": flash_traffic(100, head["n_full"]),
                      "algorithmic_flop_per_launch": ff,
                      "avg_launch_ms": round(head["full_kernel_ms"], 4)},
         "by_workload": by,

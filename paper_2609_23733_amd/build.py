@@ -23,6 +23,9 @@ ARCH = "gfx950"
 CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in arch VGPRs: the softmax reads S directly instead of
+    # copying it out of accumulation registers every tile.
+    "-mllvm", "-amdgpu-mfma-vgpr-form=true",
 ]
 
 

@@ -159,13 +159,14 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ 
     const bf16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
     const float* kmx = kmax + (int64_t)slot * nkt;
     bf16x8 pk0, pk1, pv0, pv1;
+    // Keys past N read row 0 instead (always in bounds); their logits are
+    // masked to -inf in the last tile, so their values never matter.  (No
+    // select on the loaded data: it would stall on the prefetch.)
     auto gload = [&](int t) {
         const int64_t key = (int64_t)t * kBK + lr;
-        const bool ok = key < N;
-        const bf16* kp = K + ((ok ? key : 0) * H + h) * kD + lc;
+        const bf16* kp = K + ((key < N ? key : 0) * H + h) * kD + lc;
         pk0 = load_bf16x8(kp);
         pk1 = load_bf16x8(kp + 8);
-        if (!ok) pk0 = pk1 = zero_bf16x8();
         const bf16* vp = Vth + ((int64_t)t * kD + lr) * kBK + lc;
         pv0 = load_bf16x8(vp);
         pv1 = load_bf16x8(vp + 8);
@@ -346,30 +347,25 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
     }
 
     const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
-    float4 pk[4], pv[4];
+    // Keys past N read row 0 (in bounds); their logits are masked to -inf,
+    // so they get weight exactly 0 (inputs are finite).
+    float4 pk0, pk1, pk2, pk3, pv0, pv1, pv2, pv3;
     auto gload = [&](int t) {
         const int64_t key = (int64_t)t * kBK + lr;
-        const bool ok = key < N;
-        const float4* kp = reinterpret_cast<const float4*>(K + ((ok ? key : 0) * H + h) * kD + lc);
-        const float4* vp = reinterpret_cast<const float4*>(V + ((ok ? key : 0) * H + h) * kD + lc);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            pk[i] = kp[i];
-            pv[i] = vp[i];
-            if (!ok) {   // component-wise: a whole-float4 select here crashes hipcc 7.2
-                pk[i].x = 0.f; pk[i].y = 0.f; pk[i].z = 0.f; pk[i].w = 0.f;
-                pv[i].x = 0.f; pv[i].y = 0.f; pv[i].z = 0.f; pv[i].w = 0.f;
-            }
-        }
+        const int64_t row = key < N ? key : 0;
+        const float4* kp = reinterpret_cast<const float4*>(K + (row * H + h) * kD + lc);
+        const float4* vp = reinterpret_cast<const float4*>(V + (row * H + h) * kD + lc);
+        pk0 = kp[0]; pk1 = kp[1]; pk2 = kp[2]; pk3 = kp[3];
+        pv0 = vp[0]; pv1 = vp[1]; pv2 = vp[2]; pv3 = vp[3];
+    };
+    auto put4 = [](float* d, float4 v) {
+        d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
     };
     auto lstore = [&](int buf) {
         float* kd = &sK[buf][lr * kKRow32 + lc];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            kd[4 * i] = pk[i].x; kd[4 * i + 1] = pk[i].y;
-            kd[4 * i + 2] = pk[i].z; kd[4 * i + 3] = pk[i].w;
-            *reinterpret_cast<float4*>(&sV[buf][lr * kD + lc + 4 * i]) = pv[i];
-        }
+        put4(kd, pk0); put4(kd + 4, pk1); put4(kd + 8, pk2); put4(kd + 12, pk3);
+        float4* vd = reinterpret_cast<float4*>(&sV[buf][lr * kD + lc]);
+        vd[0] = pv0; vd[1] = pv1; vd[2] = pv2; vd[3] = pv3;
     };
 
     f32x16 O[2] = {zero_f32x16(), zero_f32x16()};
