@@ -30,15 +30,18 @@ constexpr int kLdsRow = 72;   // bf16 LDS row stride (144 B: 16-B aligned, bank-
 
 // ------------------------------------------------------------------------
 // K5: bucket gather.  For each FULL head (slot s of the FULL bucket), copy V_h
-// into a packed, tile-transposed buffer Vt[s][tile][d][64 keys] (keys past N
-// are zero), and record kmax[s][tile] = max |k_j| over the tile's keys.  The
-// attention kernel reads V^T tiles as contiguous 8 KB blocks whose rows feed
-// the PV MFMA operand directly, and uses kmax to bound the tile's logits.
+// into a packed, tile-transposed buffer Vt[s][tile][d][64 keys], K_h into
+// packed fp16 tiles Kh[s][tile][64 keys][d] (key rows in swap23 order; bf16
+// values convert exactly while |k| stays in fp16's normal range), keys past N
+// zero in both, and record kmax[s][tile] = max |k_j| over the tile's keys.
+// The attention kernels read the tiles as contiguous 8 KB blocks whose rows
+// feed the MFMA operands directly, and use kmax to bound the logits.
 // ------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
                                                    const bf16* __restrict__ V,
                                                    const int32_t* __restrict__ buckets, int64_t N,
                                                    int H, int nkt, bf16* __restrict__ Vt,
+                                                   f16* __restrict__ Kh,
                                                    float* __restrict__ kmax) {
     const int slot = blockIdx.y, tile = blockIdx.x;
     const int nfull = full_count(buckets, H);
@@ -61,11 +64,17 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
         s[(dseg + 8 + j) * kLdsRow + key] = b[j];
     }
     float n2 = 0.f;
+    f16x8 ha, hb;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const float x = bf16_to_f32(ka[j]), y = bf16_to_f32(kb[j]);
+        ha[j] = (f16)x;
+        hb[j] = (f16)y;
         n2 = fmaf(x, x, fmaf(y, y, n2));
     }
+    f16* kd = Kh + (((int64_t)slot * nkt + tile) * kBK + swap23(key)) * kD + dseg;
+    *reinterpret_cast<f16x8*>(kd) = ha;
+    *reinterpret_cast<f16x8*>(kd + 8) = hb;
     n2 += __shfl_xor(n2, 1);
     n2 += __shfl_xor(n2, 2);
     n2 = wave_max(n2);
@@ -82,7 +91,250 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 }
 
 // ------------------------------------------------------------------------
-// K6 (bf16): one workgroup = 4 waves x 64 queries of one FULL head.
+// K6 (bf16): FULL-head attention, one workgroup = 4 waves x 64 queries of one
+// FULL head.  Per 64-key tile and wave:  S^T = K Q^T  (keys x queries, 2 x 2
+// blocks of 32x32, 16 MFMAs), softmax weights in registers, O^T += V^T P^T
+// (d x queries, 16 MFMAs).  Each lane owns one query column of every block,
+// so softmax row statistics stay in the lane plus one exchange with lane ^ 32.
+// K rows sit in LDS with index bits 2 and 3 swapped so that the S^T registers
+// hold eight consecutive keys per lane-half: they become the B operand of the
+// PV MFMA without any data movement.
+//
+// Softmax is invariant to the reference point subtracted from the logits
+// before exponentiation.  K6a uses zero: when Cauchy-Schwarz bounds every
+// logit of a workgroup's queries by kFastBound in log2 units
+// (|q . k| c <= |c q| max_j |k_j|), p = 2^x stays within [2^-32, 2^32] and a
+// score costs one exp2, half a bf16 pack and half a dot2 (row sums of the
+// packed P).  The scale c = log2(e) / sqrt(d) is folded into Q, rounded to
+// fp16 (relative error 2^-11; K converts exactly), so S comes out of an fp16
+// MFMA in log2 units.  Work items outside that bound (or outside fp16's safe
+// range) are flagged and left to K6b, which keeps bf16 Q and K exact, scales
+// in fp32 and carries a running reference point m: a tile whose logits
+// provably stay below m + kSlack is exponentiated against m directly
+// (p <= 2^8); only otherwise is the tile maximum computed, and m moves
+// (rescaling O and l) only when the tile exceeds m + kSlack.
+// ------------------------------------------------------------------------
+constexpr int kBQ16 = 256;
+constexpr float kSlack = 8.f;        // log2 headroom above a running reference point
+constexpr float kFastBound = 32.f;   // |logit| bound (log2 units) for reference point 0
+constexpr float kF16Safe = 4096.f;   // |c q|, |k| limit for the fp16 logit path
+
+__device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
+    const bf16x2 v = __builtin_bit_cast(bf16x2, pair);
+    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
+}
+
+// Y[q, h, d] = O / l for the wave's two 32-query blocks; lane holds
+// d = 32 db + 8 g + 4 hh + i for i = 0..3.
+__device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float (&l)[2],
+                                           const int64_t (&qidx)[2], int64_t N, int H, int h,
+                                           int hh, void* __restrict__ Y, int ydt) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float lt = l[qb] + __shfl_xor(l[qb], 32);
+        const float inv = 1.f / lt;
+        const int64_t qi = qidx[qb];
+        if (qi < N) {
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int64_t off = (qi * H + h) * kD + db * 32 + 8 * g + 4 * hh;
+                    const float y0 = O[qb][db][4 * g] * inv, y1 = O[qb][db][4 * g + 1] * inv;
+                    const float y2 = O[qb][db][4 * g + 2] * inv, y3 = O[qb][db][4 * g + 3] * inv;
+                    if (ydt == DT_BF16) {
+                        bf16x4 v;
+                        v[0] = (bf16)y0; v[1] = (bf16)y1; v[2] = (bf16)y2; v[3] = (bf16)y3;
+                        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + off) = v;
+                    } else {
+                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off) =
+                            make_float4(y0, y1, y2, y3);
+                    }
+                }
+        }
+    }
+}
+
+// K6a: reference point 0, fp16 logits.  Writes wide_items[L] for every work
+// item it owns (1 = left to K6b), so the flags never carry over between calls.
+__global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ Q,
+                                                       const f16* __restrict__ Kh,
+                                                       const bf16* __restrict__ Vt,
+                                                       const float* __restrict__ kmax,
+                                                       const int32_t* __restrict__ buckets,
+                                                       int64_t N, int H, int nqt, int nkt, float c,
+                                                       int32_t* __restrict__ wide_items,
+                                                       void* __restrict__ Y, int ydt) {
+    const int nfull = full_count(buckets, H);
+    const int active = nfull * nqt;
+    if ((int)blockIdx.x >= active) return;
+    const int L = xcd_remap(blockIdx.x, active);
+    const int slot = L / nqt, qt = L - slot * nqt;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+
+    __shared__ __attribute__((aligned(16))) f16 sK[2][kBK * kLdsRow];
+    __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kLdsRow];
+    __shared__ float sKmax[4];
+    __shared__ int sWide[4];
+
+    // max_j |k_j| over the head, from the per-tile maxima.
+    const float* kmx = kmax + (int64_t)slot * nkt;
+    {
+        float km = 0.f;
+        for (int i = threadIdx.x; i < nkt; i += 256) km = fmaxf(km, kmx[i]);
+        km = wave_max(km);
+        if (lane == 0) sKmax[wave] = km;
+    }
+
+    // (c Q)^T operands of this wave's two 32-query blocks, fp16, kept in
+    // registers, and |c q| per query.
+    f16x8 Qop[2][4];
+    int64_t qidx[2];
+    float qn[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const int64_t qi = (int64_t)qt * kBQ16 + wave * 64 + qb * 32 + n;
+        qidx[qb] = qi;
+        const bool ok = qi < N;
+        const bf16* qp = Q + ((ok ? qi : 0) * H + h) * kD + 8 * hh;
+        float n2 = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            const bf16x8 raw = load_bf16x8(qp + 16 * ks);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float x = ok ? bf16_to_f32(raw[j]) * c : 0.f;
+                Qop[qb][ks][j] = (f16)x;
+                n2 = fmaf(x, x, n2);
+            }
+        }
+        n2 += __shfl_xor(n2, 32);
+        qn[qb] = sqrtf(n2);
+    }
+    __syncthreads();
+    {
+        const float km = fmaxf(fmaxf(sKmax[0], sKmax[1]), fmaxf(sKmax[2], sKmax[3]));
+        const float qm = fmaxf(qn[0], qn[1]);
+        // Written as "not within" so that a NaN norm also goes to K6b.
+        const bool out = !(qm * km <= kFastBound && qm <= kF16Safe && km <= kF16Safe);
+        const bool wave_out = __builtin_amdgcn_ballot_w64(out) != 0;
+        if (lane == 0) sWide[wave] = wave_out;
+    }
+    __syncthreads();
+    const int wide = sWide[0] | sWide[1] | sWide[2] | sWide[3];
+    if (threadIdx.x == 0) wide_items[L] = wide;
+    if (wide) return;
+
+    // Global -> LDS copy assignment: 64 rows x 4 segments of 16 elements of
+    // the packed K and V^T tiles (rows already in LDS order).
+    const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
+    const f16* Khh = Kh + (int64_t)slot * nkt * kBK * kD;
+    const bf16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
+    f16x8 pk0, pk1;
+    bf16x8 pv0, pv1;
+    auto gload = [&](int t) {
+        const f16* kp = Khh + ((int64_t)t * kBK + lr) * kD + lc;
+        pk0 = *reinterpret_cast<const f16x8*>(kp);
+        pk1 = *reinterpret_cast<const f16x8*>(kp + 8);
+        const bf16* vp = Vth + ((int64_t)t * kD + lr) * kBK + lc;
+        pv0 = load_bf16x8(vp);
+        pv1 = load_bf16x8(vp + 8);
+    };
+    auto lstore = [&](int buf) {
+        f16* kd = &sK[buf][lr * kLdsRow + lc];
+        *reinterpret_cast<f16x8*>(kd) = pk0;
+        *reinterpret_cast<f16x8*>(kd + 8) = pk1;
+        bf16* vd = &sV[buf][lr * kLdsRow + lc];
+        *reinterpret_cast<bf16x8*>(vd) = pv0;
+        *reinterpret_cast<bf16x8*>(vd + 8) = pv1;
+    };
+
+    f32x16 O[2][2];
+    float l[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        O[qb][0] = O[qb][1] = zero_f32x16();
+        l[qb] = 0.f;
+    }
+
+    gload(0);
+    lstore(0);
+    __syncthreads();
+
+    for (int t = 0; t < nkt; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < nkt) gload(t + 1);
+
+        const bool last = (int64_t)(t + 1) * kBK > N;
+        bf16x8 P[2][2][2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            f32x16 S[2];
+            S[0] = S[1] = zero_f32x16();
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const f16x8 a = *reinterpret_cast<const f16x8*>(
+                        &sK[buf][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
+                    S[kb] = mfma_f16(a, Qop[qb][ks], S[kb]);
+                }
+            if (last) {   // ragged last tile: keys >= N get weight 0
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int64_t key =
+                            (int64_t)t * kBK + kb * 32 + 16 * (r >> 3) + 8 * hh + (r & 7);
+                        if (key >= N) S[kb][r] = -INFINITY;
+                    }
+            }
+            // p = 2^x, packed to bf16; row sums from the packed values.
+            float ls = l[qb];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    u32x4 pk;
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        f32x2 e;
+                        e[0] = exp2f_fast(S[kb][8 * b + 2 * j]);
+                        e[1] = exp2f_fast(S[kb][8 * b + 2 * j + 1]);
+                        pk[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, bf16x2));
+                        ls = dot2_ones(pk[j], ls);
+                    }
+                    P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
+                }
+            l[qb] = ls;
+        }
+
+        // O^T += V^T P^T
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                        &sV[buf][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
+#pragma unroll
+                    for (int qb = 0; qb < 2; ++qb) O[qb][db] = mfma_bf16(a, P[qb][kb][b], O[qb][db]);
+                }
+
+        if (t + 1 < nkt) lstore(buf ^ 1);
+        __syncthreads();
+    }
+    store_rows(O, l, qidx, N, H, h, hh, Y, ydt);
+}
+
+// ------------------------------------------------------------------------
+// K6b (bf16, wide logit range): one workgroup = 4 waves x 64 queries of one
+// FULL head; runs only the work items that K6a flagged.
 // Per 64-key tile and wave:  S^T = K Q^T  (keys x queries, 2 x 2 blocks of
 // 32x32, 16 MFMAs), online softmax in registers, O^T += V^T P^T (d x queries,
 // 16 MFMAs).  Each lane owns one query column of every block, so softmax row
@@ -99,21 +351,13 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 // maximum computed, and m moves (rescaling O and l) only when the tile
 // exceeds m + 8.  O / l is unchanged by the choice of reference point.
 // ------------------------------------------------------------------------
-constexpr int kBQ16 = 256;
-constexpr float kSlack = 8.f;   // log2 headroom above the reference point
-
-__device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
-    const bf16x2 v = __builtin_bit_cast(bf16x2, pair);
-    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
-    return __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
-}
-
-__global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ Q,
+__global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restrict__ Q,
                                                        const bf16* __restrict__ K,
                                                        const bf16* __restrict__ Vt,
                                                        const float* __restrict__ kmax,
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
+                                                       const int32_t* __restrict__ wide_items,
                                                        void* __restrict__ Y, int ydt) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
@@ -121,7 +365,7 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ 
     const int L = xcd_remap(blockIdx.x, active);
     const int slot = L / nqt, qt = L - slot * nqt;
     const int h = full_head(buckets, H, slot);
-    if (h < 0) return;
+    if (h < 0 || wide_items[L] == 0) return;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int n = lane & 31, hh = lane >> 5;
 
@@ -282,31 +526,7 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ 
         __syncthreads();
     }
 
-    // Y[q, h, d] = O / l; lane holds d = 32 db + 8 g + 4 hh + i for i = 0..3.
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const float lt = l[qb] + __shfl_xor(l[qb], 32);
-        const float inv = 1.f / lt;
-        const int64_t qi = qidx[qb];
-        if (qi < N) {
-#pragma unroll
-            for (int db = 0; db < 2; ++db)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int64_t off = (qi * H + h) * kD + db * 32 + 8 * g + 4 * hh;
-                    const float y0 = O[qb][db][4 * g] * inv, y1 = O[qb][db][4 * g + 1] * inv;
-                    const float y2 = O[qb][db][4 * g + 2] * inv, y3 = O[qb][db][4 * g + 3] * inv;
-                    if (ydt == DT_BF16) {
-                        bf16x4 v;
-                        v[0] = (bf16)y0; v[1] = (bf16)y1; v[2] = (bf16)y2; v[3] = (bf16)y3;
-                        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + off) = v;
-                    } else {
-                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off) =
-                            make_float4(y0, y1, y2, y3);
-                    }
-                }
-        }
-    }
+    store_rows(O, l, qidx, N, H, h, hh, Y, ydt);
 }
 
 // ------------------------------------------------------------------------
@@ -456,7 +676,8 @@ int flash_q_tile(int dtype) { return dtype == DT_BF16 ? kBQ16 : kBQ32; }
 void launch_gather(const AttnArgs& a, hipStream_t st) {
     const int nkt = (int)((a.N + kBK - 1) / kBK);
     hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.K,
-                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (bf16*)a.vt, a.kmax);
+                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (bf16*)a.vt, (f16*)a.kh,
+                       a.kmax);
 }
 
 void launch_flash(const AttnArgs& a, hipStream_t st) {
@@ -464,11 +685,15 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
     const float c = kLog2e / sqrtf((float)kD);
     const int bq = flash_q_tile(a.dtype);
     const int nqt = (int)((a.N + bq - 1) / bq);
-    if (a.dtype == DT_BF16)
+    if (a.dtype == DT_BF16) {
         hipLaunchKernelGGL(k_flash_bf16, dim3(nqt * a.H), dim3(256), 0, st, (const bf16*)a.Q,
-                           (const bf16*)a.K, (const bf16*)a.vt, (const float*)a.kmax, a.buckets,
-                           a.N, a.H, nqt, nkt, c, a.Y, a.ydt);
-    else
+                           (const f16*)a.kh, (const bf16*)a.vt, (const float*)a.kmax, a.buckets,
+                           a.N, a.H, nqt, nkt, c, a.qflag, a.Y, a.ydt);
+        hipLaunchKernelGGL(k_flash_bf16_wide, dim3(nqt * a.H), dim3(256), 0, st,
+                           (const bf16*)a.Q, (const bf16*)a.K, (const bf16*)a.vt,
+                           (const float*)a.kmax, a.buckets, a.N, a.H, nqt, nkt, c, a.qflag, a.Y,
+                           a.ydt);
+    } else
         hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,
                            c, a.Y, a.ydt);

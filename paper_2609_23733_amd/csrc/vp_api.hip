@@ -24,7 +24,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 struct Layout {
     int64_t N;
     int64_t n1, chunk1, n2, chunk2, nkt;
-    size_t off_part1, off_part2, off_vt, off_kmax, total;
+    size_t off_part1, off_part2, off_vt, off_kh, off_kmax, off_qflag, total;
 };
 
 // Chunking of the router reductions and the workspace carve-up; a pure
@@ -52,8 +52,13 @@ bool make_layout(const vp_shape* s, Layout* L) {
     off = align_up(off + (size_t)L->n2 * s->H * (2 + 2 * VP_HEAD_DIM) * sizeof(float));
     L->off_vt = off;
     if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * 64 * 64 * 2);
+    L->off_kh = off;
+    if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * 64 * 64 * 2);
     L->off_kmax = off;
     if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * sizeof(float));
+    L->off_qflag = off;
+    if (s->dtype == VP_BF16)
+        off = align_up(off + (size_t)s->H * cdiv(N, vp::flash_q_tile(VP_BF16)) * sizeof(int32_t));
     L->total = off;
     return true;
 }
@@ -220,7 +225,9 @@ vp::AttnArgs attn_args(const vp_shape* shape, const Layout& L, const void* Q, co
     a.N = L.N;
     a.H = shape->H;
     a.vt = ws ? (char*)ws + L.off_vt : nullptr;
+    a.kh = ws ? (char*)ws + L.off_kh : nullptr;
     a.kmax = ws ? (float*)((char*)ws + L.off_kmax) : nullptr;
+    a.qflag = ws ? (int32_t*)((char*)ws + L.off_qflag) : nullptr;
     a.Y = Y;
     return a;
 }

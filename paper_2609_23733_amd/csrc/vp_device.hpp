@@ -11,6 +11,8 @@ typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef __bf16 bf16x2 __attribute__((__vector_size__(2 * sizeof(__bf16))));
+typedef _Float16 f16;
+typedef _Float16 f16x8 __attribute__((__vector_size__(8 * sizeof(_Float16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
 typedef float f32x2 __attribute__((__vector_size__(2 * sizeof(float))));
@@ -37,6 +39,11 @@ __device__ __forceinline__ float bf16_to_f32(bf16 x) { return (float)x; }
 //   D[m][n]: n = l % 32, m = 8 * (r / 4) + 4 * (l / 32) + (r % 4), r = 0..15
 __device__ __forceinline__ f32x16 mfma_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 32x32x16 fp16 MFMA, fp32 accumulate; same operand layout as the bf16 one.
+__device__ __forceinline__ f32x16 mfma_f16(f16x8 a, f16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
 }
 
 // 32x32x2 fp32 MFMA: A[m][k]: m = l % 32, k = l / 32; B[k][n]: n = l % 32,

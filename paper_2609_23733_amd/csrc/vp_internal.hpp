@@ -27,8 +27,10 @@ struct AttnArgs {
     const int32_t* buckets;
     int64_t N;
     int H;
-    void* vt;      // packed V^T of FULL heads (bf16 only)
+    void* vt;      // packed V^T tiles of FULL heads (bf16 only)
+    void* kh;      // packed K tiles of FULL heads, fp16 (bf16 only)
     float* kmax;   // per (FULL slot, 64-key tile): max key norm (bf16 only)
+    int32_t* qflag;  // per FULL-head work item: needs the running reference point (bf16 only)
     void* Y;
     const float *ctx, *vmean;
     const void *g_w1, *g_w2, *d_w1, *d_w2;

@@ -273,3 +273,57 @@ def test_full_size_sampled(wl, n_full):
     for h in full:
         ref["Y"][:, h, :] = ref["Y_full_rows"][h]
     check_y(Yg, ref["Y"], "bf16", True, label="%s/%d" % (wl, n_full))
+
+
+# ------------------------------------ softmax reference point (FULL, bf16)
+
+C_LOG2 = 1.4426950408889634 / 8.0
+
+
+def tile_bounds(x, bq=256):
+    """Per 256-query tile and head: max_i |c q_i| * max_j |k_j| (log2 units),
+    the Cauchy-Schwarz bound on the tile's logits."""
+    q = torch.linalg.vector_norm(x.Q.float(), dim=2).cpu().numpy() * C_LOG2   # [N, H]
+    k = torch.linalg.vector_norm(x.K.float(), dim=2).cpu().numpy().max(axis=0)  # [H]
+    nt = -(-x.N // bq)
+    return np.stack([q[t * bq:(t + 1) * bq].max(axis=0) * k for t in range(nt)])
+
+
+FULL8 = np.array([2, 2, 1, 0, 2, 2, 1, 0, 2, 2, 1, 0, 2, 2, 1, 0], np.uint8)
+
+
+def test_reference_point_mixed_launch():
+    """Query tiles whose logits are provably small (reference point 0) and
+    tiles that need the running reference point, in one launch: queries
+    256..511 and one query of tile 4 are scaled by 8 (exact in bf16)."""
+    log("reference point: mixed tiles")
+    x = synth.make_layer(1, 1500, dtype="bf16", key=(9, 0), sharp=True, modes=FULL8,
+                         qkv_device="cuda")
+    x.Q[256:512] *= 8
+    x.Q[1100] *= 8
+    b = tile_bounds(x)
+    big = np.zeros(b.shape[0], bool)
+    big[[1, 4]] = True
+    assert (b[big] > 48).all() and (b[~big] < 24).all(), b
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="mixed")
+
+
+@pytest.mark.parametrize("P", [1500, 4097])
+def test_reference_point_moves(P):
+    """Key norms grow along the sequence (x1 to x8) and queries are scaled by
+    4, so logits exceed every earlier reference point several times: the
+    running reference point moves and O, l are rescaled; ragged last tile."""
+    log("reference point: growing logits P=%d" % P)
+    x = synth.make_layer(1, P, dtype="bf16", key=(10, P), sharp=True, modes=FULL8,
+                         qkv_device="cuda")
+    grow = torch.linspace(1.0, 8.0, x.N, device=x.K.device)[:, None, None]
+    x.K = (x.K.float() * grow).to(torch.bfloat16)
+    x.Q *= 4
+    assert (tile_bounds(x) > 64).all()
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="grow P=%d" % P)
