@@ -6,6 +6,8 @@
 // Work is taken from the FULL bucket that the mode assignment wrote on the
 // device: a grid sized for every head exits early past n_full * q_tiles, so
 // no mode is ever copied to the host.
+#include <type_traits>
+
 #include "vp_device.hpp"
 #include "vp_internal.hpp"
 
@@ -125,6 +127,13 @@ __device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
     return __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
 }
 
+// fp32 bits of x with the low 16 bits cleared: x truncated to bf16 (toward
+// zero), still as fp32.  Packing and summing these takes VALU instructions
+// that issue alongside MFMAs, unlike the bf16 convert and dot2 ones.
+__device__ __forceinline__ uint32_t trunc_bf16_bits(float x) {
+    return __builtin_bit_cast(uint32_t, x) & 0xffff0000u;
+}
+
 // Y[q, h, d] = O / l for the wave's two 32-query blocks; lane holds
 // d = 32 db + 8 g + 4 hh + i for i = 0..3.
 __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float (&l)[2],
@@ -156,180 +165,401 @@ __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float 
     }
 }
 
-// K6a: reference point 0, fp16 logits.  Writes wide_items[L] for every work
-// item it owns (1 = left to K6b), so the flags never carry over between calls.
-__global__ __launch_bounds__(256, 2) void k_flash_bf16(const bf16* __restrict__ Q,
+// K6a: reference point 0, fp16 logits.  One workgroup = 8 waves x 64 queries
+// of one FULL head, two waves per SIMD (waves w and w + 4).  Ping-pong:
+// waves 0-3 (group A) and 4-7 (group B) run the same sequence of phases,
+// matrix(0), vector(0), matrix(1), ..., group B one phase behind, with one
+// workgroup barrier per phase, so that in every phase one wave of each SIMD
+// issues MFMAs while the other issues the softmax's exp2 / pack / sums:
+//   matrix(t): O += V(t-1) P(t-1)  then  S(t) = K(t) (c Q)^T   (32 MFMAs)
+//   vector(t): P(t) = bf16(2^S(t)) (truncated), l += row sums of P(t)
+// LDS slot t % 2 holds K(t) and V(t-1).
+//
+// Balanced tail: the work is n_full x q-tiles items of nkt key tiles.  A
+// fixed grid of G workgroups (one per CU) takes the items in rounds,
+// workgroup w item r G + w, so that in every round the workgroups of an XCD
+// stream the same key tiles of one head through its L2.  The R < G items of
+// the last, partial round are cut into one flat sequence of R nkt item-tile
+// steps, split evenly over the workgroups (at least kMinPartTiles steps
+// each), so the tail takes R / G of a round instead of a whole one.  With
+// reference point 0, results over key ranges simply add: a workgroup that
+// covers only part of an item writes its unnormalized O and l to one of its
+// two partial slots (0 for the first item of its range, 1 for the last), and
+// K6c adds the parts of each split item in workgroup order.  The part
+// holding tile 0 writes wide_items[L] (1 = left to K6b), so flags never
+// carry over.
+constexpr int kBQf = 512;
+constexpr int kStreamWG = 256;      // grid: one workgroup per CU
+constexpr int kPartFloats = kBQf * kD + kBQf;   // one partial slot: O[512][64], l[512]
+
+constexpr int kMinPartTiles = 8;    // fewest key tiles per workgroup in the tail
+
+// Workgroups used for T tail steps (at most G, at least kMinPartTiles steps
+// each), the first step of workgroup w, and the workgroup holding step x.
+__device__ __forceinline__ int tail_groups(int64_t T, int G) {
+    const int64_t g = T / kMinPartTiles;
+    return g < 1 ? 1 : (g < G ? (int)g : G);
+}
+__device__ __forceinline__ int64_t tail_start(int w, int64_t T, int G) {
+    return (int64_t)w * T / G;
+}
+__device__ __forceinline__ int tail_owner(int64_t x, int64_t T, int G) {
+    return (int)(((x + 1) * G + T - 1) / T) - 1;
+}
+
+__global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ Q,
                                                        const f16* __restrict__ Kh,
                                                        const bf16* __restrict__ Vt,
                                                        const float* __restrict__ kmax,
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        int32_t* __restrict__ wide_items,
+                                                       float* __restrict__ part, int G,
                                                        void* __restrict__ Y, int ydt) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
-    if ((int)blockIdx.x >= active) return;
-    const int L = xcd_remap(blockIdx.x, active);
-    const int slot = L / nqt, qt = L - slot * nqt;
-    const int h = full_head(buckets, H, slot);
-    if (h < 0) return;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (active == 0) return;
+    const int w = xcd_remap(blockIdx.x, G);
+    const int full = active / G * G, R = active - full;
+    // The wave index is uniform within a wave: say so, so that the group
+    // choice and everything derived from it stay scalar.
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int n = lane & 31, hh = lane >> 5;
+    const bool groupB = wave >= 4;
 
     __shared__ __attribute__((aligned(16))) f16 sK[2][kBK * kLdsRow];
     __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kLdsRow];
-    __shared__ float sKmax[4];
-    __shared__ int sWide[4];
+    __shared__ float sKmax[8];
+    __shared__ int sWide[8];
 
-    // max_j |k_j| over the head, from the per-tile maxima.
-    const float* kmx = kmax + (int64_t)slot * nkt;
-    {
-        float km = 0.f;
-        for (int i = threadIdx.x; i < nkt; i += 256) km = fmaxf(km, kmx[i]);
-        km = wave_max(km);
-        if (lane == 0) sKmax[wave] = km;
-    }
+    // One segment: key tiles [t0, t1) of item L; written to partial slot
+    // pslot of this workgroup if the segment is not the whole item.
+    auto segment = [&](int L, int t0, int t1, int pslot) {
+        const int slot = L / nqt, qt = L - slot * nqt;
+        const int h = full_head(buckets, H, slot);
+        if (h < 0) return;
 
-    // (c Q)^T operands of this wave's two 32-query blocks, fp16, kept in
-    // registers, and |c q| per query.
-    f16x8 Qop[2][4];
-    int64_t qidx[2];
-    float qn[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const int64_t qi = (int64_t)qt * kBQ16 + wave * 64 + qb * 32 + n;
-        qidx[qb] = qi;
-        const bool ok = qi < N;
-        const bf16* qp = Q + ((ok ? qi : 0) * H + h) * kD + 8 * hh;
-        float n2 = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            const bf16x8 raw = load_bf16x8(qp + 16 * ks);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float x = ok ? bf16_to_f32(raw[j]) * c : 0.f;
-                Qop[qb][ks][j] = (f16)x;
-                n2 = fmaf(x, x, n2);
-            }
+        // max_j |k_j| over the head, from the per-tile maxima.
+        const float* kmx = kmax + (int64_t)slot * nkt;
+        {
+            float km = 0.f;
+            for (int i = threadIdx.x; i < nkt; i += 512) km = fmaxf(km, kmx[i]);
+            km = wave_max(km);
+            if (lane == 0) sKmax[wave] = km;
         }
-        n2 += __shfl_xor(n2, 32);
-        qn[qb] = sqrtf(n2);
-    }
-    __syncthreads();
-    {
-        const float km = fmaxf(fmaxf(sKmax[0], sKmax[1]), fmaxf(sKmax[2], sKmax[3]));
-        const float qm = fmaxf(qn[0], qn[1]);
-        // Written as "not within" so that a NaN norm also goes to K6b.
-        const bool out = !(qm * km <= kFastBound && qm <= kF16Safe && km <= kF16Safe);
-        const bool wave_out = __builtin_amdgcn_ballot_w64(out) != 0;
-        if (lane == 0) sWide[wave] = wave_out;
-    }
-    __syncthreads();
-    const int wide = sWide[0] | sWide[1] | sWide[2] | sWide[3];
-    if (threadIdx.x == 0) wide_items[L] = wide;
-    if (wide) return;
 
-    // Global -> LDS copy assignment: 64 rows x 4 segments of 16 elements of
-    // the packed K and V^T tiles (rows already in LDS order).
-    const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
-    const f16* Khh = Kh + (int64_t)slot * nkt * kBK * kD;
-    const bf16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
-    f16x8 pk0, pk1;
-    bf16x8 pv0, pv1;
-    auto gload = [&](int t) {
-        const f16* kp = Khh + ((int64_t)t * kBK + lr) * kD + lc;
-        pk0 = *reinterpret_cast<const f16x8*>(kp);
-        pk1 = *reinterpret_cast<const f16x8*>(kp + 8);
-        const bf16* vp = Vth + ((int64_t)t * kD + lr) * kBK + lc;
-        pv0 = load_bf16x8(vp);
-        pv1 = load_bf16x8(vp + 8);
-    };
-    auto lstore = [&](int buf) {
-        f16* kd = &sK[buf][lr * kLdsRow + lc];
-        *reinterpret_cast<f16x8*>(kd) = pk0;
-        *reinterpret_cast<f16x8*>(kd + 8) = pk1;
-        bf16* vd = &sV[buf][lr * kLdsRow + lc];
-        *reinterpret_cast<bf16x8*>(vd) = pv0;
-        *reinterpret_cast<bf16x8*>(vd + 8) = pv1;
-    };
-
-    f32x16 O[2][2];
-    float l[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        O[qb][0] = O[qb][1] = zero_f32x16();
-        l[qb] = 0.f;
-    }
-
-    gload(0);
-    lstore(0);
-    __syncthreads();
-
-    for (int t = 0; t < nkt; ++t) {
-        const int buf = t & 1;
-        if (t + 1 < nkt) gload(t + 1);
-
-        const bool last = (int64_t)(t + 1) * kBK > N;
-        bf16x8 P[2][2][2];
+        // (c Q)^T operands of this wave's two 32-query blocks, fp16, kept in
+        // registers, and |c q| per query.
+        f16x8 Qop[2][4];
+        int64_t qidx[2];
+        float qn[2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-            f32x16 S[2];
-            S[0] = S[1] = zero_f32x16();
+            const int64_t qi = (int64_t)qt * kBQf + wave * 64 + qb * 32 + n;
+            qidx[qb] = qi;
+            const bool ok = qi < N;
+            const bf16* qp = Q + ((ok ? qi : 0) * H + h) * kD + 8 * hh;
+            float n2 = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                const bf16x8 raw = load_bf16x8(qp + 16 * ks);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float x = ok ? bf16_to_f32(raw[j]) * c : 0.f;
+                    Qop[qb][ks][j] = (f16)x;
+                    n2 = fmaf(x, x, n2);
+                }
+            }
+            n2 += __shfl_xor(n2, 32);
+            qn[qb] = sqrtf(n2);
+        }
+        __syncthreads();
+        {
+            float km = sKmax[0];
+#pragma unroll
+            for (int v = 1; v < 8; ++v) km = fmaxf(km, sKmax[v]);
+            const float qm = fmaxf(qn[0], qn[1]);
+            // Written as "not within" so that a NaN norm also goes to K6b.
+            const bool out = !(qm * km <= kFastBound && qm <= kF16Safe && km <= kF16Safe);
+            const bool wave_out = __builtin_amdgcn_ballot_w64(out) != 0;
+            if (lane == 0) sWide[wave] = wave_out;
+        }
+        __syncthreads();
+        int wide = 0;
+#pragma unroll
+        for (int v = 0; v < 8; ++v) wide |= sWide[v];
+        if (t0 == 0 && threadIdx.x == 0) wide_items[L] = wide;
+        if (wide) return;
+
+        // Tile copies: group A (threads 0-255) copies K tiles, group B V^T
+        // tiles, each a contiguous 8 KB block: 64 rows x 4 segments of 16
+        // elements.  r counts tiles from t0.
+        const int ns = t1 - t0;
+        const int tl = threadIdx.x & 255, lr = tl >> 2, lc = (tl & 3) * 16;
+        const f16* Khh = Kh + ((int64_t)slot * nkt + t0) * kBK * kD;
+        const bf16* Vth = Vt + ((int64_t)slot * nkt + t0) * kD * kBK;
+        u32x4 g0, g1;
+        auto fetch = [&](int r) {   // tile r (clamped to the last one) into registers
+            r = r < ns ? r : ns - 1;
+            const u32x4* src = groupB
+                ? reinterpret_cast<const u32x4*>(Vth + ((int64_t)r * kD + lr) * kBK + lc)
+                : reinterpret_cast<const u32x4*>(Khh + ((int64_t)r * kBK + lr) * kD + lc);
+            g0 = src[0];
+            g1 = src[1];
+        };
+        auto stash = [&](int sl) {   // ... into LDS slot sl
+            u32x4* dst = groupB ? reinterpret_cast<u32x4*>(&sV[sl][lr * kLdsRow + lc])
+                                : reinterpret_cast<u32x4*>(&sK[sl][lr * kLdsRow + lc]);
+            dst[0] = g0;
+            dst[1] = g1;
+        };
+
+        f32x16 O[2][2], S[2][2];
+        bf16x8 P[2][2][2];
+        float l[2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+            O[qb][0] = O[qb][1] = zero_f32x16();
+            l[qb] = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) P[qb][kb][0] = P[qb][kb][1] = zero_bf16x8();
+        }
+
+        // Matrix phase of tile r: O += V(r-1) P(r-1) from sV[r%2], then S(r)
+        // from sK[r%2].  (PV first: P(r-1) is dead before S(r) is written, so
+        // the two can share registers.  r = 0: P and V slot 0 are zero, so the
+        // PV adds exactly nothing.)
+        auto pv = [&](int sl) {
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                            &sV[sl][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
+                        O[0][db] = mfma_bf16(a, P[0][kb][b], O[0][db]);
+                        O[1][db] = mfma_bf16(a, P[1][kb][b], O[1][db]);
+                    }
+        };
+        auto mma_phase = [&](int r) {
+            const int sl = r & 1;
+            __builtin_amdgcn_s_setprio(1);
+            pv(sl);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
+                    if (ks == 0) S[0][kb] = S[1][kb] = zero_f32x16();
                     const f16x8 a = *reinterpret_cast<const f16x8*>(
-                        &sK[buf][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
-                    S[kb] = mfma_f16(a, Qop[qb][ks], S[kb]);
+                        &sK[sl][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
+                    S[0][kb] = mfma_f16(a, Qop[0][ks], S[0][kb]);
+                    S[1][kb] = mfma_f16(a, Qop[1][ks], S[1][kb]);
                 }
-            if (last) {   // ragged last tile: keys >= N get weight 0
+            __builtin_amdgcn_s_setprio(0);
+        };
+        // Vector phase of tile r: S(r) -> P(r), l += row sums.  The segment's
+        // last tile masks keys >= N to weight 0 (a separate instance, so that
+        // no other tile pays for the test).
+        auto valu_phase = [&](int r, auto last_tag) {
+            if (decltype(last_tag)::value) {
+                const int64_t k0 = (int64_t)(t0 + r) * kBK;
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int64_t key =
-                            (int64_t)t * kBK + kb * 32 + 16 * (r >> 3) + 8 * hh + (r & 7);
-                        if (key >= N) S[kb][r] = -INFINITY;
+                    for (int i = 0; i < 16; ++i) {
+                        const int64_t key = k0 + kb * 32 + 16 * (i >> 3) + 8 * hh + (i & 7);
+                        if (key >= N) S[0][kb][i] = S[1][kb][i] = -INFINITY;
                     }
             }
-            // p = 2^x, packed to bf16; row sums from the packed values.
-            float ls = l[qb];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int qb = 0; qb < 2; ++qb) {
+                float ls0 = 0.f, ls1 = 0.f;
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    u32x4 pk;
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        f32x2 e;
-                        e[0] = exp2f_fast(S[kb][8 * b + 2 * j]);
-                        e[1] = exp2f_fast(S[kb][8 * b + 2 * j + 1]);
-                        pk[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, bf16x2));
-                        ls = dot2_ones(pk[j], ls);
+                    for (int b = 0; b < 2; ++b) {
+                        u32x4 pk;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const uint32_t e0 =
+                                trunc_bf16_bits(exp2f_fast(S[qb][kb][8 * b + 2 * j]));
+                            const uint32_t e1 =
+                                trunc_bf16_bits(exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]));
+                            pk[j] = __builtin_amdgcn_perm(e1, e0, 0x07060302u);
+                            ls0 += __builtin_bit_cast(float, e0);
+                            ls1 += __builtin_bit_cast(float, e1);
+                        }
+                        P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
                     }
-                    P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
-                }
-            l[qb] = ls;
+                l[qb] += ls0 + ls1;
+            }
+        };
+        const std::false_type body{};
+        const std::true_type tail{};
+        // End of a phase: a workgroup barrier that the compiler may not
+        // schedule any instruction across (it would otherwise hoist the next
+        // phase's register-only work above it and undo the alternation).
+        auto phase_end = [] {
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+        };
+
+        // Prologue: K(t0) into slot 0; V of slot 0 (tile t0 - 1) is zero.
+        if (groupB) {
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            g0 = g1 = z;
+        } else {
+            fetch(0);
         }
+        stash(0);
+        phase_end();
 
-        // O^T += V^T P^T
-#pragma unroll
-        for (int db = 0; db < 2; ++db)
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                        &sV[buf][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
-#pragma unroll
-                    for (int qb = 0; qb < 2; ++qb) O[qb][db] = mfma_bf16(a, P[qb][kb][b], O[qb][db]);
-                }
+        // Phases, one workgroup barrier each (2 ns + 1 in both groups):
+        //   group A:  M(0) V(0) M(1) V(1) ... M(ns-1) V(ns-1) -
+        //   group B:  -    M(0) V(0) M(1) ... V(ns-2) M(ns-1) V(ns-1)
+        // Group A loads K(r+1) during M(r) and stores it to slot (r+1) % 2
+        // after V(r); group B loads V(r) during V(r-1) and stores it to slot
+        // (r+1) % 2 after M(r).  A slot is rewritten only after both groups'
+        // last reads.
+        if (!groupB) {
+            for (int r = 0; r < ns - 1; ++r) {
+                fetch(r + 1);
+                mma_phase(r);
+                phase_end();
+                valu_phase(r, body);
+                stash((r + 1) & 1);
+                phase_end();
+            }
+            mma_phase(ns - 1);
+            phase_end();
+            valu_phase(ns - 1, tail);
+            phase_end();
+            phase_end();
+        } else {
+            fetch(0);
+            phase_end();
+            for (int r = 0; r < ns - 1; ++r) {
+                mma_phase(r);
+                stash((r + 1) & 1);
+                phase_end();
+                fetch(r + 1);
+                valu_phase(r, body);
+                phase_end();
+            }
+            mma_phase(ns - 1);
+            stash(ns & 1);
+            phase_end();
+            valu_phase(ns - 1, tail);
+            phase_end();
+        }
+        pv(ns & 1);   // O += V(ns-1) P(ns-1)
 
-        if (t + 1 < nkt) lstore(buf ^ 1);
-        __syncthreads();
+        if (t0 == 0 && t1 == nkt) {
+            store_rows(O, l, qidx, N, H, h, hh, Y, ydt);
+        } else {
+            // Partial slot: O[q][d] unnormalized, then l[q], q = row in item.
+            float* ps = part + (int64_t)(w * 2 + pslot) * kPartFloats;
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) {
+                const int qr = wave * 64 + qb * 32 + n;
+#pragma unroll
+                for (int db = 0; db < 2; ++db)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        *reinterpret_cast<float4*>(ps + qr * kD + db * 32 + 8 * g + 4 * hh) =
+                            make_float4(O[qb][db][4 * g], O[qb][db][4 * g + 1],
+                                        O[qb][db][4 * g + 2], O[qb][db][4 * g + 3]);
+                const float lt = l[qb] + __shfl_xor(l[qb], 32);
+                if (hh == 0) ps[kBQf * kD + qr] = lt;
+            }
+        }
+    };
+
+    for (int L = w; L < full; L += G) {
+        segment(L, 0, nkt, 0);
+        __syncthreads();   // LDS is reused by the next segment
     }
-    store_rows(O, l, qidx, N, H, h, hh, Y, ydt);
+    if (R > 0) {
+        const int64_t T = (int64_t)R * nkt;
+        const int Gt = tail_groups(T, G);
+        if (w < Gt) {
+            const int64_t start = tail_start(w, T, Gt), end = tail_start(w + 1, T, Gt);
+            for (int64_t x = start; x < end;) {
+                const int i = (int)(x / nkt);
+                const int t0 = (int)(x - (int64_t)i * nkt);
+                const int64_t left = end - x;
+                const int t1 = (int64_t)(nkt - t0) < left ? nkt : (int)(t0 + left);
+                segment(full + i, t0, t1, x == start ? 0 : 1);
+                x += t1 - t0;
+                __syncthreads();
+            }
+        }
+    }
+}
+
+// K6c: Y of the tail items that K6a split over workgroups: the parts' O and
+// l added in workgroup order (fixed, so results are deterministic), then
+// O / l.  One workgroup of 256 threads per tail item; items that K6a
+// finished whole or left to K6b exit at once.
+__global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict__ buckets,
+                                                       int64_t N, int H, int nqt, int nkt,
+                                                       const int32_t* __restrict__ wide_items,
+                                                       const float* __restrict__ part, int G,
+                                                       void* __restrict__ Y, int ydt) {
+    const int nfull = full_count(buckets, H);
+    const int active = nfull * nqt;
+    const int full = active / G * G, R = active - full;
+    const int i = blockIdx.x;
+    if (i >= R) return;
+    const int64_t T = (int64_t)R * nkt;
+    const int Gt = tail_groups(T, G);
+    const int wf = tail_owner((int64_t)i * nkt, T, Gt);
+    const int wl = tail_owner((int64_t)(i + 1) * nkt - 1, T, Gt);
+    const int L = full + i;
+    if (wf == wl || wide_items[L]) return;
+    const int slot = L / nqt, qt = L - slot * nqt;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    // partial slot of workgroup v for this item
+    auto pslot = [&](int v) {
+        const int k = i == (int)(tail_start(v, T, Gt) / nkt) ? 0 : 1;
+        return part + (int64_t)(v * 2 + k) * kPartFloats;
+    };
+#pragma unroll 1
+    for (int j = 0; j < kBQf / 256; ++j) {
+        const int qr = threadIdx.x + 256 * j;
+        const int64_t qi = (int64_t)qt * kBQf + qr;
+        if (qi >= N) continue;
+        float lt = 0.f;
+        for (int v = wf; v <= wl; ++v) lt += pslot(v)[kBQf * kD + qr];
+        const float inv = 1.f / lt;
+#pragma unroll 1
+        for (int d0 = 0; d0 < kD; d0 += 8) {
+            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int v = wf; v <= wl; ++v) {
+                const float* src = pslot(v) + qr * kD + d0;
+                const float4 a = *reinterpret_cast<const float4*>(src);
+                const float4 b = *reinterpret_cast<const float4*>(src + 4);
+                acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
+                acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
+            }
+            const int64_t off = (qi * H + h) * kD + d0;
+            if (ydt == DT_BF16) {
+                bf16x8 o;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) o[k] = (bf16)(acc[k] * inv);
+                *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + off) = o;
+            } else {
+                float* yo = reinterpret_cast<float*>(Y) + off;
+                *reinterpret_cast<float4*>(yo) =
+                    make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+                *reinterpret_cast<float4*>(yo + 4) =
+                    make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+            }
+        }
+    }
 }
 
 // ------------------------------------------------------------------------
@@ -358,14 +588,14 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        const int32_t* __restrict__ wide_items,
-                                                       void* __restrict__ Y, int ydt) {
+                                                       int nqt_fast, void* __restrict__ Y, int ydt) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
     if ((int)blockIdx.x >= active) return;
     const int L = xcd_remap(blockIdx.x, active);
     const int slot = L / nqt, qt = L - slot * nqt;
     const int h = full_head(buckets, H, slot);
-    if (h < 0 || wide_items[L] == 0) return;
+    if (h < 0 || wide_items[slot * nqt_fast + qt / (kBQf / kBQ16)] == 0) return;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int n = lane & 31, hh = lane >> 5;
 
@@ -673,6 +903,16 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
 
 int flash_q_tile(int dtype) { return dtype == DT_BF16 ? kBQ16 : kBQ32; }
 
+int flash_stream_groups(int64_t N, int H) {
+    (void)N;
+    (void)H;
+    return kStreamWG;
+}
+
+size_t flash_part_bytes(int64_t N, int H) {
+    return (size_t)2 * flash_stream_groups(N, H) * kPartFloats * sizeof(float);
+}
+
 void launch_gather(const AttnArgs& a, hipStream_t st) {
     const int nkt = (int)((a.N + kBK - 1) / kBK);
     hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.K,
@@ -686,13 +926,17 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
     const int bq = flash_q_tile(a.dtype);
     const int nqt = (int)((a.N + bq - 1) / bq);
     if (a.dtype == DT_BF16) {
-        hipLaunchKernelGGL(k_flash_bf16, dim3(nqt * a.H), dim3(256), 0, st, (const bf16*)a.Q,
+        const int nqf = (int)((a.N + kBQf - 1) / kBQf);
+        const int G = flash_stream_groups(a.N, a.H);
+        hipLaunchKernelGGL(k_flash_bf16, dim3(G), dim3(512), 0, st, (const bf16*)a.Q,
                            (const f16*)a.kh, (const bf16*)a.vt, (const float*)a.kmax, a.buckets,
-                           a.N, a.H, nqt, nkt, c, a.qflag, a.Y, a.ydt);
+                           a.N, a.H, nqf, nkt, c, a.qflag, a.part, G, a.Y, a.ydt);
+        hipLaunchKernelGGL(k_flash_combine, dim3(G), dim3(256), 0, st, a.buckets, a.N, a.H, nqf,
+                           nkt, (const int32_t*)a.qflag, (const float*)a.part, G, a.Y, a.ydt);
         hipLaunchKernelGGL(k_flash_bf16_wide, dim3(nqt * a.H), dim3(256), 0, st,
                            (const bf16*)a.Q, (const bf16*)a.K, (const bf16*)a.vt,
-                           (const float*)a.kmax, a.buckets, a.N, a.H, nqt, nkt, c, a.qflag, a.Y,
-                           a.ydt);
+                           (const float*)a.kmax, a.buckets, a.N, a.H, nqt, nkt, c, a.qflag, nqf,
+                           a.Y, a.ydt);
     } else
         hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,

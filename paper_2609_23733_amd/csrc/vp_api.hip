@@ -24,7 +24,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 struct Layout {
     int64_t N;
     int64_t n1, chunk1, n2, chunk2, nkt;
-    size_t off_part1, off_part2, off_vt, off_kh, off_kmax, off_qflag, total;
+    size_t off_part1, off_part2, off_vt, off_kh, off_kmax, off_qflag, off_fpart, total;
 };
 
 // Chunking of the router reductions and the workspace carve-up; a pure
@@ -59,6 +59,8 @@ bool make_layout(const vp_shape* s, Layout* L) {
     L->off_qflag = off;
     if (s->dtype == VP_BF16)
         off = align_up(off + (size_t)s->H * cdiv(N, vp::flash_q_tile(VP_BF16)) * sizeof(int32_t));
+    L->off_fpart = off;
+    if (s->dtype == VP_BF16) off = align_up(off + vp::flash_part_bytes(N, (int)s->H));
     L->total = off;
     return true;
 }
@@ -228,6 +230,7 @@ vp::AttnArgs attn_args(const vp_shape* shape, const Layout& L, const void* Q, co
     a.kh = ws ? (char*)ws + L.off_kh : nullptr;
     a.kmax = ws ? (float*)((char*)ws + L.off_kmax) : nullptr;
     a.qflag = ws ? (int32_t*)((char*)ws + L.off_qflag) : nullptr;
+    a.part = ws ? (float*)((char*)ws + L.off_fpart) : nullptr;
     a.Y = Y;
     return a;
 }

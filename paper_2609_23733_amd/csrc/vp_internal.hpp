@@ -31,6 +31,7 @@ struct AttnArgs {
     void* kh;      // packed K tiles of FULL heads, fp16 (bf16 only)
     float* kmax;   // per (FULL slot, 64-key tile): max key norm (bf16 only)
     int32_t* qflag;  // per FULL-head work item: needs the running reference point (bf16 only)
+    float* part;     // stream-K partial results of the FULL-head kernel (bf16 only)
     void* Y;
     const float *ctx, *vmean;
     const void *g_w1, *g_w2, *d_w1, *d_w2;
@@ -47,5 +48,7 @@ void launch_gather(const AttnArgs& a, hipStream_t st);
 void launch_flash(const AttnArgs& a, hipStream_t st);
 void launch_linear_heads(const AttnArgs& a, hipStream_t st);
 int flash_q_tile(int dtype);
+int flash_stream_groups(int64_t N, int H);
+size_t flash_part_bytes(int64_t N, int H);
 
 }  // namespace vp
