@@ -33,9 +33,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "e8848f67b40c8667626bc4b6166341cd77d438cbf8cdf94fa7f7183a15748a78",
+    "source_sha256": "6c843fb74e65eed1275e59d9cdbf33669e0a3543b04d12b19ef58b889725867e",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1309327, "write_kib": 68700,
+    "fetch_kib": 1526262, "write_kib": 104943,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 
