@@ -110,9 +110,10 @@ typedef struct {
 
 /* Bytes of device workspace that vp_router_score and
  * vp_routed_global_attention need for `shape` (0 if the shape is invalid).
- * The workspace holds router partial sums and the gathered values of FULL
- * heads; it must be 256-byte aligned and may be reused across calls on one
- * stream (calls on different streams need separate workspaces). */
+ * The workspace holds router partial sums, the gathered keys and values of
+ * FULL heads and the FULL kernel's partial results; it must be 256-byte
+ * aligned and may be reused across calls on one stream (calls on different
+ * streams need separate workspaces). */
 size_t vp_workspace_bytes(const vp_shape *shape);
 
 /* Router (Section 4.1, Eq.1-3; context Eq.5; value mean, Algorithm 1).
@@ -162,12 +163,15 @@ vp_status vp_routed_global_attention(const vp_shape *shape, const void *Q, const
  * for callers that schedule or time them separately (same arguments and
  * requirements as vp_routed_global_attention; run all three, in this order,
  * on one stream, to obtain the same Y).
- *   vp_gather_full_heads:   packs V of each FULL head (bf16 layers; no-op for
- *                           fp32) into the workspace, tile-transposed, and
- *                           records the largest key norm of every 64-key tile;
+ *   vp_gather_full_heads:   packs V (tile-transposed) and K (fp16 tiles) of
+ *                           each FULL head into the workspace (bf16 layers;
+ *                           no-op for fp32) and records the largest key norm
+ *                           of every 64-key tile;
  *   vp_full_head_attention: exact softmax attention of every FULL head
  *                           (Algorithm 1, first branch); reads the packed
- *                           values the gather left in `ws`;
+ *                           tiles the gather left in `ws`.  Results are
+ *                           deterministic for a given device (the split of
+ *                           work over its compute units is fixed);
  *   vp_linear_heads:        SURR (Eq.5-7) and MEAN heads. */
 vp_status vp_gather_full_heads(const vp_shape *shape, const void *K, const void *V,
                                const int32_t *buckets, void *ws, size_t ws_bytes, void *stream);
