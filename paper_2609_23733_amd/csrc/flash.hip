@@ -172,7 +172,10 @@ __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float 
 // workgroup barrier per phase, so that in every phase one wave of each SIMD
 // issues MFMAs while the other issues the softmax's exp2 / pack / sums:
 //   matrix(t): O += V(t-1) P(t-1)  then  S(t) = K(t) (c Q)^T   (32 MFMAs)
-//   vector(t): P(t) = bf16(2^S(t)) (truncated), l += row sums of P(t)
+//   vector(t): P(t) = bf16(2^S(t)) (round to nearest, one pack per pair),
+//              l += row sums of the fp32 2^S(t) (the packing error has zero
+//              mean, so l needs no rounded copy: five vector instructions per
+//              pair of scores, the fewest found)
 // LDS slot t % 2 holds K(t) and V(t-1).
 //
 // Balanced tail: the work is n_full x q-tiles items of nkt key tiles.  A
@@ -382,13 +385,13 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         u32x4 pk;
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
-                            const uint32_t e0 =
-                                trunc_bf16_bits(exp2f_fast(S[qb][kb][8 * b + 2 * j]));
-                            const uint32_t e1 =
-                                trunc_bf16_bits(exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]));
-                            pk[j] = __builtin_amdgcn_perm(e1, e0, 0x07060302u);
-                            ls0 += __builtin_bit_cast(float, e0);
-                            ls1 += __builtin_bit_cast(float, e1);
+                            f32x2 e;
+                            e[0] = exp2f_fast(S[qb][kb][8 * b + 2 * j]);
+                            e[1] = exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]);
+                            pk[j] = __builtin_bit_cast(uint32_t,
+                                                       __builtin_convertvector(e, bf16x2));
+                            ls0 += e[0];
+                            ls1 += e[1];
                         }
                         P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
                     }
