@@ -127,13 +127,6 @@ __device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
     return __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
 }
 
-// fp32 bits of x with the low 16 bits cleared: x truncated to bf16 (toward
-// zero), still as fp32.  Packing and summing these takes VALU instructions
-// that issue alongside MFMAs, unlike the bf16 convert and dot2 ones.
-__device__ __forceinline__ uint32_t trunc_bf16_bits(float x) {
-    return __builtin_bit_cast(uint32_t, x) & 0xffff0000u;
-}
-
 // Y[q, h, d] = O / l for the wave's two 32-query blocks; lane holds
 // d = 32 db + 8 g + 4 hh + i for i = 0..3.
 __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float (&l)[2],
@@ -347,18 +340,44 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         };
         auto mma_phase = [&](int r) {
             const int sl = r & 1;
+            // All 16 LDS operands of the phase are requested first, so LDS
+            // latency is paid once per phase rather than once per two reads.
+            bf16x8 va[2][2][2];
+            f16x8 ka[2][4];
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b)
+                        va[db][kb][b] = *reinterpret_cast<const bf16x8*>(
+                            &sV[sl][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    ka[kb][ks] = *reinterpret_cast<const f16x8*>(
+                        &sK[sl][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
             __builtin_amdgcn_s_setprio(1);
-            pv(sl);
+#pragma unroll
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) {
+                        O[0][db] = mfma_bf16(va[db][kb][b], P[0][kb][b], O[0][db]);
+                        O[1][db] = mfma_bf16(va[db][kb][b], P[1][kb][b], O[1][db]);
+                    }
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
                     if (ks == 0) S[0][kb] = S[1][kb] = zero_f32x16();
-                    const f16x8 a = *reinterpret_cast<const f16x8*>(
-                        &sK[sl][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
-                    S[0][kb] = mfma_f16(a, Qop[0][ks], S[0][kb]);
-                    S[1][kb] = mfma_f16(a, Qop[1][ks], S[1][kb]);
+                    S[0][kb] = mfma_f16(ka[kb][ks], Qop[0][ks], S[0][kb]);
+                    S[1][kb] = mfma_f16(ka[kb][ks], Qop[1][ks], S[1][kb]);
                 }
+            __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
             __builtin_amdgcn_s_setprio(0);
         };
         // Vector phase of tile r: S(r) -> P(r), l += row sums.  The segment's
