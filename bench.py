@@ -176,7 +176,7 @@ def main():
     by = [head]
     if not args.no_sweep:
         del layer
-        for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16)):
+        for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16), (500, 4)):
             r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 0))
             by.append(r)
             del lyr

@@ -255,7 +255,7 @@ def test_permutation_equivariance_gpu():
 # ------------------------------------------------- full-size workloads
 
 @pytest.mark.parametrize("wl,n_full", [("s32_bf16", 4), ("s32_bf16", 16), ("s100_bf16", 4),
-                                       ("s100_bf16", 16)])
+                                       ("s100_bf16", 16), ("s500_bf16", 1), ("s500_bf16", 6)])
 def test_full_size_sampled(wl, n_full):
     """The benchmark workloads at full size, in the benchmark's launch
     configuration (bf16 operands, bf16 Y): router and modes on all tokens,
