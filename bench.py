@@ -33,9 +33,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "6c843fb74e65eed1275e59d9cdbf33669e0a3543b04d12b19ef58b889725867e",
+    "source_sha256": "5a47d80a6923be580b02fcc7d8c7642e07c860b22492b9fd8d1a597d52616d5a",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1526262, "write_kib": 104943,
+    "fetch_kib": 1531126, "write_kib": 104942,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 
