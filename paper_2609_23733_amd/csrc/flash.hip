@@ -358,7 +358,6 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int ks = 0; ks < 4; ++ks)
                     ka[kb][ks] = *reinterpret_cast<const f16x8*>(
                         &sK[sl][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
-            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
             for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -378,7 +377,6 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 }
             __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
             __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
-            __builtin_amdgcn_s_setprio(0);
         };
         // Vector phase of tile r: S(r) -> P(r), l += row sums.  The segment's
         // last tile masks keys >= N to weight 0 (a separate instance, so that
