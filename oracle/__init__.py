@@ -32,7 +32,9 @@ _lock = threading.Lock()
 _lib = None
 
 MODE_MEAN, MODE_SURR, MODE_FULL = 0, 1, 2
-RULE_THRESHOLD, RULE_ARGMAX = 0, 1
+RULE_THRESHOLD, RULE_ARGMAX, RULE_THRESHOLD_BINARY, RULE_ARGMAX_BINARY = 0, 1, 2, 3
+POOL_GATED, POOL_MEAN = 0, 1
+SURR_EQ7, SURR_MEAN_CONTEXT, SURR_NO_RESIDUAL, SURR_ADD_IDENTITY, SURR_LINEAR_ATTN = 0, 1, 2, 3, 4
 ACT_GELU, ACT_RELU = 0, 1
 TAU_LOW, TAU_HIGH = 0.01, 0.20   # Section 4.2 and implementation details
 
@@ -64,8 +66,9 @@ def _load():
             lib.or_router_logits.argtypes = [P, P, P, i32, i32, P]
             lib.or_assign.argtypes = [P, i32, i32, flt, flt, P]
             lib.or_full_rows.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, dbl, P, i32]
-            lib.or_surr_rows.argtypes = [P, i64, i32, i32, i32, i32, i32, P, P, P, P, P, P, P,
-                                         P, P, P, i64, P, i32]
+            lib.or_surr_rows.argtypes = [P, i64, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P,
+                                         P, P, P, P, i64, P, i32]
+            lib.or_linattn_rows.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, P, i32]
             lib.or_threads_used.argtypes = [i32]
             lib.or_threads_used.restype = i32
             _lib = lib
@@ -114,6 +117,11 @@ def router_pool(Q, W, U, w, nthreads=0, want_weights=False):
     return (qp, a, al) if want_weights else qp
 
 
+def router_pool_mean(Q):
+    """Mean-query ablation (component study): q_pool = (1/N) sum_i q_i."""
+    return as_f32(Q).astype(np.float64).mean(axis=0)
+
+
 def router_route(K, V, q_pool, scale=None, nthreads=0, want_r=False):
     """Eq.3 and Eq.5: single-query attention r_h, saliency s_h = max r_h,
     context C_h = r_h V_h and value mean.  Returns (s [H], C [H,d], mean [H,d] [, r])."""
@@ -141,7 +149,8 @@ def router_logits(u, Wr, br):
 
 
 def assign(scores, rule, tau_low=TAU_LOW, tau_high=TAU_HIGH):
-    """Eq.4 (threshold on s_h) or first-argmax of per-head logits."""
+    """Eq.4 (threshold on s_h), first-argmax of per-head logits, or their
+    two-branch (MEAN / FULL only) forms of the compute-mode ablation."""
     sc = np.ascontiguousarray(scores, dtype=np.float64)
     H = sc.shape[0]
     modes = np.zeros(H, np.uint8)
@@ -175,9 +184,11 @@ def full_rows(Q, K, V, h, rows=None, scale=None, nthreads=0):
     return Y
 
 
-def surr_rows(V, C_h, surr, h, rows=None, act=ACT_GELU, nthreads=0):
+def surr_rows(V, C_h, surr, h, rows=None, act=ACT_GELU, nthreads=0, variant=SURR_EQ7):
     """Eq.5-7 SURR branch for head h: [R, d].  ``surr`` holds the per-head
-    stacked weights g_w1 [H,L,2d], g_b1 [H,L], g_w2 [H,d,L], g_b2 [H,d], d_*."""
+    stacked weights g_w1 [H,L,2d], g_b1 [H,L], g_w2 [H,d,L], g_b2 [H,d], d_*.
+    ``variant``: SURR_EQ7, SURR_NO_RESIDUAL (y = C_h) or SURR_ADD_IDENTITY
+    (y = v + Eq.7); the mean-context ablation is SURR_EQ7 with C_h = mean."""
     V = as_f32(V)
     N, H, d = V.shape
     wt = {k: np.ascontiguousarray(as_f32(v)[h]) for k, v in surr.items()}
@@ -189,16 +200,34 @@ def surr_rows(V, C_h, surr, h, rows=None, act=ACT_GELU, nthreads=0):
         rows = np.ascontiguousarray(rows, dtype=np.int64)
         nr, rp = rows.shape[0], rows
     Y = np.zeros((nr, d), np.float64)
-    _load().or_surr_rows(_p(V), N, H, d, int(h), L, int(act), _p(C_h), _p(wt["g_w1"]),
+    _load().or_surr_rows(_p(V), N, H, d, int(h), L, int(act), int(variant), _p(C_h),
+                         _p(wt["g_w1"]),
                          _p(wt["g_b1"]), _p(wt["g_w2"]), _p(wt["g_b2"]), _p(wt["d_w1"]),
                          _p(wt["d_b1"]), _p(wt["d_w2"]), _p(wt["d_b2"]), _p(rp), nr, _p(Y),
                          _nt(nthreads))
     return Y
 
 
+def linattn_rows(Q, K, V, h, rows=None, nthreads=0):
+    """Linear attention of head h (the compute-mode ablation's alternative to
+    the surrogate; phi = elu + 1) on the given query rows: [R, d]."""
+    Q, K, V = as_f32(Q), as_f32(K), as_f32(V)
+    N, H, d = Q.shape
+    if rows is None:
+        nr, rp = N, None
+    else:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        nr, rp = rows.shape[0], rows
+    Y = np.zeros((nr, d), np.float64)
+    _load().or_linattn_rows(_p(Q), _p(K), _p(V), N, H, d, int(h), _p(rp), nr, _p(Y),
+                            _nt(nthreads))
+    return Y
+
+
 def routed_layer(Q, K, V, W, U, w, surr, u=None, Wr=None, br=None, rule=RULE_ARGMAX,
                  tau_low=TAU_LOW, tau_high=TAU_HIGH, modes=None, rows=None, full_rows_sel=None,
-                 act=ACT_GELU, scale_router=None, scale_attn=None, nthreads=0):
+                 act=ACT_GELU, scale_router=None, scale_attn=None, nthreads=0,
+                 pool=POOL_GATED, surr_variant=SURR_EQ7):
     """The routed global-attention layer (Algorithm 1 step 2, Eq.1-7), in order:
     router pooling, single-query routing, mode assignment, per-head outputs,
     concatenation over heads.
@@ -208,20 +237,22 @@ def routed_layer(Q, K, V, W, U, w, surr, u=None, Wr=None, br=None, rule=RULE_ARG
     row sample used at sizes where exact attention over every row is too slow);
     the returned ``Y_full_rows`` then holds them.
     ``modes``: explicit modes (bypasses the rule, e.g. to force every head FULL).
+    ``pool``: POOL_GATED (Eq.1-2) or POOL_MEAN (mean-query ablation).
+    ``surr_variant``: how SURR heads are computed (Eq.5-7 or an ablation).
     """
     Q32 = as_f32(Q)
     N, H, d = Q32.shape
-    q_pool = router_pool(Q32, W, U, w, nthreads)
+    q_pool = router_pool(Q32, W, U, w, nthreads) if pool == POOL_GATED else router_pool_mean(Q32)
     s, C, mean = router_route(K, V, q_pool, scale_router, nthreads)
     logits = None
     if modes is None:
-        if rule == RULE_THRESHOLD:
-            modes = assign(s, RULE_THRESHOLD, tau_low, tau_high)
+        if rule in (RULE_THRESHOLD, RULE_THRESHOLD_BINARY):
+            modes = assign(s, rule, tau_low, tau_high)
         else:
             if u is None:   # default router input: the pooled queries of all heads
                 u = q_pool.reshape(-1).astype(np.float32)
             logits = router_logits(u, Wr, br)
-            modes = assign(logits, RULE_ARGMAX)
+            modes = assign(logits, rule)
     modes = np.asarray(modes, np.uint8)
     nrow = N if rows is None else len(rows)
     Y = np.zeros((nrow, H, d), np.float64)
@@ -235,7 +266,12 @@ def routed_layer(Q, K, V, W, U, w, surr, u=None, Wr=None, br=None, rule=RULE_ARG
             else:
                 Y[:, h, :] = full_rows(Q32, K, V, h, rows, scale_attn, nthreads)
         elif m == MODE_SURR:
-            Y[:, h, :] = surr_rows(V, C[h], surr, h, rows, act, nthreads)
+            if surr_variant == SURR_LINEAR_ATTN:
+                Y[:, h, :] = linattn_rows(Q32, K, V, h, rows, nthreads)
+            elif surr_variant == SURR_MEAN_CONTEXT:
+                Y[:, h, :] = surr_rows(V, mean[h], surr, h, rows, act, nthreads, SURR_EQ7)
+            else:
+                Y[:, h, :] = surr_rows(V, C[h], surr, h, rows, act, nthreads, surr_variant)
         else:
             Y[:, h, :] = mean[h][None, :]     # Algorithm 1: broadcast of the value mean
     return dict(q_pool=q_pool, s=s, C=C, mean=mean, logits=logits, modes=modes, Y=Y,

@@ -217,20 +217,24 @@ void or_router_logits(const float *u, const float *Wr, const float *br, int R, i
  * rule 0 (threshold, Eq.4): FULL if s >= tau_high; MEAN if s <= tau_low;
  *   SURR strictly between.  The thresholds arrive as fp32 and are widened.
  * rule 1 (argmax over the three logits of a head): the first maximal index.
+ * rules 2 and 3: the two-branch ablation of the compute-mode study (no
+ *   surrogate, only mean pooling and full attention): rule 2 is FULL if
+ *   s >= tau_high, else MEAN; rule 3 compares only the MEAN and FULL logits,
+ *   MEAN on a tie.
  * A NaN score sends the head to FULL (the paper is silent; FULL is exact).
  */
 void or_assign(const double *scores, int H, int rule, float tau_low, float tau_high,
                uint8_t *modes) {
     for (int h = 0; h < H; ++h) {
-        if (rule == 0) {
+        if (rule == 0 || rule == 2) {
             double s = scores[h];
             if (isnan(s) || s >= (double)tau_high)
                 modes[h] = OR_MODE_FULL;
-            else if (s <= (double)tau_low)
+            else if (rule == 2 || s <= (double)tau_low)
                 modes[h] = OR_MODE_MEAN;
             else
                 modes[h] = OR_MODE_SURR;
-        } else {
+        } else if (rule == 1) {
             const double *lg = scores + (int64_t)h * 3;
             int best = 0, bad = isnan(lg[0]);
             for (int m = 1; m < 3; ++m) {
@@ -238,6 +242,13 @@ void or_assign(const double *scores, int H, int rule, float tau_low, float tau_h
                 if (lg[m] > lg[best]) best = m;
             }
             modes[h] = bad ? OR_MODE_FULL : (uint8_t)best;
+        } else {
+            const double *lg = scores + (int64_t)h * 3;
+            const double mean_l = lg[OR_MODE_MEAN], full_l = lg[OR_MODE_FULL];
+            if (isnan(mean_l) || isnan(full_l))
+                modes[h] = OR_MODE_FULL;
+            else
+                modes[h] = full_l > mean_l ? OR_MODE_FULL : OR_MODE_MEAN;
         }
     }
 }
@@ -304,11 +315,15 @@ void or_full_rows(const float *Q, const float *K, const float *V, int64_t N, int
  *   y_i = C_h + gamma (.) delta                                        (Eq.7)
  * Each MLP is Linear(2d -> L) -> act -> Linear(L -> d), with biases;
  * act 0 = GELU (erf form), act 1 = ReLU.  w1 is [L, 2d], w2 is [d, L].
+ * variant 0: Eq.7 as above; 2: the "no residual" ablation of the component
+ * study, y_i = C_h; 3: identity added, y_i = v_{h,i} + C_h + gamma (.) delta.
+ * (The "mean context" ablation is variant 0 with C_h replaced by the value
+ * mean, done by the caller.)
  */
 typedef struct {
     const float *V;
     int64_t N;
-    int H, d, h, L, act;
+    int H, d, h, L, act, variant;
     const double *C;
     const float *gw1, *gb1, *gw2, *gb2, *dw1, *db1, *dw2, *db2;
     const int64_t *rows;
@@ -346,20 +361,80 @@ static void surr_body(void *p, int64_t lo, int64_t hi) {
             z[e] = (double)v[e];
             z[d + e] = c->C[e];
         }
+        double *y = c->Y + r * d;
+        if (c->variant == 2) {   /* no residual correction: the context alone */
+            for (int e = 0; e < d; ++e) y[e] = c->C[e];
+            continue;
+        }
         mlp(z, 2 * d, L, d, c->gw1, c->gb1, c->gw2, c->gb2, c->act, hid, g);
         mlp(z, 2 * d, L, d, c->dw1, c->db1, c->dw2, c->db2, c->act, hid, dl);
-        double *y = c->Y + r * d;
-        for (int e = 0; e < d; ++e) y[e] = c->C[e] + sigmoid(g[e]) * dl[e];
+        for (int e = 0; e < d; ++e) {
+            y[e] = c->C[e] + sigmoid(g[e]) * dl[e];
+            if (c->variant == 3) y[e] += z[e];   /* identity added: v + Eq.7 */
+        }
     }
     free(z);
 }
 
 /* Weights passed for head h only (already offset by the caller). */
-void or_surr_rows(const float *V, int64_t N, int H, int d, int h, int L, int act,
+void or_surr_rows(const float *V, int64_t N, int H, int d, int h, int L, int act, int variant,
                   const double *C_h, const float *gw1, const float *gb1, const float *gw2,
                   const float *gb2, const float *dw1, const float *db1, const float *dw2,
                   const float *db2, const int64_t *rows, int64_t nrows, double *Y,
                   int nthreads) {
-    surr_ctx c = {V, N, H, d, h, L, act, C_h, gw1, gb1, gw2, gb2, dw1, db1, dw2, db2, rows, Y};
+    surr_ctx c = {V, N, H, d, h, L, act, variant, C_h, gw1, gb1, gw2, gb2, dw1, db1, dw2, db2,
+                  rows, Y};
     or_parallel_for(nrows, nthreads, surr_body, &c);
+}
+
+/* ------------------------------------- linear attention (compute-mode study) */
+/*
+ * The linear-attention alternative to the surrogate that the compute-mode
+ * ablation evaluates (the kernelised attention of Katharopoulos et al.,
+ * with its feature map phi(x) = elu(x) + 1): for query row i of head h,
+ *   w_j = phi(q_{h,i}) . phi(k_{h,j}),  y_i = sum_j w_j v_{h,j} / sum_j w_j
+ * over all N tokens of all views (non-causal), computed from this definition
+ * row by row (no factorisation).
+ */
+typedef struct {
+    const float *Q, *K, *V;
+    int64_t N;
+    int H, d, h;
+    const int64_t *rows;
+    double *Y;
+} lin_ctx;
+
+static double elu1(double x) { return x > 0.0 ? x + 1.0 : exp(x); }
+
+static void lin_body(void *p, int64_t lo, int64_t hi) {
+    lin_ctx *c = (lin_ctx *)p;
+    const int d = c->d;
+    double *fq = (double *)malloc(sizeof(double) * 2 * d);
+    double *acc = fq + d;
+    for (int64_t r = lo; r < hi; ++r) {
+        const int64_t i = c->rows ? c->rows[r] : r;
+        const float *q = c->Q + (i * c->H + c->h) * (int64_t)d;
+        for (int e = 0; e < d; ++e) {
+            fq[e] = elu1((double)q[e]);
+            acc[e] = 0.0;
+        }
+        double den = 0.0;
+        for (int64_t j = 0; j < c->N; ++j) {
+            const float *k = c->K + (j * c->H + c->h) * (int64_t)d;
+            const float *v = c->V + (j * c->H + c->h) * (int64_t)d;
+            double wj = 0.0;
+            for (int e = 0; e < d; ++e) wj += fq[e] * elu1((double)k[e]);
+            den += wj;
+            for (int e = 0; e < d; ++e) acc[e] += wj * (double)v[e];
+        }
+        double *y = c->Y + r * d;
+        for (int e = 0; e < d; ++e) y[e] = acc[e] / den;
+    }
+    free(fq);
+}
+
+void or_linattn_rows(const float *Q, const float *K, const float *V, int64_t N, int H, int d,
+                     int h, const int64_t *rows, int64_t nrows, double *Y, int nthreads) {
+    lin_ctx c = {Q, K, V, N, H, d, h, rows, Y};
+    or_parallel_for(nrows, nthreads, lin_body, &c);
 }

@@ -36,6 +36,14 @@ MUTANTS = {
     "tau_low_exclusive": ("s <= (double)tau_low", "s < (double)tau_low"),
     "argmax_last_tie": ("if (lg[m] > lg[best]) best = m;", "if (lg[m] >= lg[best]) best = m;"),
     "logit_bias_dropped": ("logits[r] = acc + (double)br[r];", "logits[r] = acc;"),
+    "binary_keeps_surr": ("else if (rule == 2 || s <= (double)tau_low)", "else if (s <= (double)tau_low)"),
+    "binary_tie_to_full": ("modes[h] = full_l > mean_l ? OR_MODE_FULL : OR_MODE_MEAN;",
+                           "modes[h] = full_l >= mean_l ? OR_MODE_FULL : OR_MODE_MEAN;"),
+    "no_residual_keeps_correction": ("if (c->variant == 2) {", "if (c->variant == 99) {"),
+    "identity_not_added": ("if (c->variant == 3) y[e] += z[e];", "if (c->variant == 3) y[e] += 0.0;"),
+    "linattn_phi_no_shift": ("return x > 0.0 ? x + 1.0 : exp(x);", "return x > 0.0 ? x : exp(x);"),
+    "linattn_not_normalised": ("for (int e = 0; e < d; ++e) y[e] = acc[e] / den;",
+                               "for (int e = 0; e < d; ++e) y[e] = acc[e] / (double)c->N;"),
 }
 
 

@@ -386,3 +386,119 @@ def test_surrogate_gate_modulates():
     s["d_b2"][:] = 0
     C = np.random.default_rng(0).normal(size=64)
     np.testing.assert_array_equal(oracle.surr_rows(x.V, C, s, 1), np.broadcast_to(C, (16, 64)))
+
+
+# ------------------------------------ ablation variants (component study,
+# ------------------------------------ compute-mode study)
+
+def test_binary_rules():
+    """Two-branch routing (no surrogate): threshold form is FULL if s >= tau_high
+    else MEAN -- a score between the thresholds, SURR under Eq.4, becomes MEAN;
+    argmax form compares only the MEAN and FULL logits (MEAN on a tie), even
+    when the SURR logit is the largest.  NaN goes to FULL."""
+    th, tl = float(np.float32(0.2)), float(np.float32(0.01))
+    s = np.array([th, np.nextafter(th, 0), 0.05, tl, 0.0, 1.0, np.nan])
+    np.testing.assert_array_equal(oracle.assign(s, oracle.RULE_THRESHOLD), [2, 1, 1, 0, 0, 2, 2])
+    np.testing.assert_array_equal(oracle.assign(s, oracle.RULE_THRESHOLD_BINARY),
+                                  [2, 0, 0, 0, 0, 2, 2])
+    lg = np.array([[1.0, 5.0, 0.0], [0.0, 9.0, 2.0], [3.0, 3.0, 3.0], [0.0, 0.0, 1.0],
+                   [np.nan, 0.0, 0.0], [0.0, np.nan, -1.0]])
+    np.testing.assert_array_equal(oracle.assign(lg, oracle.RULE_ARGMAX_BINARY),
+                                  [0, 2, 0, 2, 2, 0])
+
+
+def test_mean_query_equals_gated_pooling_with_zero_w():
+    """Mean-query ablation: q_pool = mean_i q_i, the same value that the
+    gated pooling of Eq.1-2 gives when W = 0 (uniform alpha)."""
+    x = small(2, 40, H=3)
+    W0 = np.zeros_like(np32(x.W))
+    gated = oracle.router_pool(x.Q, W0, x.U, x.w)
+    np.testing.assert_allclose(oracle.router_pool_mean(x.Q), gated, rtol=1e-12, atol=1e-15)
+    out = oracle.routed_layer(x.Q, x.K, x.V, x.W, x.U, x.w, x.surr, modes=x.modes,
+                              pool=oracle.POOL_MEAN)
+    np.testing.assert_allclose(out["q_pool"], gated, rtol=1e-12, atol=1e-15)
+
+
+def test_mean_context_matches_base_when_routing_is_uniform():
+    """Mean-context ablation: the surrogate sees the value mean instead of C_h.
+    With Q = 0 the routing is uniform, C_h = mean_h, and both variants agree;
+    with real queries they differ."""
+    N, H = 33, 2
+    modes = np.array([1, 1], np.uint8)
+    x = small(1, N, H=H, modes=modes)
+    Q0 = np.zeros((N, H, 64), np.float32)
+    a = oracle.routed_layer(Q0, x.K, x.V, x.W, x.U, x.w, x.surr, modes=modes)
+    b = oracle.routed_layer(Q0, x.K, x.V, x.W, x.U, x.w, x.surr, modes=modes,
+                            surr_variant=oracle.SURR_MEAN_CONTEXT)
+    np.testing.assert_allclose(a["Y"], b["Y"], rtol=1e-11, atol=1e-14)
+    c = oracle.routed_layer(x.Q, x.K, x.V, x.W, x.U, x.w, x.surr, modes=modes)
+    e = oracle.routed_layer(x.Q, x.K, x.V, x.W, x.U, x.w, x.surr, modes=modes,
+                            surr_variant=oracle.SURR_MEAN_CONTEXT)
+    assert np.abs(c["Y"] - e["Y"]).max() > 1e-6
+    # and it is Eq.7 evaluated at the value mean
+    for h in range(H):
+        ref = brute.surrogate(np32(x.V), e["mean"][h], x.surr, h)
+        np.testing.assert_allclose(e["Y"][:, h, :], ref, rtol=1e-10, atol=1e-13)
+
+
+def test_no_residual_is_zero_correction():
+    """No-residual ablation: y = C_h, which is what Eq.7 gives when the
+    correction MLP's output layer is zero."""
+    x = small(1, 21, H=2)
+    s = {k: np32(v).copy() for k, v in x.surr.items()}
+    s["d_w2"][:] = 0
+    s["d_b2"][:] = 0
+    C = np.random.default_rng(1).normal(size=64)
+    np.testing.assert_array_equal(oracle.surr_rows(x.V, C, x.surr, 0, variant=oracle.SURR_NO_RESIDUAL),
+                                  oracle.surr_rows(x.V, C, s, 0))
+
+
+def test_add_identity_closed_form():
+    """Identity-added reading: y = v + C_h + gamma (.) delta; with a zero
+    correction layer y = v + C_h exactly."""
+    x = small(1, 23, H=2)
+    s = {k: np32(v).copy() for k, v in x.surr.items()}
+    s["d_w2"][:] = 0
+    s["d_b2"][:] = 0
+    C = np.random.default_rng(2).normal(size=64)
+    y = oracle.surr_rows(x.V, C, s, 1, variant=oracle.SURR_ADD_IDENTITY)
+    np.testing.assert_allclose(y, np32(x.V)[:, 1, :].astype(np.float64) + C, rtol=1e-15,
+                               atol=1e-15)
+
+
+def _phi(x):
+    return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+@pytest.mark.parametrize("N", [1, 2, 7, 64, 129])
+def test_linear_attention_against_matrix_form(N):
+    """Linear attention (phi = elu + 1): the oracle's row-by-row definition
+    against the explicit matrix A = phi(Q) phi(K)^T, rows normalised, times V."""
+    rng = np.random.default_rng(N)
+    H, d = 2, 64
+    Q = rng.normal(size=(N, H, d)).astype(np.float32)
+    K = rng.normal(size=(N, H, d)).astype(np.float32)
+    V = rng.normal(size=(N, H, d)).astype(np.float32)
+    for h in range(H):
+        A = _phi(Q[:, h].astype(np.float64)) @ _phi(K[:, h].astype(np.float64)).T
+        ref = (A / A.sum(axis=1, keepdims=True)) @ V[:, h].astype(np.float64)
+        np.testing.assert_allclose(oracle.linattn_rows(Q, K, V, h), ref, rtol=1e-11, atol=1e-13)
+
+
+def test_linear_attention_special_cases():
+    """Equal keys give equal weights: y_i = mean of V for every query.  For any
+    keys the weights are positive, so y lies in the per-coordinate hull of V;
+    a joint permutation of the key and value rows changes nothing."""
+    rng = np.random.default_rng(11)
+    N, H, d = 50, 1, 64
+    Q = rng.normal(size=(N, H, d)).astype(np.float32)
+    V = rng.normal(size=(N, H, d)).astype(np.float32)
+    K = np.broadcast_to(rng.normal(size=(1, H, d)), (N, H, d)).astype(np.float32).copy()
+    y = oracle.linattn_rows(Q, K, V, 0)
+    np.testing.assert_allclose(y, np.broadcast_to(V[:, 0].astype(np.float64).mean(axis=0), (N, d)),
+                               rtol=1e-12, atol=1e-14)
+    K = rng.normal(size=(N, H, d)).astype(np.float32)
+    y = oracle.linattn_rows(Q, K, V, 0)
+    assert (y <= V[:, 0].max(axis=0) + 1e-12).all() and (y >= V[:, 0].min(axis=0) - 1e-12).all()
+    pi = rng.permutation(N)
+    np.testing.assert_allclose(oracle.linattn_rows(Q, K[pi], V[pi], 0), y, rtol=1e-12, atol=1e-14)
