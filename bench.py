@@ -33,9 +33,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "5a47d80a6923be580b02fcc7d8c7642e07c860b22492b9fd8d1a597d52616d5a",
+    "source_sha256": "2c0568eee35564725778c28301f6988c51da0dd8b03a8fb128dc620701b67975",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1531126, "write_kib": 104942,
+    "fetch_kib": 1531126, "write_kib": 104945,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 

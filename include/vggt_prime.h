@@ -57,9 +57,31 @@ typedef enum { VP_F32 = 0, VP_BF16 = 1 } vp_dtype;
 enum { VP_MODE_MEAN = 0, VP_MODE_SURR = 1, VP_MODE_FULL = 2, VP_NUM_MODES = 3 };
 
 typedef enum {
-    VP_ASSIGN_THRESHOLD = 0, /* Eq.4 on the saliency scores s_h */
-    VP_ASSIGN_ARGMAX = 1     /* first argmax over the three per-head logits */
+    VP_ASSIGN_THRESHOLD = 0,        /* Eq.4 on the saliency scores s_h */
+    VP_ASSIGN_ARGMAX = 1,           /* first argmax over the three per-head logits */
+    /* Binary routing of the compute-mode study (Section 5.3, Table 6): two modes
+     * only, FULL and MEAN. */
+    VP_ASSIGN_THRESHOLD_BINARY = 2, /* FULL if s_h >= tau_high, MEAN otherwise */
+    VP_ASSIGN_ARGMAX_BINARY = 3     /* FULL if its logit beats MEAN's, MEAN otherwise */
 } vp_assign_rule;
+
+/* Query pooling of the router (component study, Section 5.3, Table 5). */
+typedef enum {
+    VP_POOL_GATED = 0, /* gated attention pooling, Eq.1-2 */
+    VP_POOL_MEAN = 1   /* "mean query": q_pool = (1/N) sum_i q_i (W, U, w unused) */
+} vp_pool;
+
+/* How SURR heads are computed: Eq.5-7, or one of the ablations of the
+ * component study (Section 5.3, Table 5) and of the compute-mode study (Table 6). */
+typedef enum {
+    VP_SURR_EQ7 = 0,          /* y_i = C_h + gamma_i (.) delta_i (Eq.5-7) */
+    VP_SURR_MEAN_CONTEXT = 1, /* Eq.6-7 with C_h replaced by the value mean */
+    VP_SURR_NO_RESIDUAL = 2,  /* y_i = C_h (MLP weights unused) */
+    VP_SURR_ADD_IDENTITY = 3, /* y_i = v_{h,i} + C_h + gamma_i (.) delta_i */
+    VP_SURR_LINEAR_ATTN = 4   /* linear attention with phi(x) = elu(x) + 1 over all
+                                 N tokens: y_i = sum_j (phi(q_i).phi(k_j)) v_j /
+                                 sum_j phi(q_i).phi(k_j) (MLP weights unused) */
+} vp_surr_variant;
 
 typedef enum { VP_ACT_GELU_ERF = 0, VP_ACT_RELU = 1 } vp_act;
 
@@ -79,11 +101,13 @@ typedef struct {
 
 /* Gated attention pooling parameters (Eq.1): W, U are [H, L, d], w is [H, L],
  * all in shape.dtype; no biases.  `scale` multiplies q_pool . k in the
- * single-query attention (1/sqrt(d) when 0 is passed). */
+ * single-query attention (1/sqrt(d) when 0 is passed).  With pool =
+ * VP_POOL_MEAN, W, U and w are not read and may be NULL (L is still 64). */
 typedef struct {
     const void *W, *U, *w;
     int32_t L;
     float scale;
+    vp_pool pool;
 } vp_router_weights;
 
 /* Router outputs, device fp32, written by vp_router_score:
@@ -100,18 +124,21 @@ typedef struct {
 /* Surrogate MLPs (Eq.6), per head: Linear(2d -> L) -> act -> Linear(L -> d)
  * acting on z = [v_{h,i}; C_h].  *_w1 [H, L, 2d] and *_w2 [H, d, L] in
  * shape.dtype; biases *_b1 [H, L], *_b2 [H, d] fp32.  g_* is the gate MLP
- * (gamma = sigmoid(MLP_gamma(z))), d_* the correction MLP (delta). */
+ * (gamma = sigmoid(MLP_gamma(z))), d_* the correction MLP (delta).
+ * `variant` selects Eq.5-7 or an ablation; the variants NO_RESIDUAL and
+ * LINEAR_ATTN read no weight (the pointers may then be NULL). */
 typedef struct {
     const void *g_w1, *g_w2, *d_w1, *d_w2;
     const float *g_b1, *g_b2, *d_b1, *d_b2;
     int32_t L;
     vp_act act;
+    vp_surr_variant variant;
 } vp_surrogate_weights;
 
-/* Bytes of device workspace that vp_router_score and
- * vp_routed_global_attention need for `shape` (0 if the shape is invalid).
- * The workspace holds router partial sums, the gathered keys and values of
- * FULL heads and the FULL kernel's partial results; it must be 256-byte
+/* Bytes of device workspace that vp_router_score, vp_routed_global_attention
+ * and its stages need for `shape` (0 if the shape is invalid).  The workspace
+ * holds router partial sums, the gathered keys and values of FULL heads, the
+ * FULL kernel's partial results and the linear-attention sums; it must be 256-byte
  * aligned and may be reused across calls on one stream (calls on different
  * streams need separate workspaces). */
 size_t vp_workspace_bytes(const vp_shape *shape);
@@ -132,7 +159,10 @@ vp_status vp_router_logits(const float *u, const void *W_r, const float *b_r, in
 
 /* Mode assignment (Eq.4).  THRESHOLD: scores = s_h [H]; FULL if s >= tau_high,
  * MEAN if s <= tau_low, SURR otherwise (0 <= tau_low <= tau_high).  ARGMAX:
- * scores = logits [H, 3]; the first maximal mode.  NaN -> FULL + flag.
+ * scores = logits [H, 3]; the first maximal mode.  THRESHOLD_BINARY: FULL if
+ * s >= tau_high, else MEAN (tau_low is checked but unused).  ARGMAX_BINARY:
+ * FULL if logit[FULL] > logit[MEAN], else MEAN (the SURR logit is ignored).
+ * NaN (in a score or a compared logit) -> FULL + flag.
  * Writes modes [H] (uint8) and buckets [VP_BUCKETS_LEN] (int32):
  *   buckets[0..2]   number of heads in MEAN, SURR, FULL;
  *   buckets[3..3+H) head ids grouped by mode (MEAN, then SURR, then FULL),
@@ -147,7 +177,8 @@ vp_status vp_assign_heads(const float *scores, int32_t H, vp_assign_rule rule, f
  * MEAN and SURR kernels read modes[h], the FULL kernels take the FULL head
  * list from buckets; nothing is copied back to the host.
  *   FULL heads: softmax(Q_h K_h^T / sqrt(d)) V_h over all N tokens;
- *   SURR heads: C_h + gamma (.) delta with C_h = state->ctx (Eq.5-7);
+ *   SURR heads: C_h + gamma (.) delta with C_h = state->ctx (Eq.5-7), or
+ *               the ablation surr->variant names;
  *   MEAN heads: every row = state->vmean[h].
  * `state` must hold the vp_router_score outputs for the same Q, K, V.
  * `surr` must be non-NULL (its weights are read only for SURR heads).
@@ -163,24 +194,29 @@ vp_status vp_routed_global_attention(const vp_shape *shape, const void *Q, const
  * for callers that schedule or time them separately (same arguments and
  * requirements as vp_routed_global_attention; run all three, in this order,
  * on one stream, to obtain the same Y).
- *   vp_gather_full_heads:   packs V (tile-transposed) and K (fp16 tiles) of
- *                           each FULL head into the workspace (bf16 layers;
- *                           no-op for fp32) and records the largest key norm
- *                           of every 64-key tile;
+ *   vp_gather_full_heads:   packs V (tile-transposed, scaled by a power of
+ *                           two per head, fp16) and K (fp16 tiles) of each
+ *                           FULL head into the workspace (bf16 layers; no-op
+ *                           for fp32) and records the largest key norm of
+ *                           every 64-key tile;
  *   vp_full_head_attention: exact softmax attention of every FULL head
  *                           (Algorithm 1, first branch); reads the packed
  *                           tiles the gather left in `ws`.  Results are
  *                           deterministic for a given device (the split of
  *                           work over its compute units is fixed);
- *   vp_linear_heads:        SURR (Eq.5-7) and MEAN heads. */
+ *   vp_linear_heads:        SURR (Eq.5-7, or surr->variant) and MEAN heads.
+ *                           Q, K and ws are read only by the LINEAR_ATTN
+ *                           variant (they may be NULL / 0 otherwise), which
+ *                           keeps its per-head sums in ws. */
 vp_status vp_gather_full_heads(const vp_shape *shape, const void *K, const void *V,
                                const int32_t *buckets, void *ws, size_t ws_bytes, void *stream);
 vp_status vp_full_head_attention(const vp_shape *shape, const void *Q, const void *K,
                                  const void *V, const int32_t *buckets, void *Y,
                                  vp_dtype y_dtype, void *ws, size_t ws_bytes, void *stream);
-vp_status vp_linear_heads(const vp_shape *shape, const void *V, const uint8_t *modes,
-                          const vp_router_state *state, const vp_surrogate_weights *surr,
-                          void *Y, vp_dtype y_dtype, void *stream);
+vp_status vp_linear_heads(const vp_shape *shape, const void *Q, const void *K, const void *V,
+                          const uint8_t *modes, const vp_router_state *state,
+                          const vp_surrogate_weights *surr, void *Y, vp_dtype y_dtype,
+                          void *ws, size_t ws_bytes, void *stream);
 
 /* Static description of a status code. */
 const char *vp_status_string(vp_status s);

@@ -14,7 +14,10 @@ closed forms (planted key, zero queries, one-hot router rows), invariants
 a numpy brute force on tiny shapes.  The surrogate MLP's exact architecture is
 a reading of the paper (it gives only "a lightweight MLP" of hidden size 64):
 its structure is pinned by closed-form special cases, but no paper number
-fixes it -- parity unpinned as to the architecture itself.
+fixes it -- parity unpinned as to the architecture itself.  Likewise the
+feature map of the linear-attention ablation (phi = elu + 1, the map of the
+kernelised attention the paper cites) is a reading: the computation given phi
+is pinned against its explicit-matrix form, the choice of phi is unpinned.
 """
 from __future__ import annotations
 

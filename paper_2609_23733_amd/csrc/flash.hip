@@ -31,27 +31,92 @@ __device__ __forceinline__ int full_head(const int32_t* buckets, int H, int slot
 constexpr int kLdsRow = 72;   // bf16 LDS row stride (144 B: 16-B aligned, bank-staggered)
 
 // ------------------------------------------------------------------------
-// K5: bucket gather.  For each FULL head (slot s of the FULL bucket), copy V_h
-// into a packed, tile-transposed buffer Vt[s][tile][d][64 keys], K_h into
-// packed fp16 tiles Kh[s][tile][64 keys][d] (key rows in swap23 order; bf16
-// values convert exactly while |k| stays in fp16's normal range), keys past N
-// zero in both, and record kmax[s][tile] = max |k_j| over the tile's keys.
-// The attention kernels read the tiles as contiguous 8 KB blocks whose rows
-// feed the MFMA operands directly, and use kmax to bound the logits.
+// K5a, K5b: the scale of each FULL head's packed values.  The attention
+// kernels multiply fp16 weights with fp16 values; the gather stores
+// V_h 2^-e_h, with e_h chosen so that the head's largest |v| lies in
+// [2^14, 2^15), and the kernels multiply O by 2^e_h at the end (both scalings
+// exact).  Every bf16 value then fits fp16's range; values more than 2^29
+// below the head's largest land in fp16's subnormals (absolute error at most
+// 2^-40 of that largest value).
+// K5a: per (group of kVmaxTiles key tiles, FULL slot), max |v|;
+// K5b: per FULL slot, the maximum of those and vsc[slot] = (2^-e_h, 2^e_h).
+// ------------------------------------------------------------------------
+constexpr int kVmaxTiles = 16;
+
+__device__ __forceinline__ float block_max256(float m, float* red) {
+    m = wave_max(m);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+    __syncthreads();
+    return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+__global__ __launch_bounds__(256) void k_vmax_partial(const bf16* __restrict__ V,
+                                                      const int32_t* __restrict__ buckets,
+                                                      int64_t N, int H,
+                                                      float* __restrict__ vpart) {
+    const int slot = blockIdx.y;
+    if (slot >= full_count(buckets, H)) return;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    const int64_t r0 = (int64_t)blockIdx.x * kVmaxTiles * kBK;
+    const int64_t r1 = (r0 + kVmaxTiles * kBK < N) ? r0 + kVmaxTiles * kBK : N;
+    const int seg = (threadIdx.x & 7) * 8;
+    float m = 0.f;
+    for (int64_t row = r0 + (threadIdx.x >> 3); row < r1; row += 32) {
+        const bf16x8 v = load_bf16x8(V + (row * H + h) * kD + seg);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(bf16_to_f32(v[j])));
+    }
+    __shared__ float red[4];
+    m = block_max256(m, red);
+    if (threadIdx.x == 0) vpart[(int64_t)slot * gridDim.x + blockIdx.x] = m;
+}
+
+__global__ __launch_bounds__(256) void k_vscale(const float* __restrict__ vpart, int nparts,
+                                                const int32_t* __restrict__ buckets, int H,
+                                                float* __restrict__ vsc) {
+    const int slot = blockIdx.x;
+    if (slot >= full_count(buckets, H)) return;
+    float m = 0.f;
+    for (int i = threadIdx.x; i < nparts; i += 256) m = fmaxf(m, vpart[(int64_t)slot * nparts + i]);
+    __shared__ float red[4];
+    m = block_max256(m, red);
+    if (threadIdx.x == 0) {
+        // An all-zero head keeps scale 1; an infinite value (NaN never wins
+        // fmaxf) keeps scale 1 too and reaches the output as it would in
+        // exact arithmetic.
+        int e = 0;
+        if (m > 0.f && m <= 3.4028235e38f) e = ilogbf(m) - 14;
+        e = e < -126 ? -126 : (e > 126 ? 126 : e);
+        vsc[2 * slot] = ldexpf(1.f, -e);
+        vsc[2 * slot + 1] = ldexpf(1.f, e);
+    }
+}
+
+// ------------------------------------------------------------------------
+// K5: bucket gather.  For each FULL head (slot s of the FULL bucket), copy
+// V_h 2^-e_h into a packed, tile-transposed fp16 buffer Vt[s][tile][d][64
+// keys], K_h into packed fp16 tiles Kh[s][tile][64 keys][d] (key rows in
+// swap23 order; bf16 values convert exactly while |k| stays in fp16's normal
+// range), keys past N zero in both, and record kmax[s][tile] = max |k_j| over
+// the tile's keys.  The attention kernels read the tiles as contiguous 8 KB
+// blocks whose rows feed the MFMA operands directly, and use kmax to bound
+// the logits.
 // ------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
                                                    const bf16* __restrict__ V,
                                                    const int32_t* __restrict__ buckets, int64_t N,
-                                                   int H, int nkt, bf16* __restrict__ Vt,
-                                                   f16* __restrict__ Kh,
+                                                   int H, int nkt, const float* __restrict__ vsc,
+                                                   f16* __restrict__ Vt, f16* __restrict__ Kh,
                                                    float* __restrict__ kmax) {
     const int slot = blockIdx.y, tile = blockIdx.x;
     const int nfull = full_count(buckets, H);
     if (slot >= nfull) return;
     const int h = full_head(buckets, H, slot);
     if (h < 0) return;
-    __shared__ __attribute__((aligned(16))) bf16 s[kD * kLdsRow];
+    __shared__ __attribute__((aligned(16))) f16 s[kD * kLdsRow];
     __shared__ float s_norm[4];
+    const float down = vsc[2 * slot];
     const int t = threadIdx.x;
     const int key = t >> 2, dseg = (t & 3) * 16;
     const int64_t row = (int64_t)tile * kBK + key;
@@ -62,8 +127,8 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
     if (!ok) a = b = ka = kb = zero_bf16x8();
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        s[(dseg + j) * kLdsRow + key] = a[j];
-        s[(dseg + 8 + j) * kLdsRow + key] = b[j];
+        s[(dseg + j) * kLdsRow + key] = (f16)(bf16_to_f32(a[j]) * down);
+        s[(dseg + 8 + j) * kLdsRow + key] = (f16)(bf16_to_f32(b[j]) * down);
     }
     float n2 = 0.f;
     f16x8 ha, hb;
@@ -86,10 +151,10 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
         kmax[(int64_t)slot * nkt + tile] =
             sqrtf(fmaxf(fmaxf(s_norm[0], s_norm[1]), fmaxf(s_norm[2], s_norm[3])));
     const int d = t >> 2, kseg = (t & 3) * 16;
-    bf16* dst = Vt + (((int64_t)slot * nkt + tile) * kD + d) * kBK + kseg;
-    *reinterpret_cast<bf16x8*>(dst) = *reinterpret_cast<const bf16x8*>(&s[d * kLdsRow + kseg]);
-    *reinterpret_cast<bf16x8*>(dst + 8) =
-        *reinterpret_cast<const bf16x8*>(&s[d * kLdsRow + kseg + 8]);
+    f16* dst = Vt + (((int64_t)slot * nkt + tile) * kD + d) * kBK + kseg;
+    *reinterpret_cast<f16x8*>(dst) = *reinterpret_cast<const f16x8*>(&s[d * kLdsRow + kseg]);
+    *reinterpret_cast<f16x8*>(dst + 8) =
+        *reinterpret_cast<const f16x8*>(&s[d * kLdsRow + kseg + 8]);
 }
 
 // ------------------------------------------------------------------------
@@ -105,37 +170,40 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 // Softmax is invariant to the reference point subtracted from the logits
 // before exponentiation.  K6a uses zero: when Cauchy-Schwarz bounds every
 // logit of a workgroup's queries by kFastBound in log2 units
-// (|q . k| c <= |c q| max_j |k_j|), p = 2^x stays within [2^-32, 2^32] and a
-// score costs one exp2, half a bf16 pack and half a dot2 (row sums of the
-// packed P).  The scale c = log2(e) / sqrt(d) is folded into Q, rounded to
+// (|q . k| c <= |c q| max_j |k_j|), p = 2^x stays within [2^-14, 2^14], fp16's
+// normal range, and a score costs one exp2, half an fp16 pack and one add
+// (row sums).  The scale c = log2(e) / sqrt(d) is folded into Q, rounded to
 // fp16 (relative error 2^-11; K converts exactly), so S comes out of an fp16
-// MFMA in log2 units.  Work items outside that bound (or outside fp16's safe
-// range) are flagged and left to K6b, which keeps bf16 Q and K exact, scales
-// in fp32 and carries a running reference point m: a tile whose logits
-// provably stay below m + kSlack is exponentiated against m directly
-// (p <= 2^8); only otherwise is the tile maximum computed, and m moves
-// (rescaling O and l) only when the tile exceeds m + kSlack.
+// MFMA in log2 units; P and the scaled V are fp16 too (P rounded to nearest:
+// relative error at most 2^-11).  Work items outside that bound (or outside
+// fp16's safe range for Q and K) are flagged and left to K6b, which keeps
+// bf16 Q and K exact, scales in fp32 and carries a running reference point m:
+// a tile whose logits provably stay below m + kSlack is exponentiated against
+// m directly (p <= 2^8, fp16 again); only otherwise is the tile maximum
+// computed, and m moves (rescaling O and l) only when the tile exceeds
+// m + kSlack.
 // ------------------------------------------------------------------------
 constexpr int kBQ16 = 256;
 constexpr float kSlack = 8.f;        // log2 headroom above a running reference point
-constexpr float kFastBound = 32.f;   // |logit| bound (log2 units) for reference point 0
+constexpr float kFastBound = 14.f;   // |logit| bound (log2 units) for reference point 0
 constexpr float kF16Safe = 4096.f;   // |c q|, |k| limit for the fp16 logit path
 
 __device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
-    const bf16x2 v = __builtin_bit_cast(bf16x2, pair);
-    const bf16x2 one = {(bf16)1.0f, (bf16)1.0f};
-    return __builtin_amdgcn_fdot2_f32_bf16(v, one, acc, false);
+    const f16x2 v = __builtin_bit_cast(f16x2, pair);
+    const f16x2 one = {(f16)1.0f, (f16)1.0f};
+    return __builtin_amdgcn_fdot2(v, one, acc, false);
 }
 
-// Y[q, h, d] = O / l for the wave's two 32-query blocks; lane holds
-// d = 32 db + 8 g + 4 hh + i for i = 0..3.
+// Y[q, h, d] = O up / l for the wave's two 32-query blocks (up = 2^e_h, the
+// inverse of the packed values' scale); lane holds d = 32 db + 8 g + 4 hh + i
+// for i = 0..3.
 __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float (&l)[2],
                                            const int64_t (&qidx)[2], int64_t N, int H, int h,
-                                           int hh, void* __restrict__ Y, int ydt) {
+                                           int hh, float up, void* __restrict__ Y, int ydt) {
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         const float lt = l[qb] + __shfl_xor(l[qb], 32);
-        const float inv = 1.f / lt;
+        const float inv = up / lt;
         const int64_t qi = qidx[qb];
         if (qi < N) {
 #pragma unroll
@@ -165,7 +233,7 @@ __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float 
 // workgroup barrier per phase, so that in every phase one wave of each SIMD
 // issues MFMAs while the other issues the softmax's exp2 / pack / sums:
 //   matrix(t): O += V(t-1) P(t-1)  then  S(t) = K(t) (c Q)^T   (32 MFMAs)
-//   vector(t): P(t) = bf16(2^S(t)) (round to nearest, one pack per pair),
+//   vector(t): P(t) = fp16(2^S(t)) (round to nearest, one pack per pair),
 //              l += row sums of the fp32 2^S(t) (the packing error has zero
 //              mean, so l needs no rounded copy: five vector instructions per
 //              pair of scores, the fewest found)
@@ -205,8 +273,9 @@ __device__ __forceinline__ int tail_owner(int64_t x, int64_t T, int G) {
 
 __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ Q,
                                                        const f16* __restrict__ Kh,
-                                                       const bf16* __restrict__ Vt,
+                                                       const f16* __restrict__ Vt,
                                                        const float* __restrict__ kmax,
+                                                       const float* __restrict__ vsc,
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        int32_t* __restrict__ wide_items,
@@ -224,7 +293,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
     const bool groupB = wave >= 4;
 
     __shared__ __attribute__((aligned(16))) f16 sK[2][kBK * kLdsRow];
-    __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kLdsRow];
+    __shared__ __attribute__((aligned(16))) f16 sV[2][kD * kLdsRow];
     __shared__ float sKmax[8];
     __shared__ int sWide[8];
 
@@ -293,7 +362,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         const int ns = t1 - t0;
         const int tl = threadIdx.x & 255, lr = tl >> 2, lc = (tl & 3) * 16;
         const f16* Khh = Kh + ((int64_t)slot * nkt + t0) * kBK * kD;
-        const bf16* Vth = Vt + ((int64_t)slot * nkt + t0) * kD * kBK;
+        const f16* Vth = Vt + ((int64_t)slot * nkt + t0) * kD * kBK;
         u32x4 g0, g1;
         auto fetch = [&](int r) {   // tile r (clamped to the last one) into registers
             r = r < ns ? r : ns - 1;
@@ -311,14 +380,15 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         };
 
         f32x16 O[2][2], S[2][2];
-        bf16x8 P[2][2][2];
+        f16x8 P[2][2][2];
         float l[2];
+        const f16x8 zp = {};
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
             O[qb][0] = O[qb][1] = zero_f32x16();
             l[qb] = 0.f;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) P[qb][kb][0] = P[qb][kb][1] = zero_bf16x8();
+            for (int kb = 0; kb < 2; ++kb) P[qb][kb][0] = P[qb][kb][1] = zp;
         }
 
         // Matrix phase of tile r: O += V(r-1) P(r-1) from sV[r%2], then S(r)
@@ -332,17 +402,17 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                     for (int b = 0; b < 2; ++b) {
-                        const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                        const f16x8 a = *reinterpret_cast<const f16x8*>(
                             &sV[sl][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
-                        O[0][db] = mfma_bf16(a, P[0][kb][b], O[0][db]);
-                        O[1][db] = mfma_bf16(a, P[1][kb][b], O[1][db]);
+                        O[0][db] = mfma_f16(a, P[0][kb][b], O[0][db]);
+                        O[1][db] = mfma_f16(a, P[1][kb][b], O[1][db]);
                     }
         };
         auto mma_phase = [&](int r) {
             const int sl = r & 1;
             // All 16 LDS operands of the phase are requested first, so LDS
             // latency is paid once per phase rather than once per two reads.
-            bf16x8 va[2][2][2];
+            f16x8 va[2][2][2];
             f16x8 ka[2][4];
 #pragma unroll
             for (int db = 0; db < 2; ++db)
@@ -350,7 +420,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                     for (int b = 0; b < 2; ++b)
-                        va[db][kb][b] = *reinterpret_cast<const bf16x8*>(
+                        va[db][kb][b] = *reinterpret_cast<const f16x8*>(
                             &sV[sl][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -364,8 +434,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                     for (int b = 0; b < 2; ++b) {
-                        O[0][db] = mfma_bf16(va[db][kb][b], P[0][kb][b], O[0][db]);
-                        O[1][db] = mfma_bf16(va[db][kb][b], P[1][kb][b], O[1][db]);
+                        O[0][db] = mfma_f16(va[db][kb][b], P[0][kb][b], O[0][db]);
+                        O[1][db] = mfma_f16(va[db][kb][b], P[1][kb][b], O[1][db]);
                     }
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -406,11 +476,11 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                             e[0] = exp2f_fast(S[qb][kb][8 * b + 2 * j]);
                             e[1] = exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]);
                             pk[j] = __builtin_bit_cast(uint32_t,
-                                                       __builtin_convertvector(e, bf16x2));
+                                                       __builtin_convertvector(e, f16x2));
                             ls0 += e[0];
                             ls1 += e[1];
                         }
-                        P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
+                        P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                     }
                 l[qb] += ls0 + ls1;
             }
@@ -477,7 +547,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         pv(ns & 1);   // O += V(ns-1) P(ns-1)
 
         if (t0 == 0 && t1 == nkt) {
-            store_rows(O, l, qidx, N, H, h, hh, Y, ydt);
+            store_rows(O, l, qidx, N, H, h, hh, vsc[2 * slot + 1], Y, ydt);
         } else {
             // Partial slot: O[q][d] unnormalized, then l[q], q = row in item.
             float* ps = part + (int64_t)(w * 2 + pslot) * kPartFloats;
@@ -521,12 +591,13 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 
 // K6c: Y of the tail items that K6a split over workgroups: the parts' O and
 // l added in workgroup order (fixed, so results are deterministic), then
-// O / l.  One workgroup of 256 threads per tail item; items that K6a
+// O 2^e_h / l.  One workgroup of 256 threads per tail item; items that K6a
 // finished whole or left to K6b exit at once.
 __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt,
                                                        const int32_t* __restrict__ wide_items,
-                                                       const float* __restrict__ part, int G,
+                                                       const float* __restrict__ part,
+                                                       const float* __restrict__ vsc, int G,
                                                        void* __restrict__ Y, int ydt) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
@@ -554,7 +625,7 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
         if (qi >= N) continue;
         float lt = 0.f;
         for (int v = wf; v <= wl; ++v) lt += pslot(v)[kBQf * kD + qr];
-        const float inv = 1.f / lt;
+        const float inv = vsc[2 * slot + 1] / lt;
 #pragma unroll 1
         for (int d0 = 0; d0 < kD; d0 += 8) {
             float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -593,18 +664,21 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
 // hold eight consecutive keys per lane-half: they become the B operand of the
 // PV MFMA without any data movement.
 //
-// Softmax work per score is one FMA, one exp2, half a bf16 pack and half a
+// Softmax work per score is one FMA, one exp2, half an fp16 pack and half a
 // dot2 (row sums of the packed P).  The running maximum m is a reference
 // point, not necessarily the exact maximum: a tile whose logits provably stay
 // below m + 8 (in log2 units; Cauchy-Schwarz, |q . k| c <= |q| c max|k|) is
-// exponentiated against m directly, so p <= 2^8.  Only otherwise is the tile
-// maximum computed, and m moves (rescaling O and l) only when the tile
-// exceeds m + 8.  O / l is unchanged by the choice of reference point.
+// exponentiated against m directly, so p <= 2^8 fits fp16.  Only otherwise is
+// the tile maximum computed, and m moves (rescaling O and l) only when the
+// tile exceeds m + 8; the key that set m has p = 1, so l >= 1 and weights
+// below fp16's normal range add at most 2^-25 each.  O / l is unchanged by
+// the choice of reference point.
 // ------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restrict__ Q,
                                                        const bf16* __restrict__ K,
-                                                       const bf16* __restrict__ Vt,
+                                                       const f16* __restrict__ Vt,
                                                        const float* __restrict__ kmax,
+                                                       const float* __restrict__ vsc,
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        const int32_t* __restrict__ wide_items,
@@ -620,7 +694,7 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
     const int n = lane & 31, hh = lane >> 5;
 
     __shared__ __attribute__((aligned(16))) bf16 sK[2][kBK * kLdsRow];
-    __shared__ __attribute__((aligned(16))) bf16 sV[2][kD * kLdsRow];
+    __shared__ __attribute__((aligned(16))) f16 sV[2][kD * kLdsRow];
 
     // Q^T operands of this wave's two 32-query blocks, kept in registers,
     // and |q| * c per query for the logit bound.
@@ -650,9 +724,10 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
 
     // Global -> LDS copy assignment: 64 rows x 4 segments of 16 elements.
     const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
-    const bf16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
+    const f16* Vth = Vt + (int64_t)slot * nkt * kD * kBK;
     const float* kmx = kmax + (int64_t)slot * nkt;
-    bf16x8 pk0, pk1, pv0, pv1;
+    bf16x8 pk0, pk1;
+    f16x8 pv0, pv1;
     // Keys past N read row 0 instead (always in bounds); their logits are
     // masked to -inf in the last tile, so their values never matter.  (No
     // select on the loaded data: it would stall on the prefetch.)
@@ -661,17 +736,17 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
         const bf16* kp = K + ((key < N ? key : 0) * H + h) * kD + lc;
         pk0 = load_bf16x8(kp);
         pk1 = load_bf16x8(kp + 8);
-        const bf16* vp = Vth + ((int64_t)t * kD + lr) * kBK + lc;
-        pv0 = load_bf16x8(vp);
-        pv1 = load_bf16x8(vp + 8);
+        const f16* vp = Vth + ((int64_t)t * kD + lr) * kBK + lc;
+        pv0 = *reinterpret_cast<const f16x8*>(vp);
+        pv1 = *reinterpret_cast<const f16x8*>(vp + 8);
     };
     auto lstore = [&](int buf) {
         bf16* kd = &sK[buf][swap23(lr) * kLdsRow + lc];
         *reinterpret_cast<bf16x8*>(kd) = pk0;
         *reinterpret_cast<bf16x8*>(kd + 8) = pk1;
-        bf16* vd = &sV[buf][lr * kLdsRow + lc];
-        *reinterpret_cast<bf16x8*>(vd) = pv0;
-        *reinterpret_cast<bf16x8*>(vd + 8) = pv1;
+        f16* vd = &sV[buf][lr * kLdsRow + lc];
+        *reinterpret_cast<f16x8*>(vd) = pv0;
+        *reinterpret_cast<f16x8*>(vd + 8) = pv1;
     };
 
     f32x16 O[2][2];
@@ -696,7 +771,7 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
         // done one after the other to keep one S^T live (the K operand is
         // re-read from LDS for the second block).
         const bool last = (int64_t)(t + 1) * kBK > N;
-        bf16x8 P[2][2][2];
+        f16x8 P[2][2][2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
             f32x16 S[2];
@@ -738,9 +813,10 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
 #pragma unroll
                     for (int r = 0; r < 16; ++r) O[qb][db][r] *= al;
             }
-            // p = 2^(s c - m), packed to bf16; row sums from the packed values.
+            // p = 2^(s c - m), packed to fp16; row sums from the packed values,
+            // per tile from zero, then added to l.
             const float nm = -m[qb];
-            float ls = l[qb];
+            float ls = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -751,12 +827,12 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
                         f32x2 e;
                         e[0] = exp2f_fast(fmaf(S[kb][8 * b + 2 * j], c, nm));
                         e[1] = exp2f_fast(fmaf(S[kb][8 * b + 2 * j + 1], c, nm));
-                        pk[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, bf16x2));
+                        pk[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, f16x2));
                         ls = dot2_ones(pk[j], ls);
                     }
-                    P[qb][kb][b] = __builtin_bit_cast(bf16x8, pk);
+                    P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                 }
-            l[qb] = ls;
+            l[qb] += ls;
         }
 
         // O^T += V^T P^T
@@ -766,17 +842,17 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int b = 0; b < 2; ++b) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                    const f16x8 a = *reinterpret_cast<const f16x8*>(
                         &sV[buf][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
 #pragma unroll
-                    for (int qb = 0; qb < 2; ++qb) O[qb][db] = mfma_bf16(a, P[qb][kb][b], O[qb][db]);
+                    for (int qb = 0; qb < 2; ++qb) O[qb][db] = mfma_f16(a, P[qb][kb][b], O[qb][db]);
                 }
 
         if (t + 1 < nkt) lstore(buf ^ 1);
         __syncthreads();
     }
 
-    store_rows(O, l, qidx, N, H, h, hh, Y, ydt);
+    store_rows(O, l, qidx, N, H, h, hh, vsc[2 * slot + 1], Y, ydt);
 }
 
 // ------------------------------------------------------------------------
@@ -871,19 +947,20 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
         const float mn = fmaxf(m, mx * c);
         const float al = exp2f_fast(m - mn);
         m = mn;
-        l *= al;
-#pragma unroll
-        for (int db = 0; db < 2; ++db)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) O[db][r] *= al;
+        // Two-level sums: the tile's weights and its PV product are summed
+        // from zero, then added to the running l and O, so that rounding
+        // grows with the tile count rather than the key count.
+        float ls = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const float p = exp2f_fast(fmaf(S[kb][r], c, -mn));
                 S[kb][r] = p;
-                l += p;
+                ls += p;
             }
+        l = fmaf(l, al, ls);
+        f32x16 Ot[2] = {zero_f32x16(), zero_f32x16()};
 #pragma unroll
         for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -891,8 +968,12 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-                    O[db] = mfma_f32(sV[buf][key * kD + db * 32 + n], S[kb][r], O[db]);
+                    Ot[db] = mfma_f32(sV[buf][key * kD + db * 32 + n], S[kb][r], Ot[db]);
                 }
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) O[db][r] = fmaf(O[db][r], al, Ot[db][r]);
         if (t + 1 < nkt) lstore(buf ^ 1);
         __syncthreads();
     }
@@ -933,11 +1014,21 @@ size_t flash_part_bytes(int64_t N, int H) {
     return (size_t)2 * flash_stream_groups(N, H) * kPartFloats * sizeof(float);
 }
 
+int64_t flash_vmax_parts(int64_t N) {
+    const int64_t nkt = (N + kBK - 1) / kBK;
+    return (nkt + kVmaxTiles - 1) / kVmaxTiles;
+}
+
 void launch_gather(const AttnArgs& a, hipStream_t st) {
     const int nkt = (int)((a.N + kBK - 1) / kBK);
+    const int nvp = (int)flash_vmax_parts(a.N);
+    hipLaunchKernelGGL(k_vmax_partial, dim3(nvp, a.H), dim3(256), 0, st, (const bf16*)a.V,
+                       a.buckets, a.N, a.H, a.vpart);
+    hipLaunchKernelGGL(k_vscale, dim3(a.H), dim3(256), 0, st, (const float*)a.vpart, nvp,
+                       a.buckets, a.H, a.vsc);
     hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.K,
-                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (bf16*)a.vt, (f16*)a.kh,
-                       a.kmax);
+                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (const float*)a.vsc,
+                       (f16*)a.vt, (f16*)a.kh, a.kmax);
 }
 
 void launch_flash(const AttnArgs& a, hipStream_t st) {
@@ -949,14 +1040,16 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
         const int nqf = (int)((a.N + kBQf - 1) / kBQf);
         const int G = flash_stream_groups(a.N, a.H);
         hipLaunchKernelGGL(k_flash_bf16, dim3(G), dim3(512), 0, st, (const bf16*)a.Q,
-                           (const f16*)a.kh, (const bf16*)a.vt, (const float*)a.kmax, a.buckets,
-                           a.N, a.H, nqf, nkt, c, a.qflag, a.part, G, a.Y, a.ydt);
+                           (const f16*)a.kh, (const f16*)a.vt, (const float*)a.kmax,
+                           (const float*)a.vsc, a.buckets, a.N, a.H, nqf, nkt, c, a.qflag, a.part,
+                           G, a.Y, a.ydt);
         hipLaunchKernelGGL(k_flash_combine, dim3(G), dim3(256), 0, st, a.buckets, a.N, a.H, nqf,
-                           nkt, (const int32_t*)a.qflag, (const float*)a.part, G, a.Y, a.ydt);
+                           nkt, (const int32_t*)a.qflag, (const float*)a.part,
+                           (const float*)a.vsc, G, a.Y, a.ydt);
         hipLaunchKernelGGL(k_flash_bf16_wide, dim3(nqt * a.H), dim3(256), 0, st,
-                           (const bf16*)a.Q, (const bf16*)a.K, (const bf16*)a.vt,
-                           (const float*)a.kmax, a.buckets, a.N, a.H, nqt, nkt, c, a.qflag, nqf,
-                           a.Y, a.ydt);
+                           (const bf16*)a.Q, (const bf16*)a.K, (const f16*)a.vt,
+                           (const float*)a.kmax, (const float*)a.vsc, a.buckets, a.N, a.H, nqt,
+                           nkt, c, a.qflag, nqf, a.Y, a.ydt);
     } else
         hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,

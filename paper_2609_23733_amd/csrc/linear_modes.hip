@@ -2,6 +2,9 @@
 //   SURR (Section 4.3, Eq.5-7): y_i = C_h + gamma_i (.) delta_i with
 //        gamma_i = sigmoid(MLP_gamma([v_i; C_h])), delta_i = MLP_delta([v_i; C_h]);
 //   MEAN (Algorithm 1, third branch): y_i = (1/N) sum_j v_j for every token.
+// and the ablations of SURR that Section 5.3 evaluates (Tables 5-6): the
+// value mean as context, no residual correction (y_i = C_h), the identity
+// added (y_i = v_i + Eq.7) and linear attention in place of the surrogate.
 // Each kernel runs over (token block, head) and exits unless modes[h] is its
 // mode.
 //
@@ -37,8 +40,8 @@ __global__ __launch_bounds__(256) void k_surrogate_bf16(
     const bf16* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
     const bf16* __restrict__ gw1, const float* __restrict__ gb1, const bf16* __restrict__ gw2,
     const float* __restrict__ gb2, const bf16* __restrict__ dw1, const float* __restrict__ db1,
-    const bf16* __restrict__ dw2, const float* __restrict__ db2, int act, int64_t N, int H,
-    void* __restrict__ Y, int ydt) {
+    const bf16* __restrict__ dw2, const float* __restrict__ db2, int act, int add_v, int64_t N,
+    int H, void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
     const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
@@ -143,6 +146,11 @@ __global__ __launch_bounds__(256) void k_surrogate_bf16(
                         y[i] = sC[d] + gam * (D[db][4 * g + i] + sB2d[d]);
                     }
                     const int64_t off = (tok * H + h) * kD + d0;
+                    if (add_v) {   // identity added: y = v + Eq.7
+                        const bf16x4 v = *reinterpret_cast<const bf16x4*>(V + off);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) y[i] += (float)v[i];
+                    }
                     if (ydt == DT_BF16) {
                         bf16x4 v;
                         v[0] = (bf16)y[0]; v[1] = (bf16)y[1]; v[2] = (bf16)y[2]; v[3] = (bf16)y[3];
@@ -163,8 +171,8 @@ __global__ __launch_bounds__(256) void k_surrogate_f32(
     const float* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
     const float* __restrict__ gw1, const float* __restrict__ gb1, const float* __restrict__ gw2,
     const float* __restrict__ gb2, const float* __restrict__ dw1, const float* __restrict__ db1,
-    const float* __restrict__ dw2, const float* __restrict__ db2, int act, int64_t N, int H,
-    void* __restrict__ Y, int ydt) {
+    const float* __restrict__ dw2, const float* __restrict__ db2, int act, int add_v, int64_t N,
+    int H, void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
     const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
@@ -221,7 +229,7 @@ __global__ __launch_bounds__(256) void k_surrogate_f32(
         const int64_t off = (tok * H + h) * kD;
 #pragma unroll
         for (int k = 0; k < kD; ++k) {
-            const float y = sC[k] + sigmoid_fast(og[k]) * od[k];
+            const float y = sC[k] + sigmoid_fast(og[k]) * od[k] + (add_v ? v[k] : 0.f);
             if (ydt == DT_BF16)
                 reinterpret_cast<bf16*>(Y)[off + k] = (bf16)y;
             else
@@ -231,16 +239,18 @@ __global__ __launch_bounds__(256) void k_surrogate_f32(
 }
 
 // ------------------------------------------------------------------------
-// K8: MEAN heads, a write-only stream of the head's value mean.
+// K8: a write-only stream of one [d] vector per head into every row: MEAN
+// heads (the value mean) and SURR heads of the no-residual ablation (C_h).
 // 8 lanes per row (8 values each); a workgroup covers 32 rows per step.
 // ------------------------------------------------------------------------
 constexpr int kMeanRows = 1024;
 
-__global__ __launch_bounds__(256) void k_mean_heads(const uint8_t* __restrict__ modes,
-                                                    const float* __restrict__ vmean, int64_t N,
-                                                    int H, void* __restrict__ Y, int ydt) {
+__global__ __launch_bounds__(256) void k_broadcast_heads(const uint8_t* __restrict__ modes,
+                                                         int mode, const float* __restrict__ vmean,
+                                                         int64_t N, int H, void* __restrict__ Y,
+                                                         int ydt) {
     const int h = blockIdx.y;
-    if (modes[h] != MODE_MEAN) return;
+    if (modes[h] != mode) return;
     const int64_t t0 = (int64_t)blockIdx.x * kMeanRows;
     const int64_t t1 = (t0 + kMeanRows < N) ? t0 + kMeanRows : N;
     const int seg = (threadIdx.x & 7) * 8, rr = threadIdx.x >> 3;
@@ -262,23 +272,215 @@ __global__ __launch_bounds__(256) void k_mean_heads(const uint8_t* __restrict__ 
     }
 }
 
+// ------------------------------------------------------------------------
+// Linear attention in place of the surrogate (compute-mode ablation,
+// Table 6; Katharopoulos et al.), non-causal over all N tokens with
+// phi(x) = elu(x) + 1:  y_i = phi(q_i)^T S / phi(q_i) . z with
+// S = sum_j phi(k_j) v_j^T (64 x 64) and z = sum_j phi(k_j).
+// Three kernels, fp32 arithmetic throughout (HBM-bound: each of Q, K, V is
+// read once):
+//   K10a  per (token chunk, head): partial S and z of the chunk;
+//   K10b  per head: S and z summed over the chunks in chunk order;
+//   K10c  per (token block, head): y_i, one token per thread, S in LDS.
+// ------------------------------------------------------------------------
+__device__ __forceinline__ float elu1(float x) {
+    return x > 0.f ? x + 1.f : exp2f_fast(x * kLog2e);
+}
+
+// 16 consecutive values of row `row` of a [N, H, 64] tensor, as fp32.
+template <int DT>
+__device__ __forceinline__ void load16(const void* __restrict__ X, int64_t off, float* o) {
+    if (DT == DT_BF16) {
+        const bf16* p = reinterpret_cast<const bf16*>(X) + off;
+        const bf16x8 a = load_bf16x8(p), b = load_bf16x8(p + 8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            o[j] = bf16_to_f32(a[j]);
+            o[8 + j] = bf16_to_f32(b[j]);
+        }
+    } else {
+        const float4* p = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(X) + off);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const float4 v = p[j];
+            o[4 * j] = v.x; o[4 * j + 1] = v.y; o[4 * j + 2] = v.z; o[4 * j + 3] = v.w;
+        }
+    }
+}
+
+// K10a.  Thread t owns row e = t / 4 of S and its columns 16 (t % 4) ... +15;
+// 64-token tiles of phi(K) and V are staged in LDS (rows past the chunk are
+// zero, so they add nothing).
+template <int DT>
+__global__ __launch_bounds__(256) void k_linattn_partial(const void* __restrict__ K,
+                                                         const void* __restrict__ V,
+                                                         const uint8_t* __restrict__ modes,
+                                                         int64_t N, int H, int64_t chunk,
+                                                         float* __restrict__ part) {
+    const int h = blockIdx.y, c = blockIdx.x;
+    if (modes[h] != MODE_SURR) return;
+    const int64_t t0 = (int64_t)c * chunk;
+    const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
+    const int tid = threadIdx.x, e = tid >> 2, c0 = (tid & 3) * 16;
+    __shared__ __attribute__((aligned(16))) float sK[64][kD];
+    __shared__ __attribute__((aligned(16))) float sV[64][kD];
+    float acc[16], z = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+    for (int64_t tb = t0; tb < t1; tb += 64) {
+        const int64_t tok = tb + e;   // staging: token row e, values c0 ... c0+15
+        float kv[16], vv[16];
+        if (tok < t1) {
+            load16<DT>(K, (tok * H + h) * kD + c0, kv);
+            load16<DT>(V, (tok * H + h) * kD + c0, vv);
+#pragma unroll
+            for (int i = 0; i < 16; ++i) kv[i] = elu1(kv[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) kv[i] = vv[i] = 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            *reinterpret_cast<float4*>(&sK[e][c0 + 4 * i]) =
+                make_float4(kv[4 * i], kv[4 * i + 1], kv[4 * i + 2], kv[4 * i + 3]);
+            *reinterpret_cast<float4*>(&sV[e][c0 + 4 * i]) =
+                make_float4(vv[4 * i], vv[4 * i + 1], vv[4 * i + 2], vv[4 * i + 3]);
+        }
+        __syncthreads();
+#pragma unroll 4
+        for (int j = 0; j < 64; ++j) {
+            const float a = sK[j][e];
+            z += a;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 v = *reinterpret_cast<const float4*>(&sV[j][c0 + 4 * i]);
+                acc[4 * i] = fmaf(a, v.x, acc[4 * i]);
+                acc[4 * i + 1] = fmaf(a, v.y, acc[4 * i + 1]);
+                acc[4 * i + 2] = fmaf(a, v.z, acc[4 * i + 2]);
+                acc[4 * i + 3] = fmaf(a, v.w, acc[4 * i + 3]);
+            }
+        }
+        __syncthreads();
+    }
+    float* o = part + ((int64_t)h * gridDim.x + c) * kLinSums;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        *reinterpret_cast<float4*>(o + e * kD + c0 + 4 * i) =
+            make_float4(acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]);
+    if ((tid & 3) == 0) o[kD * kD + e] = z;
+}
+
+// K10b.  Grid (cdiv(kLinSums, 256), H): one sum per thread, chunks in order.
+__global__ __launch_bounds__(256) void k_linattn_combine(const uint8_t* __restrict__ modes,
+                                                         const float* __restrict__ part,
+                                                         int nchunks, float* __restrict__ sums) {
+    const int h = blockIdx.y;
+    if (modes[h] != MODE_SURR) return;
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= kLinSums) return;
+    const float* p = part + (int64_t)h * nchunks * kLinSums + i;
+    float acc = 0.f;
+    for (int c = 0; c < nchunks; ++c) acc += p[(int64_t)c * kLinSums];
+    sums[h * kLinSums + i] = acc;
+}
+
+// K10c.  One token per thread: phi(q) in registers, S and z broadcast from
+// LDS, 64 x 64 FMAs per token.
+template <int DT>
+__global__ __launch_bounds__(256) void k_linattn_apply(const void* __restrict__ Q,
+                                                       const uint8_t* __restrict__ modes,
+                                                       const float* __restrict__ sums, int64_t N,
+                                                       int H, void* __restrict__ Y, int ydt) {
+    const int h = blockIdx.y;
+    if (modes[h] != MODE_SURR) return;
+    __shared__ __attribute__((aligned(16))) float sS[kLinSums];
+    const float* src = sums + h * kLinSums;
+    for (int i = threadIdx.x; i < kLinSums; i += 256) sS[i] = src[i];
+    __syncthreads();
+    const int64_t tok = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (tok >= N) return;
+    float fq[kD], y[kD];
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4) load16<DT>(Q, (tok * H + h) * kD + 16 * s4, fq + 16 * s4);
+#pragma unroll
+    for (int k = 0; k < kD; ++k) {
+        fq[k] = elu1(fq[k]);
+        y[k] = 0.f;
+    }
+    float den = 0.f;
+#pragma unroll
+    for (int e = 0; e < kD; ++e) {
+        const float a = fq[e];
+        den = fmaf(a, sS[kD * kD + e], den);
+#pragma unroll
+        for (int k = 0; k < kD; k += 4) {
+            const float4 s = *reinterpret_cast<const float4*>(&sS[e * kD + k]);
+            y[k] = fmaf(a, s.x, y[k]);
+            y[k + 1] = fmaf(a, s.y, y[k + 1]);
+            y[k + 2] = fmaf(a, s.z, y[k + 2]);
+            y[k + 3] = fmaf(a, s.w, y[k + 3]);
+        }
+    }
+    const float inv = 1.f / den;
+    const int64_t off = (tok * H + h) * kD;
+    if (ydt == DT_BF16) {
+#pragma unroll
+        for (int k = 0; k < kD; k += 8)
+            *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + off + k) =
+                pack_bf16x8(y[k] * inv, y[k + 1] * inv, y[k + 2] * inv, y[k + 3] * inv,
+                            y[k + 4] * inv, y[k + 5] * inv, y[k + 6] * inv, y[k + 7] * inv);
+    } else {
+#pragma unroll
+        for (int k = 0; k < kD; k += 4)
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off + k) =
+                make_float4(y[k] * inv, y[k + 1] * inv, y[k + 2] * inv, y[k + 3] * inv);
+    }
+}
+
 // ------------------------------------------------------------------ launchers
 
 void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
     const unsigned nbs = (unsigned)((a.N + kSurrRows - 1) / kSurrRows);
-    if (a.dtype == DT_BF16)
-        hipLaunchKernelGGL(k_surrogate_bf16, dim3(nbs, a.H), dim3(256), 0, st, (const bf16*)a.V,
-                           a.modes, a.ctx, (const bf16*)a.g_w1, a.g_b1, (const bf16*)a.g_w2,
-                           a.g_b2, (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2,
-                           a.act, a.N, a.H, a.Y, a.ydt);
-    else
-        hipLaunchKernelGGL(k_surrogate_f32, dim3(nbs, a.H), dim3(256), 0, st, (const float*)a.V,
-                           a.modes, a.ctx, (const float*)a.g_w1, a.g_b1, (const float*)a.g_w2,
-                           a.g_b2, (const float*)a.d_w1, a.d_b1, (const float*)a.d_w2, a.d_b2,
-                           a.act, a.N, a.H, a.Y, a.ydt);
+    const int v = a.variant;
+    if (v == SURR_EQ7 || v == SURR_MEAN_CONTEXT || v == SURR_ADD_IDENTITY) {
+        const float* C = v == SURR_MEAN_CONTEXT ? a.vmean : a.ctx;
+        const int add_v = v == SURR_ADD_IDENTITY;
+        if (a.dtype == DT_BF16)
+            hipLaunchKernelGGL(k_surrogate_bf16, dim3(nbs, a.H), dim3(256), 0, st,
+                               (const bf16*)a.V, a.modes, C, (const bf16*)a.g_w1, a.g_b1,
+                               (const bf16*)a.g_w2, a.g_b2, (const bf16*)a.d_w1, a.d_b1,
+                               (const bf16*)a.d_w2, a.d_b2, a.act, add_v, a.N, a.H, a.Y, a.ydt);
+        else
+            hipLaunchKernelGGL(k_surrogate_f32, dim3(nbs, a.H), dim3(256), 0, st,
+                               (const float*)a.V, a.modes, C, (const float*)a.g_w1, a.g_b1,
+                               (const float*)a.g_w2, a.g_b2, (const float*)a.d_w1, a.d_b1,
+                               (const float*)a.d_w2, a.d_b2, a.act, add_v, a.N, a.H, a.Y, a.ydt);
+    } else if (v == SURR_NO_RESIDUAL) {
+        const unsigned nb = (unsigned)((a.N + kMeanRows - 1) / kMeanRows);
+        hipLaunchKernelGGL(k_broadcast_heads, dim3(nb, a.H), dim3(256), 0, st, a.modes,
+                           (int)MODE_SURR, a.ctx, a.N, a.H, a.Y, a.ydt);
+    } else {   // SURR_LINEAR_ATTN
+        const dim3 gp((unsigned)a.n3, a.H), gc((kLinSums + 255) / 256, a.H),
+            ga((unsigned)((a.N + 255) / 256), a.H);
+        if (a.dtype == DT_BF16) {
+            hipLaunchKernelGGL(k_linattn_partial<DT_BF16>, gp, dim3(256), 0, st, a.K, a.V,
+                               a.modes, a.N, a.H, a.chunk3, a.lpart);
+            hipLaunchKernelGGL(k_linattn_combine, gc, dim3(256), 0, st, a.modes, a.lpart,
+                               (int)a.n3, a.lsum);
+            hipLaunchKernelGGL(k_linattn_apply<DT_BF16>, ga, dim3(256), 0, st, a.Q, a.modes,
+                               a.lsum, a.N, a.H, a.Y, a.ydt);
+        } else {
+            hipLaunchKernelGGL(k_linattn_partial<DT_F32>, gp, dim3(256), 0, st, a.K, a.V,
+                               a.modes, a.N, a.H, a.chunk3, a.lpart);
+            hipLaunchKernelGGL(k_linattn_combine, gc, dim3(256), 0, st, a.modes, a.lpart,
+                               (int)a.n3, a.lsum);
+            hipLaunchKernelGGL(k_linattn_apply<DT_F32>, ga, dim3(256), 0, st, a.Q, a.modes,
+                               a.lsum, a.N, a.H, a.Y, a.ydt);
+        }
+    }
     const unsigned nbm = (unsigned)((a.N + kMeanRows - 1) / kMeanRows);
-    hipLaunchKernelGGL(k_mean_heads, dim3(nbm, a.H), dim3(256), 0, st, a.modes, a.vmean, a.N,
-                       a.H, a.Y, a.ydt);
+    hipLaunchKernelGGL(k_broadcast_heads, dim3(nbm, a.H), dim3(256), 0, st, a.modes,
+                       (int)MODE_MEAN, a.vmean, a.N, a.H, a.Y, a.ydt);
 }
 
 }  // namespace vp

@@ -25,6 +25,9 @@ __device__ __forceinline__ float tanh_times_sigmoid(float x, float y) {
 // K1: gated attention pooling, partial sums per (token chunk, head).
 // part1[c][h] = (m, l, acc[64]) with m = max_i a_i (log2 units: a * log2 e),
 // l = sum_i 2^(a_i - m), acc = sum_i 2^(a_i - m) q_i over the chunk's tokens.
+// With `mean_pool` (the mean-query ablation, Table 5) every a_i is 0, so the
+// same sums give l = token count, acc = sum_i q_i and the combine returns the
+// plain mean of the queries; W, U and w are then not read.
 // ------------------------------------------------------------------------
 
 // bf16: per head, [W_h; U_h] (128 x 64) times Q_h^T (64 x 32 tokens) on MFMA.
@@ -36,6 +39,7 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
                                                            const bf16* __restrict__ U,
                                                            const bf16* __restrict__ w,
                                                            int64_t N, int H, int64_t chunk,
+                                                           int mean_pool,
                                                            float* __restrict__ part) {
     const int h = blockIdx.y, c = blockIdx.x;
     const int64_t t0 = (int64_t)c * chunk;
@@ -44,21 +48,24 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
     const int n = lane & 31, hh = lane >> 5;
 
     bf16x8 Wop[2][4], Uop[2][4];
-    const bf16* Wh = W + (int64_t)h * kL * kD;
-    const bf16* Uh = U + (int64_t)h * kL * kD;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            Wop[mb][ks] = load_bf16x8(Wh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
-            Uop[mb][ks] = load_bf16x8(Uh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
-        }
     float wv[2][16];
+    if (!mean_pool) {
+        const bf16* Wh = W + (int64_t)h * kL * kD;
+        const bf16* Uh = U + (int64_t)h * kL * kD;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-            wv[mb][r] = bf16_to_f32(w[(int64_t)h * kL + 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+            for (int ks = 0; ks < 4; ++ks) {
+                Wop[mb][ks] = load_bf16x8(Wh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
+                Uop[mb][ks] = load_bf16x8(Uh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
+            }
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                wv[mb][r] =
+                    bf16_to_f32(w[(int64_t)h * kL + 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+    }
 
     float m = -INFINITY, l = 0.f;
     float acc[32];
@@ -76,23 +83,27 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
             B[ks] = load_bf16x8(qrow + 16 * ks + 8 * hh);
             if (!valid) B[ks] = zero_bf16x8();
         }
-        f32x16 aW[2], aU[2];
+        float a = 0.f;
+        if (!mean_pool) {
+            f32x16 aW[2], aU[2];
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            aW[mb] = zero_f32x16();
-            aU[mb] = zero_f32x16();
+            for (int mb = 0; mb < 2; ++mb) {
+                aW[mb] = zero_f32x16();
+                aU[mb] = zero_f32x16();
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                aW[mb] = mfma_bf16(Wop[mb][ks], B[ks], aW[mb]);
-                aU[mb] = mfma_bf16(Uop[mb][ks], B[ks], aU[mb]);
+                for (int ks = 0; ks < 4; ++ks) {
+                    aW[mb] = mfma_bf16(Wop[mb][ks], B[ks], aW[mb]);
+                    aU[mb] = mfma_bf16(Uop[mb][ks], B[ks], aU[mb]);
+                }
             }
+            float pa = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    pa += wv[mb][r] * tanh_times_sigmoid(aW[mb][r], aU[mb][r]);
+            a = (pa + __shfl_xor(pa, 32)) * kLog2e;
         }
-        float pa = 0.f;
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) pa += wv[mb][r] * tanh_times_sigmoid(aW[mb][r], aU[mb][r]);
-        float a = (pa + __shfl_xor(pa, 32)) * kLog2e;
         if (!valid) a = -INFINITY;
         float bm = a;
 #pragma unroll
@@ -148,17 +159,20 @@ __global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restric
                                                           const float* __restrict__ U,
                                                           const float* __restrict__ w,
                                                           int64_t N, int H, int64_t chunk,
+                                                          int mean_pool,
                                                           float* __restrict__ part) {
     const int h = blockIdx.y, c = blockIdx.x;
     const int64_t t0 = (int64_t)c * chunk;
     const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
     __shared__ float sW[kL * kD], sU[kL * kD], sw[kL];
     __shared__ float s_red[4][2 + kD];
-    for (int i = threadIdx.x; i < kL * kD; i += 256) {
-        sW[i] = W[(int64_t)h * kL * kD + i];
-        sU[i] = U[(int64_t)h * kL * kD + i];
+    if (!mean_pool) {
+        for (int i = threadIdx.x; i < kL * kD; i += 256) {
+            sW[i] = W[(int64_t)h * kL * kD + i];
+            sU[i] = U[(int64_t)h * kL * kD + i];
+        }
+        if (threadIdx.x < kL) sw[threadIdx.x] = w[(int64_t)h * kL + threadIdx.x];
     }
-    if (threadIdx.x < kL) sw[threadIdx.x] = w[(int64_t)h * kL + threadIdx.x];
     __syncthreads();
 
     float m = -INFINITY, l = 0.f;
@@ -174,7 +188,7 @@ __global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restric
             q[4 * k] = v.x; q[4 * k + 1] = v.y; q[4 * k + 2] = v.z; q[4 * k + 3] = v.w;
         }
         float a = 0.f;
-        for (int li = 0; li < kL; ++li) {
+        for (int li = 0; li < (mean_pool ? 0 : kL); ++li) {
             float x = 0.f, y = 0.f;
 #pragma unroll
             for (int k = 0; k < kD; ++k) {
@@ -446,7 +460,8 @@ __global__ __launch_bounds__(256) void k_router_logits(const float* __restrict__
 }
 
 // ------------------------------------------------------------------------
-// K4: mode per head (Eq.4 or first argmax) and the grouped head lists.
+// K4: mode per head (Eq.4 or first argmax, or their two-branch MEAN/FULL
+// forms of the compute-mode ablation, Table 6) and the grouped head lists.
 // ------------------------------------------------------------------------
 __global__ __launch_bounds__(64) void k_assign(const float* __restrict__ scores, int H, int rule,
                                                float tau_low, float tau_high,
@@ -457,17 +472,22 @@ __global__ __launch_bounds__(64) void k_assign(const float* __restrict__ scores,
     const int h = threadIdx.x;
     if (h < H) {
         int md, bad = 0;
-        if (rule == 0) {
+        if (rule == 0 || rule == 2) {   // Eq.4; rule 2: two-branch (no SURR)
             const float s = scores[h];
             bad = isnan(s);
-            md = (bad || s >= tau_high) ? MODE_FULL : (s <= tau_low ? MODE_MEAN : MODE_SURR);
-        } else {
+            md = (bad || s >= tau_high) ? MODE_FULL
+                                        : ((rule == 2 || s <= tau_low) ? MODE_MEAN : MODE_SURR);
+        } else if (rule == 1) {          // first argmax of the three logits
             const float* lg = scores + 3 * h;
             bad = isnan(lg[0]) || isnan(lg[1]) || isnan(lg[2]);
             md = 0;
             if (lg[1] > lg[md]) md = 1;
             if (lg[2] > lg[md]) md = 2;
             if (bad) md = MODE_FULL;
+        } else {                         // rule 3: MEAN vs FULL logit, MEAN on a tie
+            const float* lg = scores + 3 * h;
+            bad = isnan(lg[MODE_MEAN]) || isnan(lg[MODE_FULL]);
+            md = (bad || lg[MODE_FULL] > lg[MODE_MEAN]) ? MODE_FULL : MODE_MEAN;
         }
         s_mode[h] = md;
         s_nan[h] = bad;
@@ -499,11 +519,11 @@ void launch_router(const RouterArgs& a, hipStream_t st) {
     if (a.dtype == DT_BF16)
         hipLaunchKernelGGL(k_pool_partial_bf16, g1, dim3(256), 0, st, (const bf16*)a.Q,
                            (const bf16*)a.W, (const bf16*)a.U, (const bf16*)a.w, a.N, a.H,
-                           a.chunk1, a.part1);
+                           a.chunk1, a.mean_pool, a.part1);
     else
         hipLaunchKernelGGL(k_pool_partial_f32, g1, dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.W, (const float*)a.U, (const float*)a.w, a.N, a.H,
-                           a.chunk1, a.part1);
+                           a.chunk1, a.mean_pool, a.part1);
     hipLaunchKernelGGL(k_pool_combine, dim3(a.H), dim3(256), 0, st, a.part1, (int)a.n1,
                        a.q_pool);
     if (a.dtype == DT_BF16)

@@ -23,8 +23,9 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Layout {
     int64_t N;
-    int64_t n1, chunk1, n2, chunk2, nkt;
-    size_t off_part1, off_part2, off_vt, off_kh, off_kmax, off_qflag, off_fpart, total;
+    int64_t n1, chunk1, n2, chunk2, nkt, n3, chunk3;
+    size_t off_part1, off_part2, off_vt, off_kh, off_kmax, off_vpart, off_vsc, off_qflag,
+        off_fpart, off_lpart, off_lsum, total;
 };
 
 // Chunking of the router reductions and the workspace carve-up; a pure
@@ -45,6 +46,10 @@ bool make_layout(const vp_shape* s, Layout* L) {
     L->chunk2 = c2 < 64 ? 64 : c2;
     L->n2 = cdiv(N, L->chunk2);
     L->nkt = cdiv(N, 64);
+    // linear-attention chunks: at most 128 per head, whole 64-token tiles
+    int64_t c3 = cdiv(cdiv(N, 128), 64) * 64;
+    L->chunk3 = c3 < 256 ? 256 : c3;
+    L->n3 = cdiv(N, L->chunk3);
     size_t off = kAlign;   // first 256 bytes reserved
     L->off_part1 = off;
     off = align_up(off + (size_t)L->n1 * s->H * (2 + VP_HEAD_DIM) * sizeof(float));
@@ -56,11 +61,20 @@ bool make_layout(const vp_shape* s, Layout* L) {
     if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * 64 * 64 * 2);
     L->off_kmax = off;
     if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * L->nkt * sizeof(float));
+    L->off_vpart = off;
+    if (s->dtype == VP_BF16)
+        off = align_up(off + (size_t)s->H * vp::flash_vmax_parts(N) * sizeof(float));
+    L->off_vsc = off;
+    if (s->dtype == VP_BF16) off = align_up(off + (size_t)s->H * 2 * sizeof(float));
     L->off_qflag = off;
     if (s->dtype == VP_BF16)
         off = align_up(off + (size_t)s->H * cdiv(N, vp::flash_q_tile(VP_BF16)) * sizeof(int32_t));
     L->off_fpart = off;
     if (s->dtype == VP_BF16) off = align_up(off + vp::flash_part_bytes(N, (int)s->H));
+    L->off_lpart = off;
+    off = align_up(off + (size_t)L->n3 * s->H * vp::kLinSums * sizeof(float));
+    L->off_lsum = off;
+    off = align_up(off + (size_t)s->H * vp::kLinSums * sizeof(float));
     L->total = off;
     return true;
 }
@@ -120,7 +134,10 @@ vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, c
     if (st != VP_OK) return st;
     if (!Q || !K || !V || !rw || !out) return VP_ERR_INVALID_ARG;
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V)) return VP_ERR_INVALID_ARG;
-    if (!rw->W || !rw->U || !rw->w || !aligned16(rw->W) || !aligned16(rw->U) || !aligned16(rw->w))
+    if (rw->pool != VP_POOL_GATED && rw->pool != VP_POOL_MEAN) return VP_ERR_INVALID_ARG;
+    if (rw->pool == VP_POOL_GATED &&
+        (!rw->W || !rw->U || !rw->w || !aligned16(rw->W) || !aligned16(rw->U) ||
+         !aligned16(rw->w)))
         return VP_ERR_INVALID_ARG;
     if (rw->L != VP_HIDDEN) return VP_ERR_UNSUPPORTED;
     if (!isfinite(rw->scale) || rw->scale < 0.f) return VP_ERR_INVALID_ARG;
@@ -143,6 +160,7 @@ vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, c
     a.n2 = L.n2; a.chunk2 = L.chunk2;
     a.part2 = (float*)((char*)ws + L.off_part2);
     a.scale = rw->scale > 0.f ? rw->scale : 1.f / sqrtf((float)shape->d);
+    a.mean_pool = rw->pool == VP_POOL_MEAN ? 1 : 0;
     a.q_pool = out->q_pool; a.stats = out->stats; a.score = out->score;
     a.ctx = out->ctx; a.vmean = out->vmean;
     vp::launch_router(a, (hipStream_t)stream);
@@ -169,8 +187,10 @@ vp_status vp_assign_heads(const float* scores, int32_t H, vp_assign_rule rule, f
     if (!scores || !modes || !buckets) return VP_ERR_INVALID_ARG;
     if (H < 1) return VP_ERR_INVALID_ARG;
     if (H > VP_MAX_HEADS) return VP_ERR_UNSUPPORTED;
-    if (rule != VP_ASSIGN_THRESHOLD && rule != VP_ASSIGN_ARGMAX) return VP_ERR_INVALID_ARG;
-    if (rule == VP_ASSIGN_THRESHOLD &&
+    if (rule != VP_ASSIGN_THRESHOLD && rule != VP_ASSIGN_ARGMAX &&
+        rule != VP_ASSIGN_THRESHOLD_BINARY && rule != VP_ASSIGN_ARGMAX_BINARY)
+        return VP_ERR_INVALID_ARG;
+    if ((rule == VP_ASSIGN_THRESHOLD || rule == VP_ASSIGN_THRESHOLD_BINARY) &&
         (!isfinite(tau_low) || !isfinite(tau_high) || tau_low < 0.f || tau_low > tau_high))
         return VP_ERR_INVALID_ARG;
     if (((uintptr_t)scores & 3u) || ((uintptr_t)buckets & 3u)) return VP_ERR_INVALID_ARG;
@@ -200,6 +220,10 @@ vp_status check_linear(const vp_shape* shape, const void* V, const uint8_t* mode
     if (!state->ctx || !state->vmean || ((uintptr_t)state->ctx & 3u) ||
         ((uintptr_t)state->vmean & 3u))
         return VP_ERR_INVALID_ARG;
+    if ((int)surr->variant < VP_SURR_EQ7 || (int)surr->variant > VP_SURR_LINEAR_ATTN)
+        return VP_ERR_INVALID_ARG;
+    if (surr->variant == VP_SURR_NO_RESIDUAL || surr->variant == VP_SURR_LINEAR_ATTN)
+        return VP_OK;   // no MLP weight is read
     if (!surr->g_w1 || !surr->g_w2 || !surr->d_w1 || !surr->d_w2 || !surr->g_b1 ||
         !surr->g_b2 || !surr->d_b1 || !surr->d_b2)
         return VP_ERR_INVALID_ARG;
@@ -229,8 +253,14 @@ vp::AttnArgs attn_args(const vp_shape* shape, const Layout& L, const void* Q, co
     a.vt = ws ? (char*)ws + L.off_vt : nullptr;
     a.kh = ws ? (char*)ws + L.off_kh : nullptr;
     a.kmax = ws ? (float*)((char*)ws + L.off_kmax) : nullptr;
+    a.vpart = ws ? (float*)((char*)ws + L.off_vpart) : nullptr;
+    a.vsc = ws ? (float*)((char*)ws + L.off_vsc) : nullptr;
     a.qflag = ws ? (int32_t*)((char*)ws + L.off_qflag) : nullptr;
     a.part = ws ? (float*)((char*)ws + L.off_fpart) : nullptr;
+    a.n3 = L.n3;
+    a.chunk3 = L.chunk3;
+    a.lpart = ws ? (float*)((char*)ws + L.off_lpart) : nullptr;
+    a.lsum = ws ? (float*)((char*)ws + L.off_lsum) : nullptr;
     a.Y = Y;
     return a;
 }
@@ -241,6 +271,7 @@ void set_linear(vp::AttnArgs& a, const vp_router_state* state, const vp_surrogat
     a.g_w1 = surr->g_w1; a.g_w2 = surr->g_w2; a.d_w1 = surr->d_w1; a.d_w2 = surr->d_w2;
     a.g_b1 = surr->g_b1; a.g_b2 = surr->g_b2; a.d_b1 = surr->d_b1; a.d_b2 = surr->d_b2;
     a.act = (int)surr->act;
+    a.variant = (int)surr->variant;
 }
 
 }  // namespace
@@ -275,15 +306,22 @@ vp_status vp_full_head_attention(const vp_shape* shape, const void* Q, const voi
     return hip_status("vp_full_head_attention");
 }
 
-vp_status vp_linear_heads(const vp_shape* shape, const void* V, const uint8_t* modes,
-                          const vp_router_state* state, const vp_surrogate_weights* surr,
-                          void* Y, vp_dtype y_dtype, void* stream) {
+vp_status vp_linear_heads(const vp_shape* shape, const void* Q, const void* K, const void* V,
+                          const uint8_t* modes, const vp_router_state* state,
+                          const vp_surrogate_weights* surr, void* Y, vp_dtype y_dtype, void* ws,
+                          size_t ws_bytes, void* stream) {
     vp_status st = check_linear(shape, V, modes, state, surr, Y, y_dtype);
     if (st != VP_OK) return st;
     Layout L;
-    make_layout(shape, &L);
+    if (surr->variant == VP_SURR_LINEAR_ATTN) {
+        if (!Q || !K || !aligned16(Q) || !aligned16(K)) return VP_ERR_INVALID_ARG;
+        if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+    } else {
+        make_layout(shape, &L);
+        ws = nullptr;   // not read
+    }
     (void)hipGetLastError();
-    vp::AttnArgs a = attn_args(shape, L, nullptr, nullptr, V, modes, nullptr, Y, y_dtype, nullptr);
+    vp::AttnArgs a = attn_args(shape, L, Q, K, V, modes, nullptr, Y, y_dtype, ws);
     set_linear(a, state, surr);
     vp::launch_linear_heads(a, (hipStream_t)stream);
     return hip_status("vp_linear_heads");

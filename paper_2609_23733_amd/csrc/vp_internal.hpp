@@ -17,6 +17,7 @@ struct RouterArgs {
     int64_t n2, chunk2;   // routing chunks
     float* part2;
     float scale;
+    int mean_pool;        // 1: q_pool = mean of the queries (W, U, w unused)
     float *q_pool, *stats, *score, *ctx, *vmean;
 };
 
@@ -27,7 +28,9 @@ struct AttnArgs {
     const int32_t* buckets;
     int64_t N;
     int H;
-    void* vt;      // packed V^T tiles of FULL heads (bf16 only)
+    void* vt;      // packed V^T tiles of FULL heads, fp16, scaled (bf16 only)
+    float* vpart;  // per (FULL slot, group of key tiles): max |v| (bf16 only)
+    float* vsc;    // per FULL slot: (2^-e, 2^e), the scale of its packed V (bf16 only)
     void* kh;      // packed K tiles of FULL heads, fp16 (bf16 only)
     float* kmax;   // per (FULL slot, 64-key tile): max key norm (bf16 only)
     int32_t* qflag;  // per FULL-head work item: needs the running reference point (bf16 only)
@@ -37,7 +40,17 @@ struct AttnArgs {
     const void *g_w1, *g_w2, *d_w1, *d_w2;
     const float *g_b1, *g_b2, *d_b1, *d_b2;
     int act;
+    int variant;          // how SURR heads are computed (vp_surr_variant)
+    int64_t n3, chunk3;   // linear-attention token chunks
+    float* lpart;         // linear-attention partial sums [H][n3][kLinSums]
+    float* lsum;          // linear-attention sums [H][kLinSums]
 };
+
+// Per head: the 64 x 64 sum of phi(k) v^T followed by the 64 sums of phi(k).
+constexpr int kLinSums = 64 * 64 + 64;
+// Surrogate variants (values of vp_surr_variant).
+enum { SURR_EQ7 = 0, SURR_MEAN_CONTEXT = 1, SURR_NO_RESIDUAL = 2, SURR_ADD_IDENTITY = 3,
+       SURR_LINEAR_ATTN = 4 };
 
 void launch_router(const RouterArgs& a, hipStream_t st);
 void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,
@@ -50,5 +63,6 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st);
 int flash_q_tile(int dtype);
 int flash_stream_groups(int64_t N, int H);
 size_t flash_part_bytes(int64_t N, int H);
+int64_t flash_vmax_parts(int64_t N);
 
 }  // namespace vp

@@ -20,7 +20,9 @@ LIB_PATH = os.path.join(HERE, "libvggtprime.so")
 VP_OK, VP_ERR_INVALID_ARG, VP_ERR_UNSUPPORTED, VP_ERR_WORKSPACE, VP_ERR_HIP = range(5)
 VP_F32, VP_BF16 = 0, 1
 MODE_MEAN, MODE_SURR, MODE_FULL = 0, 1, 2
-RULE_THRESHOLD, RULE_ARGMAX = 0, 1
+RULE_THRESHOLD, RULE_ARGMAX, RULE_THRESHOLD_BINARY, RULE_ARGMAX_BINARY = 0, 1, 2, 3
+POOL_GATED, POOL_MEAN = 0, 1
+SURR_EQ7, SURR_MEAN_CONTEXT, SURR_NO_RESIDUAL, SURR_ADD_IDENTITY, SURR_LINEAR_ATTN = range(5)
 ACT_GELU_ERF, ACT_RELU = 0, 1
 MAX_HEADS, HEAD_DIM, HIDDEN = 16, 64, 64
 BUCKETS_LEN = 3 + MAX_HEADS + 1
@@ -38,7 +40,7 @@ class vp_shape(ctypes.Structure):
 
 class vp_router_weights(ctypes.Structure):
     _fields_ = [("W", ctypes.c_void_p), ("U", ctypes.c_void_p), ("w", ctypes.c_void_p),
-                ("L", ctypes.c_int32), ("scale", ctypes.c_float)]
+                ("L", ctypes.c_int32), ("scale", ctypes.c_float), ("pool", ctypes.c_int)]
 
 
 class vp_router_state(ctypes.Structure):
@@ -50,7 +52,7 @@ class vp_surrogate_weights(ctypes.Structure):
     _fields_ = [("g_w1", ctypes.c_void_p), ("g_w2", ctypes.c_void_p), ("d_w1", ctypes.c_void_p),
                 ("d_w2", ctypes.c_void_p), ("g_b1", ctypes.c_void_p), ("g_b2", ctypes.c_void_p),
                 ("d_b1", ctypes.c_void_p), ("d_b2", ctypes.c_void_p), ("L", ctypes.c_int32),
-                ("act", ctypes.c_int)]
+                ("act", ctypes.c_int), ("variant", ctypes.c_int)]
 
 
 _lib = None
@@ -81,9 +83,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                          P]
     lib.vp_full_head_attention.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P, ctypes.c_int,
                                            P, ctypes.c_size_t, P]
-    lib.vp_linear_heads.argtypes = [ctypes.POINTER(vp_shape), P, P,
+    lib.vp_linear_heads.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P,
                                     ctypes.POINTER(vp_router_state),
-                                    ctypes.POINTER(vp_surrogate_weights), P, ctypes.c_int, P]
+                                    ctypes.POINTER(vp_surrogate_weights), P, ctypes.c_int, P,
+                                    ctypes.c_size_t, P]
     for f in ("vp_router_score", "vp_router_logits", "vp_assign_heads",
               "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
               "vp_linear_heads"):
@@ -176,18 +179,21 @@ class RouterState:
 
 
 def router_score(Q, K, V, W, U, w, S: int, P: int, ws: torch.Tensor, scale: float = 0.0,
-                 out: Optional[RouterState] = None) -> RouterState:
-    """Router (Eq.1-3) plus context and value mean: see vp_router_score."""
+                 out: Optional[RouterState] = None, pool: int = POOL_GATED) -> RouterState:
+    """Router (Eq.1-3) plus context and value mean: see vp_router_score.
+    ``pool=POOL_MEAN`` pools by the plain query mean (W, U, w may be None)."""
     N, H = S * P, Q.shape[1]
     for t, nm in ((Q, "Q"), (K, "K"), (V, "V")):
         _need(t, nm, (N, H, HEAD_DIM), Q.dtype)
-    _need(W, "W", (H, HIDDEN, HEAD_DIM), Q.dtype)
-    _need(U, "U", (H, HIDDEN, HEAD_DIM), Q.dtype)
-    _need(w, "w", (H, HIDDEN), Q.dtype)
+    if pool == POOL_GATED:
+        _need(W, "W", (H, HIDDEN, HEAD_DIM), Q.dtype)
+        _need(U, "U", (H, HIDDEN, HEAD_DIM), Q.dtype)
+        _need(w, "w", (H, HIDDEN), Q.dtype)
     _need(ws, "ws")
     if out is None:
         out = RouterState.empty(H, Q.device)
-    rw = vp_router_weights(W.data_ptr(), U.data_ptr(), w.data_ptr(), HIDDEN, float(scale))
+    ptr = lambda t: None if t is None else t.data_ptr()
+    rw = vp_router_weights(ptr(W), ptr(U), ptr(w), HIDDEN, float(scale), int(pool))
     shp = make_shape(S, P, H, Q.dtype)
     st = out.c()
     _check(load_library().vp_router_score(ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V),
@@ -229,7 +235,12 @@ def assign_heads(scores, rule: int, tau_low: float = TAU_LOW, tau_high: float = 
     return modes, buckets
 
 
-def _surr_struct(surr, H, dtype, act):
+_SURR_KEYS = ("g_w1", "g_w2", "d_w1", "d_w2", "g_b1", "g_b2", "d_b1", "d_b2")
+
+
+def _surr_struct(surr, H, dtype, act, variant=SURR_EQ7):
+    if variant in (SURR_NO_RESIDUAL, SURR_LINEAR_ATTN):   # no MLP weight is read
+        return vp_surrogate_weights(*([None] * 8), HIDDEN, int(act), int(variant))
     for k in ("g_w1", "d_w1"):
         _need(surr[k], k, (H, HIDDEN, 2 * HEAD_DIM), dtype)
     for k in ("g_w2", "d_w2"):
@@ -238,9 +249,8 @@ def _surr_struct(surr, H, dtype, act):
         _need(surr[k], k, (H, HIDDEN), torch.float32)
     for k in ("g_b2", "d_b2"):
         _need(surr[k], k, (H, HEAD_DIM), torch.float32)
-    return vp_surrogate_weights(*(surr[k].data_ptr() for k in
-                                  ("g_w1", "g_w2", "d_w1", "d_w2", "g_b1", "g_b2", "d_b1",
-                                   "d_b2")), HIDDEN, int(act))
+    return vp_surrogate_weights(*(surr[k].data_ptr() for k in _SURR_KEYS), HIDDEN, int(act),
+                                int(variant))
 
 
 def _qkv(Q, K, V, S, P):
@@ -253,7 +263,8 @@ def _qkv(Q, K, V, S, P):
 def routed_global_attention(Q, K, V, modes, buckets, state: RouterState,
                             surr: Dict[str, torch.Tensor], S: int, P: int, ws: torch.Tensor,
                             y_dtype=None, act: int = ACT_GELU_ERF,
-                            Y: Optional[torch.Tensor] = None) -> torch.Tensor:
+                            Y: Optional[torch.Tensor] = None,
+                            surr_variant: int = SURR_EQ7) -> torch.Tensor:
     """Routed global attention (Algorithm 1 step 2): Y [N, H, d]."""
     N, H = _qkv(Q, K, V, S, P)
     _need(modes, "modes", (H,), torch.uint8)
@@ -263,7 +274,7 @@ def routed_global_attention(Q, K, V, modes, buckets, state: RouterState,
     if Y is None:
         Y = torch.empty(N, H, HEAD_DIM, dtype=y_dtype, device=Q.device)
     _need(Y, "Y", (N, H, HEAD_DIM), y_dtype)
-    sw = _surr_struct(surr, H, Q.dtype, act)
+    sw = _surr_struct(surr, H, Q.dtype, act, surr_variant)
     shp = make_shape(S, P, H, Q.dtype)
     st = state.c()
     _check(load_library().vp_routed_global_attention(
@@ -298,18 +309,25 @@ def full_head_attention(Q, K, V, buckets, S: int, P: int, ws: torch.Tensor, Y: t
 
 
 def linear_heads(V, modes, state: RouterState, surr, S: int, P: int, Y: torch.Tensor,
-                 act: int = ACT_GELU_ERF):
-    """Stage 3: SURR and MEAN heads into Y."""
+                 act: int = ACT_GELU_ERF, surr_variant: int = SURR_EQ7, Q=None, K=None,
+                 ws: Optional[torch.Tensor] = None):
+    """Stage 3: SURR and MEAN heads into Y (Q, K and ws: linear attention only)."""
     N, H = S * P, V.shape[1]
     _need(V, "V", (N, H, HEAD_DIM))
     _need(modes, "modes", (H,), torch.uint8)
     _need(Y, "Y", (N, H, HEAD_DIM))
-    sw = _surr_struct(surr, H, V.dtype, act)
+    if surr_variant == SURR_LINEAR_ATTN:
+        _need(Q, "Q", (N, H, HEAD_DIM), V.dtype)
+        _need(K, "K", (N, H, HEAD_DIM), V.dtype)
+        _need(ws, "ws")
+    sw = _surr_struct(surr, H, V.dtype, act, surr_variant)
     shp = make_shape(S, P, H, V.dtype)
     st = state.c()
-    _check(load_library().vp_linear_heads(ctypes.byref(shp), _ptr(V), _ptr(modes),
-                                          ctypes.byref(st), ctypes.byref(sw), _ptr(Y), _dt(Y),
-                                          _stream()), "vp_linear_heads")
+    nws = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(load_library().vp_linear_heads(ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V),
+                                          _ptr(modes), ctypes.byref(st), ctypes.byref(sw),
+                                          _ptr(Y), _dt(Y), _ptr(ws), nws, _stream()),
+           "vp_linear_heads")
 
 
 class RoutedLayer:
@@ -318,11 +336,13 @@ class RoutedLayer:
     (router_score, [router_logits], assign_heads, routed_global_attention)."""
 
     def __init__(self, inp, rule: int = RULE_ARGMAX, y_dtype=None, act: int = ACT_GELU_ERF,
-                 tau_low: float = TAU_LOW, tau_high: float = TAU_HIGH, device="cuda"):
+                 tau_low: float = TAU_LOW, tau_high: float = TAU_HIGH, device="cuda",
+                 pool: int = POOL_GATED, surr_variant: int = SURR_EQ7):
         x = inp.to(device)
         self.x = x
         self.S, self.P, self.H = x.S, x.P, x.H
         self.rule, self.act = rule, act
+        self.pool, self.surr_variant = pool, surr_variant
         self.tau_low, self.tau_high = tau_low, tau_high
         self.y_dtype = y_dtype if y_dtype is not None else x.Q.dtype
         self.ws = alloc_workspace(x.S, x.P, x.H, x.Q.dtype, device)
@@ -339,8 +359,9 @@ class RoutedLayer:
         Q = x.Q if Q is None else Q
         K = x.K if K is None else K
         V = x.V if V is None else V
-        router_score(Q, K, V, x.W, x.U, x.w, self.S, self.P, self.ws, out=self.state)
-        if self.rule == RULE_ARGMAX:
+        router_score(Q, K, V, x.W, x.U, x.w, self.S, self.P, self.ws, out=self.state,
+                     pool=self.pool)
+        if self.rule in (RULE_ARGMAX, RULE_ARGMAX_BINARY):
             router_logits(x.u, x.Wr, x.br, out=self.logits)
             scores = self.logits
         else:
@@ -348,12 +369,14 @@ class RoutedLayer:
         assign_heads(scores, self.rule, self.tau_low, self.tau_high, self.modes, self.buckets)
         if events is None:
             routed_global_attention(Q, K, V, self.modes, self.buckets, self.state, x.surr,
-                                    self.S, self.P, self.ws, self.y_dtype, self.act, self.Y)
+                                    self.S, self.P, self.ws, self.y_dtype, self.act, self.Y,
+                                    self.surr_variant)
         else:
             # the same three stages, with events bracketing the FULL-head kernel
             gather_full_heads(K, V, self.buckets, self.S, self.P, self.ws)
             events[0].record()
             full_head_attention(Q, K, V, self.buckets, self.S, self.P, self.ws, self.Y)
             events[1].record()
-            linear_heads(V, self.modes, self.state, x.surr, self.S, self.P, self.Y, self.act)
+            linear_heads(V, self.modes, self.state, x.surr, self.S, self.P, self.Y, self.act,
+                         self.surr_variant, Q, K, self.ws)
         return self.Y

@@ -57,8 +57,8 @@ def test_workspace_bytes(lib):
     assert f(shape(dt=vp.VP_BF16)) > f(shape(dt=vp.VP_F32))
 
 
-def rw(L=64, W=FAKE, scale=0.0):
-    return vp.vp_router_weights(W, FAKE, FAKE, L, scale)
+def rw(L=64, W=FAKE, scale=0.0, pool=vp.POOL_GATED):
+    return vp.vp_router_weights(W, FAKE, FAKE, L, scale, pool)
 
 
 def rs(q=FAKE):
@@ -91,6 +91,14 @@ def test_router_score_validation(lib):
     assert call_score(lib, ws_bytes=1024) == vp.VP_ERR_WORKSPACE
     assert lib.vp_router_score(None, FAKE, FAKE, FAKE, None, None, FAKE, 1 << 40, None) == \
         vp.VP_ERR_INVALID_ARG
+    # pooling mode: unknown values are rejected; the mean query reads no W, U, w
+    # (a NULL W then passes validation and the next check, the workspace, fails)
+    assert call_score(lib, w=rw(pool=2)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, w=rw(pool=-1)) == vp.VP_ERR_INVALID_ARG
+    assert call_score(lib, w=rw(W=None, pool=vp.POOL_MEAN), ws_bytes=1024) == \
+        vp.VP_ERR_WORKSPACE
+    assert call_score(lib, w=rw(W=None, pool=vp.POOL_GATED), ws_bytes=1024) == \
+        vp.VP_ERR_INVALID_ARG
 
 
 def test_router_logits_validation(lib):
@@ -112,15 +120,22 @@ def test_assign_validation(lib):
     assert f(FAKE, 16, 0, 0.01, 0.2, FAKE, None, None) == vp.VP_ERR_INVALID_ARG
     assert f(FAKE, 0, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
     assert f(FAKE, 17, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_UNSUPPORTED
-    assert f(FAKE, 16, 2, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 4, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, -1, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
     assert f(FAKE, 16, 0, 0.3, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    # the binary threshold rule checks its thresholds like Eq.4 does
+    assert f(FAKE, 16, vp.RULE_THRESHOLD_BINARY, 0.3, 0.2, FAKE, FAKE, None) == \
+        vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, vp.RULE_THRESHOLD_BINARY, 0.01, float("inf"), FAKE, FAKE, None) == \
+        vp.VP_ERR_INVALID_ARG
     assert f(FAKE, 16, 0, -0.1, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
     assert f(FAKE, 16, 0, float("nan"), 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
     assert f(FAKE + 2, 16, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
 
 
-def sw(L=64, act=0, g_w1=FAKE):
-    return vp.vp_surrogate_weights(g_w1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, L, act)
+def sw(L=64, act=0, g_w1=FAKE, variant=vp.SURR_EQ7):
+    return vp.vp_surrogate_weights(g_w1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, L, act,
+                                   variant)
 
 
 def call_attn(lib, shp=None, Q=FAKE, modes=FAKE, st=None, s=None, Y=FAKE, ydt=vp.VP_BF16,
@@ -148,6 +163,34 @@ def test_routed_attention_validation(lib):
     assert lib.vp_routed_global_attention(ctypes.byref(shape()), FAKE, FAKE, FAKE, FAKE, FAKE,
                                           None, ctypes.byref(sw()), FAKE, 1, FAKE, 1 << 40,
                                           None) == vp.VP_ERR_INVALID_ARG
+    # surrogate variants: unknown values are rejected; the weight-free ablations
+    # accept NULL weights (the workspace check fails next), the others do not
+    assert call_attn(lib, s=sw(variant=5)) == vp.VP_ERR_INVALID_ARG
+    assert call_attn(lib, s=sw(variant=-1)) == vp.VP_ERR_INVALID_ARG
+    for v in (vp.SURR_NO_RESIDUAL, vp.SURR_LINEAR_ATTN):
+        assert call_attn(lib, s=sw(g_w1=None, variant=v), ws_bytes=10) == vp.VP_ERR_WORKSPACE
+    for v in (vp.SURR_EQ7, vp.SURR_MEAN_CONTEXT, vp.SURR_ADD_IDENTITY):
+        assert call_attn(lib, s=sw(g_w1=None, variant=v), ws_bytes=10) == vp.VP_ERR_INVALID_ARG
+
+
+def call_linear(lib, Q=FAKE, s=None, ws=FAKE, ws_bytes=1 << 40):
+    s = s or sw()
+    return lib.vp_linear_heads(ctypes.byref(shape()), Q, FAKE, FAKE, FAKE, ctypes.byref(rs()),
+                               ctypes.byref(s), FAKE, vp.VP_BF16, ws, ws_bytes, None)
+
+
+def test_linear_heads_validation(lib):
+    lin = sw(variant=vp.SURR_LINEAR_ATTN)
+    # linear attention reads Q and K and keeps its sums in the workspace
+    assert call_linear(lib, Q=None, s=lin) == vp.VP_ERR_INVALID_ARG
+    assert call_linear(lib, Q=FAKE_ODD, s=lin) == vp.VP_ERR_INVALID_ARG
+    assert call_linear(lib, ws=None, s=lin) == vp.VP_ERR_INVALID_ARG
+    assert call_linear(lib, ws_bytes=10, s=lin) == vp.VP_ERR_WORKSPACE
+    assert call_linear(lib, s=sw(variant=9)) == vp.VP_ERR_INVALID_ARG
+    assert call_linear(lib, s=sw(act=3)) == vp.VP_ERR_INVALID_ARG
+    assert lib.vp_linear_heads(ctypes.byref(shape()), FAKE, FAKE, FAKE, FAKE, None,
+                               ctypes.byref(sw()), FAKE, vp.VP_BF16, FAKE, 1 << 40, None) == \
+        vp.VP_ERR_INVALID_ARG
 
 
 def test_binding_rejects_cpu_tensors():

@@ -6,10 +6,12 @@ the oracle on the same seeded inputs, then compares:
   - modes and buckets: bit-exact (inputs are generated with logit margins
     >= 1e-3, or planted saliencies >= 1e-3 away from the thresholds);
   - router outputs q_pool, s, C, mean: max |diff| <= 1e-4 * RMS;
-  - Y per head h: max |Y - Y_oracle| <= tol * RMS(Y_oracle[:, h]) with
-    tol = 1e-4 for fp32 operands and 2e-2 for bf16 operands; when Y is
-    stored as bf16 the bound adds the half-ulp of round-to-nearest-even,
-    2^-8 |Y_oracle|, elementwise.
+  - Y: max |Y - Y_oracle| <= tol * RMS with tol = 1e-4 for fp32 operands and
+    2e-2 for bf16 operands (the stated bounds), where RMS is the smaller of
+    the head's own RMS and the RMS of the compared layer output over all
+    heads, so that the check holds under either reading of "output RMS".
+    When Y is stored as bf16 the bound adds the half-ulp of
+    round-to-nearest-even, 2^-8 |Y_oracle|, elementwise.
 """
 import math
 import sys
@@ -39,9 +41,11 @@ def _gpu():
     vp.load_library()
 
 
-def run_gpu(x, rule=oracle.RULE_ARGMAX, y_dtype=None, act=0):
+def run_gpu(x, rule=oracle.RULE_ARGMAX, y_dtype=None, act=0, pool=oracle.POOL_GATED,
+            surr_variant=oracle.SURR_EQ7):
     from paper_2609_23733_amd import vp
-    layer = vp.RoutedLayer(x, rule=rule, y_dtype=y_dtype, act=act)
+    layer = vp.RoutedLayer(x, rule=rule, y_dtype=y_dtype, act=act, pool=pool,
+                           surr_variant=surr_variant)
     layer.step()
     torch.cuda.synchronize()
     return layer
@@ -61,7 +65,7 @@ def check_router(layer, ref, rule):
             assert err <= 1e-4 * max(rms(r[h]), 1e-30), (name, h, err, rms(r[h]))
     s = st.score.cpu().numpy().astype(np.float64)
     np.testing.assert_allclose(s, ref["s"], rtol=1e-4)
-    if rule == oracle.RULE_ARGMAX and ref["logits"] is not None:
+    if rule in (oracle.RULE_ARGMAX, oracle.RULE_ARGMAX_BINARY) and ref["logits"] is not None:
         lg = layer.logits.cpu().numpy().astype(np.float64)
         assert np.abs(lg - ref["logits"]).max() <= 1e-5
     modes = layer.modes.cpu().numpy()
@@ -77,21 +81,26 @@ def check_y(Yg, Yo, dtype, y_bf16, heads=None, label=""):
     """Yg: GPU rows [R, H, d] (float64); Yo: oracle rows [R, H, d]."""
     tol = TOL[dtype]
     H = Yo.shape[1]
+    heads = list(range(H) if heads is None else heads)
+    layer_rms = rms(Yo[:, heads, :])
     worst = 0.0
-    for h in (range(H) if heads is None else heads):
+    for h in heads:
         r = Yo[:, h, :]
-        bound = tol * rms(r) + (2.0 ** -8 * np.abs(r) if y_bf16 else 0.0)
+        half_ulp = 2.0 ** -8 * np.abs(r) if y_bf16 else 0.0
+        bound = tol * min(rms(r), layer_rms) + half_ulp
         err = np.abs(Yg[:, h, :] - r)
         ratio = float((err / np.maximum(bound, 1e-300)).max())
         worst = max(worst, ratio)
-        assert (err <= bound).all(), "%s head %d: max err %.3e, rms %.3e, ratio %.3f" % (
-            label, h, err.max(), rms(r), ratio)
+        assert (err <= bound).all(), "%s head %d: max err %.3e, rms %.3e (layer %.3e), " \
+            "ratio %.3f" % (label, h, err.max(), rms(r), layer_rms, ratio)
     log("%s worst err/bound = %.3f" % (label, worst))
 
 
-def oracle_layer(x, rule=oracle.RULE_ARGMAX, rows=None, full_rows_sel=None, act=0):
+def oracle_layer(x, rule=oracle.RULE_ARGMAX, rows=None, full_rows_sel=None, act=0,
+                 pool=oracle.POOL_GATED, surr_variant=oracle.SURR_EQ7):
     return oracle.routed_layer(x.Q, x.K, x.V, x.W, x.U, x.w, x.surr, u=x.u, Wr=x.Wr, br=x.br,
-                               rule=rule, rows=rows, full_rows_sel=full_rows_sel, act=act)
+                               rule=rule, rows=rows, full_rows_sel=full_rows_sel, act=act,
+                               pool=pool, surr_variant=surr_variant)
 
 
 # ------------------------------------------------------------- small layers
@@ -293,18 +302,20 @@ FULL8 = np.array([2, 2, 1, 0, 2, 2, 1, 0, 2, 2, 1, 0, 2, 2, 1, 0], np.uint8)
 
 
 def test_reference_point_mixed_launch():
-    """Query tiles whose logits are provably small (reference point 0) and
-    tiles that need the running reference point, in one launch: queries
-    256..511 and one query of tile 4 are scaled by 8 (exact in bf16)."""
+    """Query tiles whose logits are provably small (reference point 0: bound
+    at most 14 in log2 units) and tiles that need the running reference point,
+    in one launch: sharp queries halved, then queries 256..511 and one query of
+    tile 4 scaled by 16 (both exact in bf16)."""
     log("reference point: mixed tiles")
     x = synth.make_layer(1, 1500, dtype="bf16", key=(9, 0), sharp=True, modes=FULL8,
                          qkv_device="cuda")
-    x.Q[256:512] *= 8
-    x.Q[1100] *= 8
+    x.Q *= 0.5
+    x.Q[256:512] *= 16
+    x.Q[1100] *= 16
     b = tile_bounds(x)
     big = np.zeros(b.shape[0], bool)
     big[[1, 4]] = True
-    assert (b[big] > 48).all() and (b[~big] < 24).all(), b
+    assert (b[big] > 48).all() and (b[~big] < 13).all(), b
     layer = run_gpu(x, y_dtype=torch.float32)
     ref = oracle_layer(x)
     check_router(layer, ref, oracle.RULE_ARGMAX)
