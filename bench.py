@@ -22,6 +22,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "routed global-attn layer latency (ms) + TFLOP/s & % bf16 MFMA peak vs S"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0
 P_TOKENS = 1374
 HEADS, D, L = 16, 64, 64
@@ -109,6 +110,67 @@ def run_workload(S, n_full, steps, warmup, seed_key):
     return rec, layer, x
 
 
+# Ablation variants of the layer (Section 5.3, Tables 5-6), timed on the
+# headline inputs: (name, assignment rule, pooling, SURR-head variant).
+VARIANTS = (
+    ("eq7", 1, 0, 0),
+    ("binary_argmax", 3, 0, 0),
+    ("mean_query", 1, 1, 0),
+    ("mean_context", 1, 0, 1),
+    ("no_residual", 1, 0, 2),
+    ("add_identity", 1, 0, 3),
+    ("linear_attention", 1, 0, 4),
+)
+
+
+def linattn_flops(N, n_surr):
+    """Linear attention per (token, SURR head): sum phi(k) v^T and sum phi(k)
+    (2 d^2 + d), then phi(q)^T S and phi(q) . z (2 d^2 + 2 d)."""
+    return float(N) * n_surr * (4 * D * D + 3 * D)
+
+
+def run_variants(x, steps, warmup):
+    """Layer latency per variant, and the SURR/MEAN stage (vp_linear_heads)
+    alone, timed with HIP events over `steps` launches."""
+    import torch
+    from paper_2609_23733_amd import vp
+    out = []
+    for name, rule, pool, sv in VARIANTS:
+        layer = vp.RoutedLayer(x, rule=rule, y_dtype=torch.bfloat16, pool=pool, surr_variant=sv)
+        ms_step, full_avg, _ = measure(layer, steps, warmup)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        xd = layer.x   # the layer's device copy of the inputs
+        lin = lambda: vp.linear_heads(xd.V, layer.modes, layer.state, xd.surr, xd.S, xd.P,
+                                      layer.Y, layer.act, sv, xd.Q, xd.K, layer.ws)
+        for _ in range(warmup):
+            lin()
+        torch.cuda.synchronize()
+        t0.record()
+        for _ in range(steps):
+            lin()
+        t1.record()
+        torch.cuda.synchronize()
+        lin_ms = t0.elapsed_time(t1) / steps
+        modes = layer.modes.cpu().numpy()
+        counts = [int((modes == m).sum()) for m in range(3)]
+        rec = dict(variant=name, ms=round(ms_step, 4), full_kernel_ms=round(full_avg, 4),
+                   linear_stage_ms=round(lin_ms, 4), n_full=counts[2], n_surr=counts[1],
+                   n_mean=counts[0])
+        if sv == 4 and counts[1]:
+            fl = linattn_flops(x.N, counts[1])
+            ach = fl / lin_ms / 1e9
+            rec["roofline"] = {"kernel": "k_linattn_partial + k_linattn_combine + "
+                                         "k_linattn_apply (+ MEAN broadcast)",
+                               "bound": "alu", "achieved": round(ach, 2),
+                               "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                               "frac": round(ach / PEAK_FP32_TFLOPS, 4),
+                               "algorithmic_flop_per_launch": fl}
+        out.append(rec)
+        del layer
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(x, rows_per_head=640):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
@@ -150,6 +212,7 @@ def main():
     ap.add_argument("--n-full", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the "
                          "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -174,6 +237,9 @@ def main():
 
     head, layer, x = run_workload(100, args.n_full, args.steps, args.warmup, (100, 0))
     by = [head]
+    variants = None
+    if not args.no_variants:
+        variants = run_variants(x, args.steps, args.warmup)
     if not args.no_sweep:
         del layer
         for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16), (500, 4)):
@@ -219,6 +285,8 @@ def main():
                      "avg_launch_ms": round(head["full_kernel_ms"], 4)},
         "by_workload": by,
     }
+    if variants is not None:
+        out["variants"] = variants
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x)
     print(json.dumps(out))

@@ -277,40 +277,56 @@ __global__ __launch_bounds__(256) void k_broadcast_heads(const uint8_t* __restri
 // Table 6; Katharopoulos et al.), non-causal over all N tokens with
 // phi(x) = elu(x) + 1:  y_i = phi(q_i)^T S / phi(q_i) . z with
 // S = sum_j phi(k_j) v_j^T (64 x 64) and z = sum_j phi(k_j).
-// Three kernels, fp32 arithmetic throughout (HBM-bound: each of Q, K, V is
-// read once):
+// Both contractions run on the fp32 MFMA (32x32x2: exact fp32 products,
+// operands taken straight from the row-major [N, H, 64] rows), sums in fp32:
 //   K10a  per (token chunk, head): partial S and z of the chunk;
 //   K10b  per head: S and z summed over the chunks in chunk order;
-//   K10c  per (token block, head): y_i, one token per thread, S in LDS.
+//   K10c  per (32-query block, head): y_i.
 // ------------------------------------------------------------------------
 __device__ __forceinline__ float elu1(float x) {
     return x > 0.f ? x + 1.f : exp2f_fast(x * kLog2e);
 }
 
-// 16 consecutive values of row `row` of a [N, H, 64] tensor, as fp32.
+// Elements 2c and 2c + 1 of the 64-value row starting at element `off`.
 template <int DT>
-__device__ __forceinline__ void load16(const void* __restrict__ X, int64_t off, float* o) {
+__device__ __forceinline__ float2 load_pair(const void* __restrict__ X, int64_t off, int c) {
+    if (DT == DT_BF16) {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(
+            reinterpret_cast<const bf16*>(X) + off + 2 * c);
+        const bf16x2 v = __builtin_bit_cast(bf16x2, w);
+        return make_float2(bf16_to_f32(v[0]), bf16_to_f32(v[1]));
+    }
+    return *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(X) + off + 2 * c);
+}
+
+// 32 consecutive values of a row, as fp32.
+template <int DT>
+__device__ __forceinline__ void load32(const void* __restrict__ X, int64_t off, float* o) {
     if (DT == DT_BF16) {
         const bf16* p = reinterpret_cast<const bf16*>(X) + off;
-        const bf16x8 a = load_bf16x8(p), b = load_bf16x8(p + 8);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            o[j] = bf16_to_f32(a[j]);
-            o[8 + j] = bf16_to_f32(b[j]);
+        for (int k = 0; k < 4; ++k) {
+            const bf16x8 v = load_bf16x8(p + 8 * k);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) o[8 * k + j] = bf16_to_f32(v[j]);
         }
     } else {
         const float4* p = reinterpret_cast<const float4*>(reinterpret_cast<const float*>(X) + off);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const float4 v = p[j];
-            o[4 * j] = v.x; o[4 * j + 1] = v.y; o[4 * j + 2] = v.z; o[4 * j + 3] = v.w;
+        for (int k = 0; k < 8; ++k) {
+            const float4 v = p[k];
+            o[4 * k] = v.x; o[4 * k + 1] = v.y; o[4 * k + 2] = v.z; o[4 * k + 3] = v.w;
         }
     }
 }
 
-// K10a.  Thread t owns row e = t / 4 of S and its columns 16 (t % 4) ... +15;
-// 64-token tiles of phi(K) and V are staged in LDS (rows past the chunk are
-// zero, so they add nothing).
+// K10a.  S^T blocks on MFMA with the token pair as the reduction index:
+// A[m][k] = phi(k_{t+k})[2m + mb], B[k][n] = v_{t+k}[2n + nb], so that a lane
+// reads one 4-byte pair per row and 32 lanes one whole 128-byte row.  Block
+// (mb, nb) register r of lane l then holds S[2m + mb][2n + nb] with
+// n = l % 32, m = 8 (r / 4) + 4 (l / 32) + r % 4.  Wave w takes token pairs
+// w, w + 4, ..., four per step with the next step's rows already loading; the
+// four waves' sums meet in one 16 KB LDS buffer, added in wave order.
 template <int DT>
 __global__ __launch_bounds__(256) void k_linattn_partial(const void* __restrict__ K,
                                                          const void* __restrict__ V,
@@ -321,53 +337,78 @@ __global__ __launch_bounds__(256) void k_linattn_partial(const void* __restrict_
     if (modes[h] != MODE_SURR) return;
     const int64_t t0 = (int64_t)c * chunk;
     const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
-    const int tid = threadIdx.x, e = tid >> 2, c0 = (tid & 3) * 16;
-    __shared__ __attribute__((aligned(16))) float sK[64][kD];
-    __shared__ __attribute__((aligned(16))) float sV[64][kD];
-    float acc[16], z = 0.f;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+    f32x16 acc[2][2];
+    float zacc[2] = {0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 16; ++i) acc[i] = 0.f;
-    for (int64_t tb = t0; tb < t1; tb += 64) {
-        const int64_t tok = tb + e;   // staging: token row e, values c0 ... c0+15
-        float kv[16], vv[16];
-        if (tok < t1) {
-            load16<DT>(K, (tok * H + h) * kD + c0, kv);
-            load16<DT>(V, (tok * H + h) * kD + c0, vv);
+    for (int mb = 0; mb < 2; ++mb) acc[mb][0] = acc[mb][1] = zero_f32x16();
+    // Rows of step tg: pairs tg + 8 u, u < kLinPairs (wave w starts at
+    // t0 + 2 w).
+    constexpr int kLinPairs = 4;
+    float2 a[kLinPairs], b[kLinPairs], an[kLinPairs], bn[kLinPairs];
+    auto load = [&](int64_t tg, float2 (&ka)[kLinPairs], float2 (&vb)[kLinPairs]) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) kv[i] = elu1(kv[i]);
-        } else {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) kv[i] = vv[i] = 0.f;
+        for (int u = 0; u < kLinPairs; ++u) {
+            const int64_t tok = tg + 8 * u + hh;
+            ka[u] = vb[u] = make_float2(0.f, 0.f);
+            if (tok < t1) {
+                const int64_t off = (tok * H + h) * kD;
+                ka[u] = load_pair<DT>(K, off, n);
+                vb[u] = load_pair<DT>(V, off, n);
+            }
         }
+    };
+    int64_t tg = t0 + 2 * wave;
+    load(tg, an, bn);
+    for (; tg < t1; tg += 8 * kLinPairs) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            *reinterpret_cast<float4*>(&sK[e][c0 + 4 * i]) =
-                make_float4(kv[4 * i], kv[4 * i + 1], kv[4 * i + 2], kv[4 * i + 3]);
-            *reinterpret_cast<float4*>(&sV[e][c0 + 4 * i]) =
-                make_float4(vv[4 * i], vv[4 * i + 1], vv[4 * i + 2], vv[4 * i + 3]);
+        for (int u = 0; u < kLinPairs; ++u) {
+            a[u] = an[u];
+            b[u] = bn[u];
         }
-        __syncthreads();
-#pragma unroll 4
-        for (int j = 0; j < 64; ++j) {
-            const float a = sK[j][e];
-            z += a;
+        if (tg + 8 * kLinPairs < t1) load(tg + 8 * kLinPairs, an, bn);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float4 v = *reinterpret_cast<const float4*>(&sV[j][c0 + 4 * i]);
-                acc[4 * i] = fmaf(a, v.x, acc[4 * i]);
-                acc[4 * i + 1] = fmaf(a, v.y, acc[4 * i + 1]);
-                acc[4 * i + 2] = fmaf(a, v.z, acc[4 * i + 2]);
-                acc[4 * i + 3] = fmaf(a, v.w, acc[4 * i + 3]);
+        for (int u = 0; u < kLinPairs; ++u) {
+            if (tg + 8 * u + hh < t1) {
+                a[u].x = elu1(a[u].x);
+                a[u].y = elu1(a[u].y);
+            }
+            zacc[0] += a[u].x;
+            zacc[1] += a[u].y;
+            acc[0][0] = mfma_f32(a[u].x, b[u].x, acc[0][0]);
+            acc[0][1] = mfma_f32(a[u].x, b[u].y, acc[0][1]);
+            acc[1][0] = mfma_f32(a[u].y, b[u].x, acc[1][0]);
+            acc[1][1] = mfma_f32(a[u].y, b[u].y, acc[1][1]);
+        }
+    }
+    __shared__ float sP[kD * kD + kD];   // S then z
+#pragma unroll 1
+    for (int wv = 0; wv < 4; ++wv) {
+        if (wave == wv) {
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int m = 8 * (r >> 2) + 4 * hh + (r & 3);
+                        float* d = &sP[(2 * m + mb) * kD + 2 * n + nb];
+                        *d = wv == 0 ? acc[mb][nb][r] : *d + acc[mb][nb][r];
+                    }
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                const float zt = zacc[mb] + __shfl_xor(zacc[mb], 32);
+                if (hh == 0) {
+                    float* d = &sP[kD * kD + 2 * n + mb];
+                    *d = wv == 0 ? zt : *d + zt;
+                }
             }
         }
         __syncthreads();
     }
     float* o = part + ((int64_t)h * gridDim.x + c) * kLinSums;
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        *reinterpret_cast<float4*>(o + e * kD + c0 + 4 * i) =
-            make_float4(acc[4 * i], acc[4 * i + 1], acc[4 * i + 2], acc[4 * i + 3]);
-    if ((tid & 3) == 0) o[kD * kD + e] = z;
+    for (int e = threadIdx.x; e < kLinSums; e += 256) o[e] = sP[e];
 }
 
 // K10b.  Grid (cdiv(kLinSums, 256), H): one sum per thread, chunks in order.
@@ -384,8 +425,15 @@ __global__ __launch_bounds__(256) void k_linattn_combine(const uint8_t* __restri
     sums[h * kLinSums + i] = acc;
 }
 
-// K10c.  One token per thread: phi(q) in registers, S and z broadcast from
-// LDS, 64 x 64 FMAs per token.
+// K10c.  Y^T = S^T phi(Q)^T per 32-query block on MFMA: reduction step s
+// covers features s and s + 32 (k = l / 32 picks one), so lane l needs the
+// contiguous half-row [32 (l / 32), 32 (l / 32) + 32) of its query l % 32,
+// and A[m][k] = S[s + 32 k][32 db + m] stays in registers for every block.
+// The denominator phi(q) . z is a dot product on the same halves plus one
+// exchange with lane l ^ 32.  Each wave takes kLinQBlocks blocks of 32
+// queries.
+constexpr int kLinQBlocks = 4;
+
 template <int DT>
 __global__ __launch_bounds__(256) void k_linattn_apply(const void* __restrict__ Q,
                                                        const uint8_t* __restrict__ modes,
@@ -393,47 +441,69 @@ __global__ __launch_bounds__(256) void k_linattn_apply(const void* __restrict__ 
                                                        int H, void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
-    __shared__ __attribute__((aligned(16))) float sS[kLinSums];
-    const float* src = sums + h * kLinSums;
-    for (int i = threadIdx.x; i < kLinSums; i += 256) sS[i] = src[i];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+    __shared__ float S[kLinSums];   // the head's S and z, staged once
+    for (int i = threadIdx.x; i < kLinSums; i += 256) S[i] = sums[h * kLinSums + i];
     __syncthreads();
-    const int64_t tok = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (tok >= N) return;
-    float fq[kD], y[kD];
+    float As[2][32], zr[32];
 #pragma unroll
-    for (int s4 = 0; s4 < 4; ++s4) load16<DT>(Q, (tok * H + h) * kD + 16 * s4, fq + 16 * s4);
-#pragma unroll
-    for (int k = 0; k < kD; ++k) {
-        fq[k] = elu1(fq[k]);
-        y[k] = 0.f;
+    for (int s = 0; s < 32; ++s) {
+        const int dk = s + 32 * hh;
+        As[0][s] = S[dk * kD + n];
+        As[1][s] = S[dk * kD + 32 + n];
+        zr[s] = S[kD * kD + dk];
     }
-    float den = 0.f;
+    // Blocks of this wave: q0(qb) = 32 (first + qb); the next block's
+    // half-rows load while the current block's MFMAs run.
+    const int64_t first = (int64_t)blockIdx.x * 4 * kLinQBlocks + wave * kLinQBlocks;
+    auto qrow = [&](int qb) {
+        const int64_t q0 = (first + qb) * 32, qi = q0 + n;
+        return ((qi < N ? qi : q0) * H + h) * kD + 32 * hh;
+    };
+    float fn[32];
+    if (first * 32 < N) load32<DT>(Q, qrow(0), fn);
+    for (int qb = 0; qb < kLinQBlocks; ++qb) {
+        const int64_t q0 = (first + qb) * 32;
+        if (q0 >= N) break;
+        const int64_t qi = q0 + n;
+        const bool ok = qi < N;
+        float fq[32];
 #pragma unroll
-    for (int e = 0; e < kD; ++e) {
-        const float a = fq[e];
-        den = fmaf(a, sS[kD * kD + e], den);
+        for (int s = 0; s < 32; ++s) fq[s] = fn[s];
+        if (qb + 1 < kLinQBlocks && q0 + 32 < N) load32<DT>(Q, qrow(qb + 1), fn);
+        float den = 0.f;
 #pragma unroll
-        for (int k = 0; k < kD; k += 4) {
-            const float4 s = *reinterpret_cast<const float4*>(&sS[e * kD + k]);
-            y[k] = fmaf(a, s.x, y[k]);
-            y[k + 1] = fmaf(a, s.y, y[k + 1]);
-            y[k + 2] = fmaf(a, s.z, y[k + 2]);
-            y[k + 3] = fmaf(a, s.w, y[k + 3]);
+        for (int s = 0; s < 32; ++s) {
+            fq[s] = elu1(fq[s]);
+            den = fmaf(fq[s], zr[s], den);
         }
-    }
-    const float inv = 1.f / den;
-    const int64_t off = (tok * H + h) * kD;
-    if (ydt == DT_BF16) {
+        den += __shfl_xor(den, 32);
+        f32x16 y[2] = {zero_f32x16(), zero_f32x16()};
 #pragma unroll
-        for (int k = 0; k < kD; k += 8)
-            *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + off + k) =
-                pack_bf16x8(y[k] * inv, y[k + 1] * inv, y[k + 2] * inv, y[k + 3] * inv,
-                            y[k + 4] * inv, y[k + 5] * inv, y[k + 6] * inv, y[k + 7] * inv);
-    } else {
+        for (int s = 0; s < 32; ++s) {
+            y[0] = mfma_f32(As[0][s], fq[s], y[0]);
+            y[1] = mfma_f32(As[1][s], fq[s], y[1]);
+        }
+        if (ok) {
+            const float inv = 1.f / den;
 #pragma unroll
-        for (int k = 0; k < kD; k += 4)
-            *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off + k) =
-                make_float4(y[k] * inv, y[k + 1] * inv, y[k + 2] * inv, y[k + 3] * inv);
+            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int64_t off = (qi * H + h) * kD + 32 * db + 8 * g + 4 * hh;
+                    const float y0 = y[db][4 * g] * inv, y1 = y[db][4 * g + 1] * inv;
+                    const float y2 = y[db][4 * g + 2] * inv, y3 = y[db][4 * g + 3] * inv;
+                    if (ydt == DT_BF16) {
+                        bf16x4 v;
+                        v[0] = (bf16)y0; v[1] = (bf16)y1; v[2] = (bf16)y2; v[3] = (bf16)y3;
+                        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + off) = v;
+                    } else {
+                        *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + off) =
+                            make_float4(y0, y1, y2, y3);
+                    }
+                }
+        }
     }
 }
 
@@ -461,7 +531,7 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
                            (int)MODE_SURR, a.ctx, a.N, a.H, a.Y, a.ydt);
     } else {   // SURR_LINEAR_ATTN
         const dim3 gp((unsigned)a.n3, a.H), gc((kLinSums + 255) / 256, a.H),
-            ga((unsigned)((a.N + 255) / 256), a.H);
+            ga((unsigned)((a.N + 32 * 4 * kLinQBlocks - 1) / (32 * 4 * kLinQBlocks)), a.H);
         if (a.dtype == DT_BF16) {
             hipLaunchKernelGGL(k_linattn_partial<DT_BF16>, gp, dim3(256), 0, st, a.K, a.V,
                                a.modes, a.N, a.H, a.chunk3, a.lpart);
