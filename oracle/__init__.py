@@ -40,6 +40,7 @@ POOL_GATED, POOL_MEAN = 0, 1
 SURR_EQ7, SURR_MEAN_CONTEXT, SURR_NO_RESIDUAL, SURR_ADD_IDENTITY, SURR_LINEAR_ATTN = 0, 1, 2, 3, 4
 ACT_GELU, ACT_RELU = 0, 1
 TAU_LOW, TAU_HIGH = 0.01, 0.20   # Section 4.2 and implementation details
+LN_EPS, ROPE_BASE = 1e-6, 100.0  # readings for the block around the layer
 
 
 def build(force: bool = False) -> str:
@@ -72,6 +73,9 @@ def _load():
             lib.or_surr_rows.argtypes = [P, i64, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P,
                                          P, P, P, P, i64, P, i32]
             lib.or_linattn_rows.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, P, i32]
+            lib.or_layernorm.argtypes = [P, i64, i32, P, P, dbl, P, i32]
+            lib.or_rope2d.argtypes = [P, i64, i32, i32, P, dbl, i32]
+            lib.or_gelu.argtypes = [P, i64]
             lib.or_threads_used.argtypes = [i32]
             lib.or_threads_used.restype = i32
             _lib = lib
@@ -279,3 +283,71 @@ def routed_layer(Q, K, V, W, U, w, surr, u=None, Wr=None, br=None, rule=RULE_ARG
             Y[:, h, :] = mean[h][None, :]     # Algorithm 1: broadcast of the value mean
     return dict(q_pool=q_pool, s=s, C=C, mean=mean, logits=logits, modes=modes, Y=Y,
                 Y_full_rows=Yf)
+
+
+# ------------------------------------------- dense block around the layer
+
+def layernorm(X, g, b, eps=LN_EPS, nthreads=0):
+    """Algorithm 1, LN: per row, (x - mean) / sqrt(var + eps) * g + b.  X: stored
+    values or float64 rows."""
+    if hasattr(X, "detach"):
+        X = as_f32(X)
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    N, D = X.shape
+    g, b = as_f32(g), as_f32(b)
+    Y = np.zeros((N, D), np.float64)
+    _load().or_layernorm(_p(X), N, D, _p(g), _p(b), float(eps), _p(Y), _nt(nthreads))
+    return Y
+
+
+def rope2d(T, pos, base=ROPE_BASE, nthreads=0):
+    """The positional information of QKV_h(., P): 2D rotary encoding of each
+    head's features by the token's (row, column) coordinates.  T: [N, H, d]
+    float64 (rotated copy returned); pos: [N, 2] int."""
+    T = np.array(T, dtype=np.float64, order="C", copy=True)
+    N, H, d = T.shape
+    pos = np.ascontiguousarray(pos, dtype=np.int32)
+    _load().or_rope2d(_p(T), N, H, d, _p(pos), float(base), _nt(nthreads))
+    return T
+
+
+def gelu(X):
+    """GELU with the exact normal CDF (erf form)."""
+    X = np.array(X, dtype=np.float64, order="C", copy=True)
+    _load().or_gelu(_p(X), X.size)
+    return X
+
+
+def linear(X, W, b):
+    """y = x W^T + b in float64 (W [out, in] as stored; a library matmul)."""
+    X = np.asarray(X, dtype=np.float64)
+    return X @ as_f32(W).astype(np.float64).T + as_f32(b).astype(np.float64)
+
+
+def block_qkv(X, pos, wt, H=16, eps=LN_EPS, base=ROPE_BASE, nthreads=0):
+    """Algorithm 1 steps (1)-(2a): X~ = LN_1(X); (Q_h, K_h, V_h) = QKV_h(X~, P),
+    the projection followed by the rotary encoding of Q and K.
+    X [N, D] -> Q, K, V [N, H, D/H] float64."""
+    Xn = layernorm(X, wt["ln1_w"], wt["ln1_b"], eps, nthreads)
+    N, D = Xn.shape
+    qkv = linear(Xn, wt["w_qkv"], wt["b_qkv"])
+    d = D // H
+    Q = rope2d(qkv[:, :D].reshape(N, H, d), pos, base, nthreads)
+    K = rope2d(qkv[:, D:2 * D].reshape(N, H, d), pos, base, nthreads)
+    V = qkv[:, 2 * D:].reshape(N, H, d).copy()
+    return Q, K, V
+
+
+def block_out(X, Y, wt, eps=LN_EPS, nthreads=0):
+    """Algorithm 1 steps (3)-(4): X_attn = X + LS_1(Y W_O); the block output
+    X_attn + LS_2(FFN(LN_2(X_attn))), FFN = Linear -> GELU -> Linear.
+    X, Y [N, D] stored values (Y = Concat of the head outputs; [N, H, d] is
+    accepted) -> (block output, X_attn), float64."""
+    X64 = as_f32(X).astype(np.float64)
+    N = X64.shape[0]
+    Y64 = (as_f32(Y) if hasattr(Y, "detach") else np.asarray(Y)).astype(np.float64)
+    A = linear(Y64.reshape(N, -1), wt["w_o"], wt["b_o"])
+    Xa = X64 + as_f32(wt["ls1"]).astype(np.float64) * A
+    Z = layernorm(Xa, wt["ln2_w"], wt["ln2_b"], eps, nthreads)
+    F = linear(gelu(linear(Z, wt["w_fc1"], wt["b_fc1"])), wt["w_fc2"], wt["b_fc2"])
+    return Xa + as_f32(wt["ls2"]).astype(np.float64) * F, Xa

@@ -438,3 +438,85 @@ void or_linattn_rows(const float *Q, const float *K, const float *V, int64_t N, 
     lin_ctx c = {Q, K, V, N, H, d, h, rows, Y};
     or_parallel_for(nrows, nthreads, lin_body, &c);
 }
+
+/* ------------------------------------------ dense block around the layer */
+/*
+ * Algorithm 1, steps (1), (3) and (4): the normalisations, the rotary
+ * positional encoding applied inside QKV_h(., P), and the FFN activation.
+ * (The linear layers are plain matrix products; the Python side uses a
+ * library matmul for them.)
+ */
+
+/* LN: y = (x - mean) / sqrt(var + eps) * g + b per row of D values, mean and
+ * the biased variance taken in index order. */
+typedef struct {
+    const double *X;
+    int64_t N;
+    int D;
+    const float *g, *b;
+    double eps;
+    double *Y;
+} ln_ctx;
+
+static void ln_body(void *p, int64_t lo, int64_t hi) {
+    ln_ctx *c = (ln_ctx *)p;
+    for (int64_t i = lo; i < hi; ++i) {
+        const double *x = c->X + i * c->D;
+        double mean = 0.0, var = 0.0;
+        for (int k = 0; k < c->D; ++k) mean += (double)x[k];
+        mean /= c->D;
+        for (int k = 0; k < c->D; ++k) var += ((double)x[k] - mean) * ((double)x[k] - mean);
+        var /= c->D;
+        const double r = 1.0 / sqrt(var + c->eps);
+        for (int k = 0; k < c->D; ++k)
+            c->Y[i * c->D + k] = ((double)x[k] - mean) * r * (double)c->g[k] + (double)c->b[k];
+    }
+}
+
+void or_layernorm(const double *X, int64_t N, int D, const float *g, const float *b, double eps,
+                  double *Y, int nthreads) {
+    ln_ctx c = {X, N, D, g, b, eps, Y};
+    or_parallel_for(N, nthreads, ln_body, &c);
+}
+
+/* 2D rotary encoding, in place on T [N, H, d] (d a multiple of 4).  The d
+ * features of a head split into two halves of d/2: the first is rotated by
+ * the token's row coordinate pos[i][0], the second by its column coordinate
+ * pos[i][1].  Within a half of m = d/2 features, feature j and feature
+ * j + m/2 (j < m/2) form a plane rotated by the angle p * base^(-2j/m):
+ *   (u, w) -> (u cos a - w sin a, u sin a + w cos a). */
+typedef struct {
+    double *T;
+    int64_t N;
+    int H, d;
+    const int32_t *pos;
+    double base;
+} rope_ctx;
+
+static void rope_body(void *p, int64_t lo, int64_t hi) {
+    rope_ctx *c = (rope_ctx *)p;
+    const int m = c->d / 2, q = m / 2;
+    for (int64_t i = lo; i < hi; ++i)
+        for (int h = 0; h < c->H; ++h)
+            for (int half = 0; half < 2; ++half) {
+                const double coord = (double)c->pos[2 * i + half];
+                double *t = c->T + (i * c->H + h) * (int64_t)c->d + half * m;
+                for (int j = 0; j < q; ++j) {
+                    const double a = coord * pow(c->base, -2.0 * j / (double)m);
+                    const double u = t[j], w = t[j + q];
+                    t[j] = u * cos(a) - w * sin(a);
+                    t[j + q] = u * sin(a) + w * cos(a);
+                }
+            }
+}
+
+void or_rope2d(double *T, int64_t N, int H, int d, const int32_t *pos, double base,
+               int nthreads) {
+    rope_ctx c = {T, N, H, d, pos, base};
+    or_parallel_for(N, nthreads, rope_body, &c);
+}
+
+/* GELU with the exact normal CDF: x * (1 + erf(x / sqrt 2)) / 2, in place. */
+void or_gelu(double *X, int64_t n) {
+    for (int64_t i = 0; i < n; ++i) X[i] = 0.5 * X[i] * (1.0 + erf(X[i] / sqrt(2.0)));
+}

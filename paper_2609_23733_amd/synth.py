@@ -50,7 +50,12 @@ TENSOR_IDS = {
     "g_w1": 12, "g_b1": 13, "g_w2": 14, "g_b2": 15,
     "d_w1": 16, "d_b1": 17, "d_w2": 18, "d_b2": 19,
     "rows": 20,
+    "X": 30, "ln1_w": 31, "ln1_b": 32, "w_qkv": 33, "b_qkv": 34, "w_o": 35, "b_o": 36,
+    "ls1": 37, "ln2_w": 38, "ln2_b": 39, "w_fc1": 40, "b_fc1": 41, "w_fc2": 42, "b_fc2": 43,
+    "ls2": 44,
 }
+SPECIAL_TOKENS = 5      # camera + 4 register tokens at the start of every view
+PATCH_GRID = 37         # patch tokens per row of the 37 x 37 grid
 
 
 def splitmix64(x: int) -> int:
@@ -239,3 +244,55 @@ WORKLOADS = {
     "s100_bf16": dict(S=100, dtype="bf16", n_full=4),
     "s500_bf16": dict(S=500, dtype="bf16", n_full=4),
 }
+
+
+# ----------------------------------------------------- block around the layer
+#
+# Inputs of the dense block of Algorithm 1 (LN_1, QKV with positions, W_O,
+# LayerScale, LN_2, FFN) for D = H * d = 1024 and FFN width 4 D:
+#   X                       ~ N(0, 1)                        (stored dtype)
+#   LN gains ~ U(0.5, 1.5), LN biases ~ U(-0.1, 0.1)        (fp32)
+#   W_qkv, W_o, W_fc1       ~ U(-1/sqrt(D), 1/sqrt(D))      (stored dtype)
+#   W_fc2                   ~ U(-1/sqrt(4D), 1/sqrt(4D))    (stored dtype)
+#   biases                  ~ U(-0.02, 0.02)                 (fp32)
+#   LayerScale LS_1, LS_2   ~ U(0.5, 1.5)                    (fp32; large enough
+#                             that both residual branches matter in parity tests)
+# Positions: the SPECIAL_TOKENS tokens of a view at (0, 0), patch k of the view
+# at (k // PATCH_GRID + 1, k % PATCH_GRID + 1).
+
+BLOCK_KEYS = ("ln1_w", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ls1", "ln2_w", "ln2_b",
+              "w_fc1", "b_fc1", "w_fc2", "b_fc2", "ls2")
+
+
+def token_positions(S: int, P: int = TOKENS_PER_VIEW) -> np.ndarray:
+    """(row, column) of every token of S views of P tokens: int32 [S * P, 2]."""
+    t = np.arange(P)
+    k = t - SPECIAL_TOKENS
+    rc = np.stack([k // PATCH_GRID + 1, k % PATCH_GRID + 1], axis=1)
+    rc[t < SPECIAL_TOKENS] = 0
+    return np.ascontiguousarray(np.tile(rc, (S, 1)), dtype=np.int32)
+
+
+def make_block_weights(key: Sequence[int] = (0, 0), dtype: str = "bf16", H: int = H_HEADS,
+                       d: int = HEAD_DIM) -> Dict[str, torch.Tensor]:
+    """Seeded weights of one dense block (CPU tensors)."""
+    D = H * d
+    sd = lambda name: derive_seed(*key, TENSOR_IDS[name])
+    u = lambda name, shape, lo, hi: uniform(shape, sd(name), (hi - lo) / 2) + (hi + lo) / 2
+    mat = lambda name, shape, fan: stored(uniform(shape, sd(name), 1.0 / np.sqrt(fan)), dtype)
+    return {
+        "ln1_w": u("ln1_w", (D,), 0.5, 1.5), "ln1_b": u("ln1_b", (D,), -0.1, 0.1),
+        "w_qkv": mat("w_qkv", (3 * D, D), D), "b_qkv": u("b_qkv", (3 * D,), -0.02, 0.02),
+        "w_o": mat("w_o", (D, D), D), "b_o": u("b_o", (D,), -0.02, 0.02),
+        "ls1": u("ls1", (D,), 0.5, 1.5),
+        "ln2_w": u("ln2_w", (D,), 0.5, 1.5), "ln2_b": u("ln2_b", (D,), -0.1, 0.1),
+        "w_fc1": mat("w_fc1", (4 * D, D), D), "b_fc1": u("b_fc1", (4 * D,), -0.02, 0.02),
+        "w_fc2": mat("w_fc2", (D, 4 * D), 4 * D), "b_fc2": u("b_fc2", (D,), -0.02, 0.02),
+        "ls2": u("ls2", (D,), 0.5, 1.5),
+    }
+
+
+def make_block_input(S: int, P: int = TOKENS_PER_VIEW, key: Sequence[int] = (0, 0),
+                     dtype: str = "bf16", D: int = H_HEADS * HEAD_DIM, device="cpu"):
+    """Seeded block input tokens X [S * P, D] in the stored dtype."""
+    return stored(normal((S * P, D), derive_seed(*key, TENSOR_IDS["X"]), 1.0, device), dtype)

@@ -44,12 +44,30 @@ MUTANTS = {
     "linattn_phi_no_shift": ("return x > 0.0 ? x + 1.0 : exp(x);", "return x > 0.0 ? x : exp(x);"),
     "linattn_not_normalised": ("for (int e = 0; e < d; ++e) y[e] = acc[e] / den;",
                                "for (int e = 0; e < d; ++e) y[e] = acc[e] / (double)c->N;"),
+    # dense block around the layer (pins in test_oracle_block_pins.py)
+    "ln_unbiased_variance": ("        var /= c->D;", "        var /= (c->D - 1);", "block"),
+    "ln_eps_outside_sqrt": ("const double r = 1.0 / sqrt(var + c->eps);",
+                            "const double r = 1.0 / (sqrt(var) + c->eps);", "block"),
+    "ln_bias_dropped": ("* (double)c->g[k] + (double)c->b[k];", "* (double)c->g[k];", "block"),
+    "rope_sign_flipped": ("t[j] = u * cos(a) - w * sin(a);", "t[j] = u * cos(a) + w * sin(a);",
+                          "block"),
+    "rope_adjacent_pairs": ("const double u = t[j], w = t[j + q];",
+                            "const double u = t[2 * j], w = t[2 * j + 1];", "block"),
+    "rope_halves_same_coordinate": ("const double coord = (double)c->pos[2 * i + half];",
+                                    "const double coord = (double)c->pos[2 * i];", "block"),
+    "rope_frequency_exponent": ("pow(c->base, -2.0 * j / (double)m)", "pow(c->base, -1.0 * j / (double)m)",
+                                "block"),
+    "block_gelu_tanh_form": ("X[i] = 0.5 * X[i] * (1.0 + erf(X[i] / sqrt(2.0)));",
+                             "X[i] = 0.5 * X[i] * (1.0 + tanh(0.7978845608 * (X[i] + 0.044715 * X[i] * X[i] * X[i])));",
+                             "block"),
 }
+PIN_FILES = {"layer": "test_oracle_pins.py", "block": "test_oracle_block_pins.py"}
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_pins_catch_mutant(name, tmp_path):
-    old, new = MUTANTS[name]
+    old, new = MUTANTS[name][:2]
+    pins = PIN_FILES[MUTANTS[name][2] if len(MUTANTS[name]) > 2 else "layer"]
     src = open(SRC).read()
     assert src.count(old) == 1, "mutation anchor not found once: " + name
     msrc = tmp_path / "mutant.c"
@@ -59,6 +77,6 @@ def test_pins_catch_mutant(name, tmp_path):
                            str(msrc), "-lm", "-lpthread"])
     env = dict(os.environ, VP_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", pins)],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, "pins did not catch mutant %s:\n%s" % (name, r.stdout[-2000:])
