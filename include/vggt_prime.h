@@ -218,6 +218,51 @@ vp_status vp_linear_heads(const vp_shape *shape, const void *Q, const void *K, c
                           const vp_surrogate_weights *surr, void *Y, vp_dtype y_dtype,
                           void *ws, size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------------------
+ * The dense block around the routed layer (Algorithm 1, steps 1, 3 and 4), for
+ * bf16 layers with H = 16 heads of d = 64 (model width D = 1024):
+ *   vp_block_qkv:  X~ = LN_1(X); (Q, K, V) = X~ W_qkv^T + b_qkv, then the 2D
+ *                  rotary encoding of the token positions applied to Q and K
+ *                  (the positional information P of QKV_h(X~, P));
+ *   [vp_router_score, vp_assign_heads, vp_routed_global_attention: Y]
+ *   vp_block_out:  X_attn = X + LS_1 (Y W_O^T + b_O);
+ *                  X_out  = X_attn + LS_2 (GELU(LN_2(X_attn) W_fc1^T + b_fc1)
+ *                           W_fc2^T + b_fc2).
+ * LN: per token, (x - mean) / sqrt(var + eps) * gain + bias (biased variance).
+ * Rotary encoding: in each head, features j and j + 16 of the first 32 form a
+ * plane rotated by row * base^(-j/16), those of the last 32 by column *
+ * base^(-j/16), j < 16.  GELU: x (1 + erf(x / sqrt 2)) / 2.
+ * X, Y, X_out, Q, K, V: [N, D] bf16 (Q, K, V and Y are the [N, H, d] tensors
+ * of the routed layer); pos: int32 [N, 2] (row, column) per token.  Weight
+ * matrices bf16 [out, in] row-major; biases, LN gains and biases and LayerScale
+ * vectors fp32.  Arithmetic in fp32, every output rounded once to bf16.
+ * X_out may be the same buffer as X. */
+typedef struct {
+    const float *ln1_w, *ln1_b;   /* [D] */
+    const void *w_qkv;            /* [3D, D]: rows 0..D-1 Q, D..2D-1 K, 2D..3D-1 V */
+    const float *b_qkv;           /* [3D] */
+    const void *w_o;              /* [D, D] */
+    const float *b_o, *ls1;       /* [D] */
+    const float *ln2_w, *ln2_b;   /* [D] */
+    const void *w_fc1;            /* [4D, D] */
+    const float *b_fc1;           /* [4D] */
+    const void *w_fc2;            /* [D, 4D] */
+    const float *b_fc2, *ls2;     /* [D] */
+    float ln_eps;                 /* 1e-6 when 0 */
+    float rope_base;              /* 100 when 0 */
+} vp_block_weights;
+
+/* Bytes of device workspace vp_block_qkv and vp_block_out need for `shape`
+ * (0 if the shape is invalid or not a bf16 layer with H = 16): LN output,
+ * X_attn and the FFN hidden layer, 12 KB per token.  256-byte aligned. */
+size_t vp_block_workspace_bytes(const vp_shape *shape);
+vp_status vp_block_qkv(const vp_shape *shape, const void *X, const int32_t *pos,
+                       const vp_block_weights *w, void *Q, void *K, void *V, void *ws,
+                       size_t ws_bytes, void *stream);
+vp_status vp_block_out(const vp_shape *shape, const void *X, const void *Y,
+                       const vp_block_weights *w, void *X_out, void *ws, size_t ws_bytes,
+                       void *stream);
+
 /* Static description of a status code. */
 const char *vp_status_string(vp_status s);
 

@@ -1,0 +1,294 @@
+// The dense block around the routed layer (Algorithm 1, steps 1, 3 and 4):
+//   X~ = LN_1(X);  (Q, K, V) = QKV(X~) with the 2D rotary encoding of the
+//   token positions applied to Q and K;  [routed attention: Y];
+//   X_attn = X + LS_1 (Y W_O^T + b_O);
+//   X_out  = X_attn + LS_2 (W_fc2 GELU(W_fc1 LN_2(X_attn) + b_fc1) + b_fc2).
+// Two kinds of kernel: a LayerNorm (one wave per row, HBM-bound) and a bf16
+// GEMM on MFMA whose epilogue applies the bias and then the step's own
+// elementwise work (rotary encoding and the split into Q, K, V; GELU; or
+// LayerScale plus residuals), so no projection output makes an extra trip
+// through HBM.  The residual stream is never rounded in between: the W_O
+// step stores only the attention update A = LS_1 (Y W_O^T + b_O), and LN_2
+// and the last step form X_attn = X + A in fp32 from X and A.
+#include "vp_device.hpp"
+#include "vp_internal.hpp"
+
+namespace vp {
+
+constexpr int kDm = 1024;   // model width D = 16 heads x 64
+
+// ------------------------------------------------------------------------
+// B1: LayerNorm over the D = 1024 features of each row of X (+ X2 when given,
+// added in fp32): mean and biased variance in fp32 (two passes over
+// registers), y = (x - mean) r g + b, r = 1 / sqrt(var + eps), rounded to
+// bf16.  One wave per row; lane l holds features 16 l ... 16 l + 15.
+// ------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_layernorm(const bf16* __restrict__ X,
+                                                   const bf16* __restrict__ X2, int64_t T,
+                                                   const float* __restrict__ g,
+                                                   const float* __restrict__ b, float eps,
+                                                   bf16* __restrict__ Y) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= T) return;
+    const int lane = threadIdx.x & 63, c0 = 16 * lane;
+    const bf16* xr = X + row * kDm + c0;
+    const bf16x8 a = load_bf16x8(xr), bb = load_bf16x8(xr + 8);
+    float x[16];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        x[j] = bf16_to_f32(a[j]);
+        x[8 + j] = bf16_to_f32(bb[j]);
+    }
+    if (X2) {
+        const bf16* x2 = X2 + row * kDm + c0;
+        const bf16x8 a2 = load_bf16x8(x2), b2 = load_bf16x8(x2 + 8);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            x[j] += bf16_to_f32(a2[j]);
+            x[8 + j] += bf16_to_f32(b2[j]);
+        }
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) s += x[j];
+    const float mean = wave_sum(s) * (1.f / kDm);
+    float q = 0.f;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) q = fmaf(x[j] - mean, x[j] - mean, q);
+    const float r = rsqrtf(wave_sum(q) * (1.f / kDm) + eps);
+    float y[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) y[j] = fmaf((x[j] - mean) * r, g[c0 + j], b[c0 + j]);
+    bf16* yr = Y + row * kDm + c0;
+    *reinterpret_cast<bf16x8*>(yr) = pack_bf16x8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]);
+    *reinterpret_cast<bf16x8*>(yr + 8) =
+        pack_bf16x8(y[8], y[9], y[10], y[11], y[12], y[13], y[14], y[15]);
+}
+
+// ------------------------------------------------------------------------
+// B2: D^T = W X^T for W [F, Kd] (weights as stored, [out, in]) and X [T, Kd]
+// (token rows), bf16 operands, fp32 accumulation: both operands are
+// Kd-contiguous, as the MFMA wants them.  Workgroup tile 256 features x 256
+// tokens, 8 waves of 128 x 64 (4 x 2 blocks of 32 x 32), Kd in stages of 64
+// double-buffered through LDS (144-byte rows: conflict-free 16-byte reads),
+// one barrier per stage.  Output features are the MFMA rows, so lane l holds
+// token l % 32 of a block and features 8 (r / 4) + 4 (l / 32) + r % 4 in its
+// register r: four consecutive features per store, and the rotary pair
+// (j, j + 16) of a 32-feature half in registers r and r + 8 of one lane.
+// Tiles are ordered in groups of four feature tiles per token tile, and
+// consecutive tiles share an XCD, so an XCD's L2 keeps a token tile for four
+// feature tiles and a group of weight tiles for all its token tiles.
+// ------------------------------------------------------------------------
+constexpr int kGM = 256, kGN = 256, kGK = 64, kGRow = 72, kGGroup = 4;
+
+enum { EPI_QKV = 0, EPI_GELU = 1, EPI_RESID = 2 };
+
+struct GemmArgs {
+    const bf16* W;        // [F, Kd]
+    const bf16* X;        // [T, Kd]
+    const float* bias;    // [F]
+    int64_t T;
+    int F, Kd;
+    bf16* out;            // GELU: [T, F]; RESID: [T, F]
+    const bf16 *res, *res2;   // RESID: residuals [T, F] (either may be null)
+    const float* ls;      // RESID: LayerScale [F]
+    bf16 *q, *k, *v;      // QKV: [T, D] each
+    const int32_t* pos;   // QKV: [T, 2] (row, column)
+    float log2_base;      // QKV: log2 of the rotary base
+};
+
+__device__ __forceinline__ float gelu_erf(float x) {
+    return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
+}
+
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void k_gemm(GemmArgs g) {
+    const int nft = g.F / kGM;
+    const int ntt = (int)((g.T + kGN - 1) / kGN);
+    const int total = nft * ntt;
+    const int L = xcd_remap(blockIdx.x, total);
+    const int grp = L / (kGGroup * ntt), in = L - grp * kGGroup * ntt;
+    const int tt = in / kGGroup, ft = grp * kGGroup + in % kGGroup;
+    const int f0 = ft * kGM;
+    const int64_t t0 = (int64_t)tt * kGN;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = lane & 31, hh = lane >> 5;
+    const int wm = wave >> 2, wn = wave & 3;
+
+    __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
+    __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
+
+    // Stage copy: 4 chunks of 16 bytes of W and 4 of X per thread; chunk
+    // c = tid + 512 i is row c / 8, bytes 16 (c % 8) of the stage's 128.
+    // Token rows past T read row T - 1; their outputs are never stored.
+    u32x4 rw[4], rx[4];
+    auto gload = [&](int kt) {
+        const int k0 = kt * kGK;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 512 * i, row = c >> 3, seg = (c & 7) * 8;
+            rw[i] = *reinterpret_cast<const u32x4*>(g.W + (int64_t)(f0 + row) * g.Kd + k0 + seg);
+            const int64_t tr = t0 + row < g.T ? t0 + row : g.T - 1;
+            rx[i] = *reinterpret_cast<const u32x4*>(g.X + tr * g.Kd + k0 + seg);
+        }
+    };
+    auto lstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 512 * i, row = c >> 3, seg = (c & 7) * 8;
+            *reinterpret_cast<u32x4*>(&sW[buf][row * kGRow + seg]) = rw[i];
+            *reinterpret_cast<u32x4*>(&sX[buf][row * kGRow + seg]) = rx[i];
+        }
+    };
+
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int fb = 0; fb < 4; ++fb) acc[fb][0] = acc[fb][1] = zero_f32x16();
+
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    const int nk = g.Kd / kGK;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < nk) gload(kt + 1);
+#pragma unroll
+        for (int ks = 0; ks < kGK / 16; ++ks) {
+            bf16x8 a[4], b[2];
+#pragma unroll
+            for (int fb = 0; fb < 4; ++fb)
+                a[fb] = *reinterpret_cast<const bf16x8*>(
+                    &sW[buf][(128 * wm + 32 * fb + n) * kGRow + 16 * ks + 8 * hh]);
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+                b[tb] = *reinterpret_cast<const bf16x8*>(
+                    &sX[buf][(64 * wn + 32 * tb + n) * kGRow + 16 * ks + 8 * hh]);
+#pragma unroll
+            for (int fb = 0; fb < 4; ++fb)
+#pragma unroll
+                for (int tb = 0; tb < 2; ++tb) acc[fb][tb] = mfma_bf16(a[fb], b[tb], acc[fb][tb]);
+        }
+        if (kt + 1 < nk) lstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    // Epilogue.  Lane: token t of block tb, features fbase + 8 gq + 4 hh + i
+    // in register r = 4 gq + i.
+    float omega[8];   // rotary frequencies of features j = 8 (r / 4) + 4 hh + r % 4, r < 8
+    if (EPI == EPI_QKV) {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+            const int j = 8 * (r >> 2) + 4 * hh + (r & 3);
+            omega[r] = exp2f(-(float)j * (1.f / 16.f) * g.log2_base);
+        }
+    }
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+        const int64_t t = t0 + 64 * wn + 32 * tb + n;
+        if (t >= g.T) continue;
+        int2 p = make_int2(0, 0);
+        if (EPI == EPI_QKV) p = *reinterpret_cast<const int2*>(g.pos + 2 * t);
+#pragma unroll
+        for (int fb = 0; fb < 4; ++fb) {
+            const int fbase = f0 + 128 * wm + 32 * fb;
+            float v[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                v[r] = acc[fb][tb][r] + g.bias[fbase + 8 * (r >> 2) + 4 * hh + (r & 3)];
+            bf16* dst;
+            if (EPI == EPI_QKV) {
+                const int which = fbase / kDm, fin = fbase - which * kDm;
+                if (which < 2) {   // Q, K: rotate the planes (j, j + 16) of this half
+                    const float coord = (float)((fin & 32) ? p.y : p.x);
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) {
+                        float sn, cs;
+                        __sincosf(coord * omega[r], &sn, &cs);
+                        const float u = v[r], w = v[r + 8];
+                        v[r] = u * cs - w * sn;
+                        v[r + 8] = u * sn + w * cs;
+                    }
+                }
+                dst = (which == 0 ? g.q : (which == 1 ? g.k : g.v)) + t * kDm + fin;
+            } else {
+                dst = g.out + t * g.F + fbase;
+                if (EPI == EPI_GELU) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) v[r] = gelu_erf(v[r]);
+                } else {   // ls (acc + bias) + res + res2, summed in fp32
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        const int f = fbase + 8 * gq + 4 * hh;
+                        float base[4] = {0.f, 0.f, 0.f, 0.f};
+                        if (g.res) {
+                            const bf16x4 rs = *reinterpret_cast<const bf16x4*>(g.res + t * g.F + f);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) base[i] = (float)rs[i];
+                        }
+                        if (g.res2) {
+                            const bf16x4 rs = *reinterpret_cast<const bf16x4*>(g.res2 + t * g.F + f);
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) base[i] += (float)rs[i];
+                        }
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            v[4 * gq + i] = fmaf(g.ls[f + i], v[4 * gq + i], base[i]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                bf16x4 o;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) o[i] = (bf16)v[4 * gq + i];
+                *reinterpret_cast<bf16x4*>(dst + 8 * gq + 4 * hh) = o;
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------ launchers
+
+static void gemm(int epi, const GemmArgs& a, hipStream_t st) {
+    const unsigned grid =
+        (unsigned)((a.F / kGM) * ((a.T + kGN - 1) / kGN));
+    if (epi == EPI_QKV)
+        hipLaunchKernelGGL(k_gemm<EPI_QKV>, dim3(grid), dim3(512), 0, st, a);
+    else if (epi == EPI_GELU)
+        hipLaunchKernelGGL(k_gemm<EPI_GELU>, dim3(grid), dim3(512), 0, st, a);
+    else
+        hipLaunchKernelGGL(k_gemm<EPI_RESID>, dim3(grid), dim3(512), 0, st, a);
+}
+
+static void layernorm(const bf16* X, const bf16* X2, int64_t T, const float* g, const float* b,
+                      float eps, bf16* Y, hipStream_t st) {
+    hipLaunchKernelGGL(k_layernorm, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, st, X, X2, T, g,
+                       b, eps, Y);
+}
+
+void launch_block_qkv(const BlockArgs& a, hipStream_t st) {
+    layernorm(a.X, nullptr, a.T, a.ln1_w, a.ln1_b, a.eps, a.ln, st);
+    GemmArgs g = {};
+    g.W = a.w_qkv; g.X = a.ln; g.bias = a.b_qkv; g.T = a.T; g.F = 3 * kDm; g.Kd = kDm;
+    g.q = a.Q; g.k = a.K; g.v = a.V; g.pos = a.pos; g.log2_base = log2f(a.rope_base);
+    gemm(EPI_QKV, g, st);
+}
+
+void launch_block_out(const BlockArgs& a, hipStream_t st) {
+    GemmArgs g = {};
+    g.T = a.T;
+    // A = LS_1 (Y W_O^T + b_O), the attention update (X_attn = X + A)
+    g.W = a.w_o; g.X = a.Y; g.bias = a.b_o; g.F = kDm; g.Kd = kDm;
+    g.res = nullptr; g.res2 = nullptr; g.ls = a.ls1; g.out = a.xa;
+    gemm(EPI_RESID, g, st);
+    layernorm(a.X, a.xa, a.T, a.ln2_w, a.ln2_b, a.eps, a.ln, st);
+    // H = GELU(LN_2(X + A) W_fc1^T + b_fc1)
+    g.W = a.w_fc1; g.X = a.ln; g.bias = a.b_fc1; g.F = 4 * kDm; g.Kd = kDm; g.out = a.hid;
+    gemm(EPI_GELU, g, st);
+    // X_out = X + A + LS_2 (H W_fc2^T + b_fc2)
+    g.W = a.w_fc2; g.X = a.hid; g.bias = a.b_fc2; g.F = kDm; g.Kd = 4 * kDm;
+    g.res = a.X; g.res2 = a.xa; g.ls = a.ls2; g.out = a.Xout;
+    gemm(EPI_RESID, g, st);
+}
+
+}  // namespace vp

@@ -348,4 +348,95 @@ vp_status vp_routed_global_attention(const vp_shape* shape, const void* Q, const
     return hip_status("vp_routed_global_attention");
 }
 
+// ------------------------------------------------ dense block around the layer
+
+namespace {
+
+constexpr int64_t kBlockD = 1024;
+
+bool block_shape_ok(const vp_shape* s) {
+    return s && s->S >= 1 && s->P >= 1 && s->S <= kMaxTokens && s->P <= kMaxTokens &&
+           s->S * s->P <= kMaxTokens && s->H == VP_MAX_HEADS && s->d == VP_HEAD_DIM &&
+           s->dtype == VP_BF16;
+}
+
+size_t block_ws(int64_t N) { return align_up((size_t)N * kBlockD * 2 * (1 + 1 + 4)); }
+
+bool aligned4(const void* p) { return ((uintptr_t)p & 3u) == 0; }
+
+vp_status check_block(const vp_shape* shape, const vp_block_weights* w, void* ws,
+                      size_t ws_bytes, vp::BlockArgs* a) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (!block_shape_ok(shape)) return VP_ERR_UNSUPPORTED;
+    if (!w) return VP_ERR_INVALID_ARG;
+    const void* mats[] = {w->w_qkv, w->w_o, w->w_fc1, w->w_fc2};
+    for (const void* m : mats)
+        if (!m || !aligned16(m)) return VP_ERR_INVALID_ARG;
+    const float* vecs[] = {w->ln1_w, w->ln1_b, w->b_qkv, w->b_o, w->ls1, w->ln2_w,
+                           w->ln2_b, w->b_fc1, w->b_fc2, w->ls2};
+    for (const float* v : vecs)
+        if (!v || !aligned4(v)) return VP_ERR_INVALID_ARG;
+    if (!isfinite(w->ln_eps) || w->ln_eps < 0.f || !isfinite(w->rope_base) ||
+        w->rope_base < 0.f || (w->rope_base > 0.f && w->rope_base <= 1.f))
+        return VP_ERR_INVALID_ARG;
+    if (!ws || ((uintptr_t)ws & (kAlign - 1))) return VP_ERR_INVALID_ARG;
+    const int64_t N = shape->S * shape->P;
+    if (ws_bytes < block_ws(N)) return VP_ERR_WORKSPACE;
+    memset(a, 0, sizeof(*a));
+    a->T = N;
+    a->ln1_w = w->ln1_w; a->ln1_b = w->ln1_b; a->ln2_w = w->ln2_w; a->ln2_b = w->ln2_b;
+    a->ls1 = w->ls1; a->ls2 = w->ls2;
+    a->w_qkv = (const __bf16*)w->w_qkv; a->w_o = (const __bf16*)w->w_o;
+    a->w_fc1 = (const __bf16*)w->w_fc1; a->w_fc2 = (const __bf16*)w->w_fc2;
+    a->b_qkv = w->b_qkv; a->b_o = w->b_o; a->b_fc1 = w->b_fc1; a->b_fc2 = w->b_fc2;
+    a->eps = w->ln_eps > 0.f ? w->ln_eps : 1e-6f;
+    a->rope_base = w->rope_base > 0.f ? w->rope_base : 100.f;
+    char* p = (char*)ws;
+    a->ln = (__bf16*)p;
+    a->xa = (__bf16*)(p + (size_t)N * kBlockD * 2);
+    a->hid = (__bf16*)(p + (size_t)N * kBlockD * 4);
+    return VP_OK;
+}
+
+}  // namespace
+
+size_t vp_block_workspace_bytes(const vp_shape* shape) {
+    if (shape_status(shape) != VP_OK || !block_shape_ok(shape)) return 0;
+    return block_ws(shape->S * shape->P);
+}
+
+vp_status vp_block_qkv(const vp_shape* shape, const void* X, const int32_t* pos,
+                       const vp_block_weights* w, void* Q, void* K, void* V, void* ws,
+                       size_t ws_bytes, void* stream) {
+    vp::BlockArgs a;
+    vp_status st = check_block(shape, w, ws, ws_bytes, &a);
+    if (st != VP_OK) return st;
+    if (!X || !Q || !K || !V || !pos || !aligned16(X) || !aligned16(Q) || !aligned16(K) ||
+        !aligned16(V) || ((uintptr_t)pos & 7u))
+        return VP_ERR_INVALID_ARG;
+    a.X = (const __bf16*)X;
+    a.pos = pos;
+    a.Q = (__bf16*)Q; a.K = (__bf16*)K; a.V = (__bf16*)V;
+    (void)hipGetLastError();
+    vp::launch_block_qkv(a, (hipStream_t)stream);
+    return hip_status("vp_block_qkv");
+}
+
+vp_status vp_block_out(const vp_shape* shape, const void* X, const void* Y,
+                       const vp_block_weights* w, void* X_out, void* ws, size_t ws_bytes,
+                       void* stream) {
+    vp::BlockArgs a;
+    vp_status st = check_block(shape, w, ws, ws_bytes, &a);
+    if (st != VP_OK) return st;
+    if (!X || !Y || !X_out || !aligned16(X) || !aligned16(Y) || !aligned16(X_out))
+        return VP_ERR_INVALID_ARG;
+    a.X = (const __bf16*)X;
+    a.Y = (const __bf16*)Y;
+    a.Xout = (__bf16*)X_out;
+    (void)hipGetLastError();
+    vp::launch_block_out(a, (hipStream_t)stream);
+    return hip_status("vp_block_out");
+}
+
 }  // extern "C"

@@ -52,6 +52,22 @@ constexpr int kLinSums = 64 * 64 + 64;
 enum { SURR_EQ7 = 0, SURR_MEAN_CONTEXT = 1, SURR_NO_RESIDUAL = 2, SURR_ADD_IDENTITY = 3,
        SURR_LINEAR_ATTN = 4 };
 
+// The dense block around the routed layer (bf16, D = 1024).
+struct BlockArgs {
+    int64_t T;                       // tokens
+    const __bf16 *X, *Y;             // block input; routed-attention output (Y: block_out)
+    const int32_t* pos;              // [T, 2] (row, column)
+    const float *ln1_w, *ln1_b, *ln2_w, *ln2_b, *ls1, *ls2;
+    const __bf16 *w_qkv, *w_o, *w_fc1, *w_fc2;
+    const float *b_qkv, *b_o, *b_fc1, *b_fc2;
+    float eps, rope_base;
+    __bf16 *Q, *K, *V;               // block_qkv outputs [T, D]
+    __bf16* Xout;                    // block_out output [T, D]
+    __bf16 *ln, *xa, *hid;           // workspace: LN output [T, D], attention update [T, D], FFN hidden [T, 4D]
+};
+
+void launch_block_qkv(const BlockArgs& a, hipStream_t st);
+void launch_block_out(const BlockArgs& a, hipStream_t st);
 void launch_router(const RouterArgs& a, hipStream_t st);
 void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,
                           int dtype, float* logits, hipStream_t st);

@@ -30,7 +30,11 @@ TAU_LOW, TAU_HIGH = 0.01, 0.20
 
 EXPORTS = ("vp_workspace_bytes", "vp_router_score", "vp_router_logits", "vp_assign_heads",
            "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
-           "vp_linear_heads", "vp_status_string", "vp_last_error")
+           "vp_linear_heads", "vp_status_string", "vp_last_error", "vp_block_workspace_bytes",
+           "vp_block_qkv", "vp_block_out")
+MODEL_DIM = MAX_HEADS * HEAD_DIM
+BLOCK_VECS = ("ln1_w", "ln1_b", "b_qkv", "b_o", "ls1", "ln2_w", "ln2_b", "b_fc1", "b_fc2", "ls2")
+BLOCK_MATS = ("w_qkv", "w_o", "w_fc1", "w_fc2")
 
 
 class vp_shape(ctypes.Structure):
@@ -53,6 +57,16 @@ class vp_surrogate_weights(ctypes.Structure):
                 ("d_w2", ctypes.c_void_p), ("g_b1", ctypes.c_void_p), ("g_b2", ctypes.c_void_p),
                 ("d_b1", ctypes.c_void_p), ("d_b2", ctypes.c_void_p), ("L", ctypes.c_int32),
                 ("act", ctypes.c_int), ("variant", ctypes.c_int)]
+
+
+class vp_block_weights(ctypes.Structure):
+    _fields_ = [("ln1_w", ctypes.c_void_p), ("ln1_b", ctypes.c_void_p),
+                ("w_qkv", ctypes.c_void_p), ("b_qkv", ctypes.c_void_p),
+                ("w_o", ctypes.c_void_p), ("b_o", ctypes.c_void_p), ("ls1", ctypes.c_void_p),
+                ("ln2_w", ctypes.c_void_p), ("ln2_b", ctypes.c_void_p),
+                ("w_fc1", ctypes.c_void_p), ("b_fc1", ctypes.c_void_p),
+                ("w_fc2", ctypes.c_void_p), ("b_fc2", ctypes.c_void_p), ("ls2", ctypes.c_void_p),
+                ("ln_eps", ctypes.c_float), ("rope_base", ctypes.c_float)]
 
 
 _lib = None
@@ -87,9 +101,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                     ctypes.POINTER(vp_router_state),
                                     ctypes.POINTER(vp_surrogate_weights), P, ctypes.c_int, P,
                                     ctypes.c_size_t, P]
+    lib.vp_block_workspace_bytes.argtypes = [ctypes.POINTER(vp_shape)]
+    lib.vp_block_workspace_bytes.restype = ctypes.c_size_t
+    lib.vp_block_qkv.argtypes = [ctypes.POINTER(vp_shape), P, P, ctypes.POINTER(vp_block_weights),
+                                 P, P, P, P, ctypes.c_size_t, P]
+    lib.vp_block_out.argtypes = [ctypes.POINTER(vp_shape), P, P, ctypes.POINTER(vp_block_weights),
+                                 P, P, ctypes.c_size_t, P]
     for f in ("vp_router_score", "vp_router_logits", "vp_assign_heads",
               "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
-              "vp_linear_heads"):
+              "vp_linear_heads", "vp_block_qkv", "vp_block_out"):
         getattr(lib, f).restype = ctypes.c_int
     lib.vp_status_string.argtypes = [ctypes.c_int]
     lib.vp_status_string.restype = ctypes.c_char_p
@@ -380,3 +400,100 @@ class RoutedLayer:
             linear_heads(V, self.modes, self.state, x.surr, self.S, self.P, self.Y, self.act,
                          self.surr_variant, Q, K, self.ws)
         return self.Y
+
+
+# ------------------------------------------- dense block around the layer
+
+def block_workspace_bytes(S: int, P: int) -> int:
+    n = load_library().vp_block_workspace_bytes(ctypes.byref(make_shape(S, P, MAX_HEADS,
+                                                                        torch.bfloat16)))
+    if n == 0:
+        raise ValueError("invalid block shape")
+    return int(n)
+
+
+def _block_struct(w: Dict[str, torch.Tensor], eps: float = 0.0, rope_base: float = 0.0):
+    D = MODEL_DIM
+    shapes = {"w_qkv": (3 * D, D), "w_o": (D, D), "w_fc1": (4 * D, D), "w_fc2": (D, 4 * D),
+              "b_qkv": (3 * D,), "b_fc1": (4 * D,)}
+    for k in BLOCK_MATS:
+        _need(w[k], k, shapes[k], torch.bfloat16)
+    for k in BLOCK_VECS:
+        _need(w[k], k, shapes.get(k, (D,)), torch.float32)
+    names = [f[0] for f in vp_block_weights._fields_[:14]]
+    return vp_block_weights(*[w[k].data_ptr() for k in names], float(eps), float(rope_base))
+
+
+def block_qkv(X, pos, w, S: int, P: int, ws: torch.Tensor, Q=None, K=None, V=None):
+    """LN_1, QKV projection and rotary encoding: Q, K, V [N, H, d] bf16."""
+    N = S * P
+    _need(X, "X", (N, MODEL_DIM), torch.bfloat16)
+    _need(pos, "pos", (N, 2), torch.int32)
+    _need(ws, "ws")
+    out = []
+    for t, nm in ((Q, "Q"), (K, "K"), (V, "V")):
+        if t is None:
+            t = torch.empty(N, MAX_HEADS, HEAD_DIM, dtype=torch.bfloat16, device=X.device)
+        _need(t, nm, (N, MAX_HEADS, HEAD_DIM), torch.bfloat16)
+        out.append(t)
+    bw = _block_struct(w)
+    shp = make_shape(S, P, MAX_HEADS, torch.bfloat16)
+    _check(load_library().vp_block_qkv(ctypes.byref(shp), _ptr(X), _ptr(pos), ctypes.byref(bw),
+                                       _ptr(out[0]), _ptr(out[1]), _ptr(out[2]), _ptr(ws),
+                                       ws.numel() * ws.element_size(), _stream()),
+           "vp_block_qkv")
+    return tuple(out)
+
+
+def block_out(X, Y, w, S: int, P: int, ws: torch.Tensor, X_out=None):
+    """W_O, LayerScale, residual, LN_2, FFN, LayerScale, residual: [N, D] bf16."""
+    N = S * P
+    _need(X, "X", (N, MODEL_DIM), torch.bfloat16)
+    _need(Y, "Y")
+    if Y.numel() != N * MODEL_DIM or Y.dtype != torch.bfloat16:
+        raise ValueError("Y must be [N, %d] bf16" % MODEL_DIM)
+    _need(ws, "ws")
+    if X_out is None:
+        X_out = torch.empty_like(X)
+    _need(X_out, "X_out", (N, MODEL_DIM), torch.bfloat16)
+    bw = _block_struct(w)
+    shp = make_shape(S, P, MAX_HEADS, torch.bfloat16)
+    _check(load_library().vp_block_out(ctypes.byref(shp), _ptr(X), _ptr(Y), ctypes.byref(bw),
+                                       _ptr(X_out), _ptr(ws), ws.numel() * ws.element_size(),
+                                       _stream()), "vp_block_out")
+    return X_out
+
+
+class PrimeBlock:
+    """One global-attention block of Algorithm 1 on the GPU: block_qkv, the
+    routed layer on the block's own Q, K, V (router_score, [router_logits],
+    assign_heads, routed_global_attention) and block_out."""
+
+    def __init__(self, layer_inp, block_w: Dict[str, torch.Tensor], pos, device="cuda",
+                 **layer_kw):
+        self.S, self.P = layer_inp.S, layer_inp.P
+        self.w = {k: v.to(device) for k, v in block_w.items()}
+        self.pos = torch.as_tensor(pos, dtype=torch.int32).to(device)
+        self.layer = RoutedLayer(layer_inp, y_dtype=torch.bfloat16, device=device, **layer_kw)
+        self.ws = torch.empty(block_workspace_bytes(self.S, self.P), dtype=torch.uint8,
+                              device=device)
+        x = self.layer.x
+        self.Q, self.K, self.V = x.Q, x.K, x.V   # the layer's own buffers, overwritten
+
+    def step(self, X, X_out=None, events=None):
+        """X [N, D] bf16 -> block output [N, D] bf16.  ``events``: optional
+        list of torch.cuda.Event pairs (qkv, attention, out) to time stages."""
+        ev = events or [None, None, None]
+        def rec(i, j):
+            if ev[i] is not None:
+                ev[i][j].record()
+        rec(0, 0)
+        block_qkv(X, self.pos, self.w, self.S, self.P, self.ws, self.Q, self.K, self.V)
+        rec(0, 1)
+        rec(1, 0)
+        Y = self.layer.step(self.Q, self.K, self.V)
+        rec(1, 1)
+        rec(2, 0)
+        out = block_out(X, Y, self.w, self.S, self.P, self.ws, X_out)
+        rec(2, 1)
+        return out

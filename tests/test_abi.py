@@ -200,3 +200,55 @@ def test_binding_rejects_cpu_tensors():
                         torch.zeros(16, 64, 64, dtype=torch.bfloat16),
                         torch.zeros(16, 64, dtype=torch.bfloat16), 1, 4,
                         torch.zeros(10, dtype=torch.uint8))
+
+
+# ------------------------------------------------------------------ block
+
+def bw(mat=FAKE, vec=FAKE, eps=0.0, base=0.0):
+    f = dict(ln1_w=vec, ln1_b=vec, w_qkv=mat, b_qkv=vec, w_o=mat, b_o=vec, ls1=vec, ln2_w=vec,
+             ln2_b=vec, w_fc1=mat, b_fc1=vec, w_fc2=mat, b_fc2=vec, ls2=vec, ln_eps=eps,
+             rope_base=base)
+    return vp.vp_block_weights(**f)
+
+
+def test_block_workspace_bytes(lib):
+    f = lambda s: lib.vp_block_workspace_bytes(ctypes.byref(s))
+    assert f(shape(dt=vp.VP_F32)) == 0          # bf16 layers only
+    assert f(shape(H=8)) == 0                   # model width 1024 only
+    assert f(shape(S=0)) == 0
+    n = f(shape(S=2, P=1374))
+    assert n >= 2 * 1374 * 1024 * 2 * 6 and n % 256 == 0
+
+
+def call_qkv(lib, shp=None, X=FAKE, pos=FAKE, w=None, Q=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return lib.vp_block_qkv(ctypes.byref(shp or shape()), X, pos, ctypes.byref(w or bw()), Q,
+                            FAKE, FAKE, ws, ws_bytes, None)
+
+
+def call_out(lib, shp=None, X=FAKE, Y=FAKE, w=None, Xo=FAKE, ws=FAKE, ws_bytes=1 << 40):
+    return lib.vp_block_out(ctypes.byref(shp or shape()), X, Y, ctypes.byref(w or bw()), Xo, ws,
+                            ws_bytes, None)
+
+
+def test_block_validation(lib):
+    for call in (call_qkv, call_out):
+        assert call(lib, shp=shape(dt=vp.VP_F32)) == vp.VP_ERR_UNSUPPORTED
+        assert call(lib, shp=shape(H=4)) == vp.VP_ERR_UNSUPPORTED
+        assert call(lib, shp=shape(P=0)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, X=None) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, X=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(mat=None)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(mat=FAKE + 8)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(vec=None)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(vec=FAKE + 2)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(eps=-1.0)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(eps=float("nan"))) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, w=bw(base=0.5)) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, ws=None) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, ws=FAKE + 16) == vp.VP_ERR_INVALID_ARG
+        assert call(lib, ws_bytes=1024) == vp.VP_ERR_WORKSPACE
+    assert call_qkv(lib, pos=None) == vp.VP_ERR_INVALID_ARG
+    assert call_qkv(lib, pos=FAKE + 4) == vp.VP_ERR_INVALID_ARG
+    assert call_qkv(lib, Q=None) == vp.VP_ERR_INVALID_ARG
+    assert call_out(lib, Y=None) == vp.VP_ERR_INVALID_ARG
+    assert call_out(lib, Xo=FAKE + 2) == vp.VP_ERR_INVALID_ARG
