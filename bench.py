@@ -171,6 +171,89 @@ def run_variants(x, steps, warmup):
     return out
 
 
+def block_gemm_flops(N):
+    """Projections of one block: QKV (3D), W_O (D), FFN (4D and back), D = 1024."""
+    Dm = HEADS * D
+    return 2.0 * N * Dm * (3 * Dm + Dm + 4 * Dm + 4 * Dm)
+
+
+def run_block(S, n_full, steps, warmup):
+    """One global block of Algorithm 1 (LN_1, QKV with rotary positions, the
+    routed layer, W_O, LayerScale, LN_2, FFN): per-stage latency from HIP
+    events, and the projections' MFMA roofline."""
+    import torch
+    from paper_2609_23733_amd import synth, vp
+    lay = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=n_full, key=(S, 7), with_qkv=False)
+    blk = vp.PrimeBlock(lay, synth.make_block_weights((S, 7)), synth.token_positions(S, P_TOKENS))
+    X = synth.make_block_input(S, P_TOKENS, key=(S, 7), device="cuda")
+    Xo = torch.empty_like(X)
+    for _ in range(warmup):
+        blk.step(X, Xo)
+    torch.cuda.synchronize()
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(3)] for _ in range(steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for k in range(steps):
+        blk.step(X, Xo, events=evs[k])
+    t1.record()
+    torch.cuda.synchronize()
+    stage = [sum(e[i][0].elapsed_time(e[i][1]) for e in evs) / steps for i in range(3)]
+    N = S * P_TOKENS
+    fl = block_gemm_flops(N)
+    ach = fl / (stage[0] + stage[2]) / 1e9
+    return dict(S=S, N=N, n_full=int((blk.layer.modes == 2).sum()),
+                ms=round(t0.elapsed_time(t1) / steps, 4), qkv_ms=round(stage[0], 4),
+                routed_layer_ms=round(stage[1], 4), out_ms=round(stage[2], 4),
+                roofline={"kernel": "k_gemm (QKV, W_O, FFN) + k_layernorm", "bound": "mfma",
+                          "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                          "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                          "algorithmic_flop_per_launch": fl})
+
+
+def run_stack(S, layers, steps, warmup):
+    """A stack of global blocks with independent seeded weights, layer l + 1
+    taking layer l's output; FULL-head counts drawn from {1, ..., 6} per
+    layer.  Per-layer latency from HIP events around each block."""
+    import numpy as np
+    import torch
+    from paper_2609_23733_amd import synth, vp
+    rng = np.random.Generator(np.random.PCG64(synth.derive_seed(S, 500)))
+    n_full = rng.integers(1, 7, size=layers)
+    sh = vp.PrimeBlock.make_shared(S, P_TOKENS)
+    pos = torch.from_numpy(synth.token_positions(S, P_TOKENS)).cuda()
+    blocks = [vp.PrimeBlock(synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=int(n_full[l]),
+                                             key=(S, 100 + l), with_qkv=False),
+                            synth.make_block_weights((S, 100 + l)), pos, shared=sh)
+              for l in range(layers)]
+    X0 = synth.make_block_input(S, P_TOKENS, key=(S, 100), device="cuda")
+    X = torch.empty_like(X0)
+
+    def once(evs=None):
+        X.copy_(X0)
+        for l, b in enumerate(blocks):
+            if evs is not None:
+                evs[l][0].record()
+            b.step(X, X)
+            if evs is not None:
+                evs[l][1].record()
+    for _ in range(warmup):
+        once()
+    torch.cuda.synchronize()
+    per = np.zeros(layers)
+    for _ in range(steps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(layers)]
+        once(evs)
+        torch.cuda.synchronize()
+        per += [a.elapsed_time(b) for a, b in evs]
+    per /= steps
+    got = [int((b.layer.modes == 2).sum()) for b in blocks]
+    return dict(S=S, N=S * P_TOKENS, layers=layers, n_full=got,
+                per_layer_ms=[round(float(v), 3) for v in per],
+                total_ms=round(float(per.sum()), 3))
+
+
 def cpu_baseline(x, rows_per_head=640):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
@@ -213,6 +296,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--no-block", action="store_true")
+    ap.add_argument("--stack", type=int, default=0, metavar="S",
+                    help="also time a 24-block stack at S views (e.g. 500)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the "
                          "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -240,8 +326,15 @@ def main():
     variants = None
     if not args.no_variants:
         variants = run_variants(x, args.steps, args.warmup)
+    del layer
+    torch.cuda.empty_cache()
+    block = None
+    if not args.no_block:
+        block = run_block(100, args.n_full, args.steps, args.warmup)
+    stack = None
+    if args.stack:
+        stack = run_stack(args.stack, 24, 2, 1)
     if not args.no_sweep:
-        del layer
         for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16), (500, 4)):
             r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 0))
             by.append(r)
@@ -287,6 +380,10 @@ def main():
     }
     if variants is not None:
         out["variants"] = variants
+    if block is not None:
+        out["block"] = block
+    if stack is not None:
+        out["stack"] = stack
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x)
     print(json.dumps(out))

@@ -180,19 +180,23 @@ def make_layer(S: int, P: int = TOKENS_PER_VIEW, dtype: str = "bf16", n_full: in
                n_surr: Optional[int] = None, key: Sequence[int] = (0, 0),
                qkv_device="cpu", sharp: bool = False, H: int = H_HEADS,
                d: int = HEAD_DIM, L: int = HIDDEN,
-               modes: Optional[np.ndarray] = None) -> LayerInputs:
+               modes: Optional[np.ndarray] = None, with_qkv: bool = True) -> LayerInputs:
     """Seeded inputs of one routed global-attention layer.
 
     ``key`` = (workload id, layer index) selects the seed stream.  Q/K/V are
     drawn on ``qkv_device`` (a CUDA device for the large workloads); the small
-    weight tensors are always drawn on the CPU.
+    weight tensors are always drawn on the CPU.  ``with_qkv=False`` leaves
+    Q/K/V empty (a layer inside a block, whose Q/K/V come from the block).
     """
     N = S * P
     sd = lambda name: derive_seed(*key, TENSOR_IDS[name])
     std = 1.0 if sharp else 1.0 / np.sqrt(d)
-    Q = stored(normal((N, H, d), sd("Q"), std, qkv_device), dtype)
-    K = stored(normal((N, H, d), sd("K"), std, qkv_device), dtype)
-    V = stored(normal((N, H, d), sd("V"), 1.0 / np.sqrt(d), qkv_device), dtype)
+    if with_qkv:
+        Q = stored(normal((N, H, d), sd("Q"), std, qkv_device), dtype)
+        K = stored(normal((N, H, d), sd("K"), std, qkv_device), dtype)
+        V = stored(normal((N, H, d), sd("V"), 1.0 / np.sqrt(d), qkv_device), dtype)
+    else:
+        Q = K = V = torch.empty(0, dtype=torch_dtype(dtype))
 
     bw = 1.0 / np.sqrt(d)
     W = stored(uniform((H, L, d), sd("W"), bw), dtype)

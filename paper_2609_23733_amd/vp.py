@@ -357,7 +357,10 @@ class RoutedLayer:
 
     def __init__(self, inp, rule: int = RULE_ARGMAX, y_dtype=None, act: int = ACT_GELU_ERF,
                  tau_low: float = TAU_LOW, tau_high: float = TAU_HIGH, device="cuda",
-                 pool: int = POOL_GATED, surr_variant: int = SURR_EQ7):
+                 pool: int = POOL_GATED, surr_variant: int = SURR_EQ7,
+                 ws: Optional[torch.Tensor] = None, Y: Optional[torch.Tensor] = None):
+        """``ws`` and ``Y`` may be shared by layers that run one after another
+        on one stream (a stack); they are allocated when not given."""
         x = inp.to(device)
         self.x = x
         self.S, self.P, self.H = x.S, x.P, x.H
@@ -365,12 +368,13 @@ class RoutedLayer:
         self.pool, self.surr_variant = pool, surr_variant
         self.tau_low, self.tau_high = tau_low, tau_high
         self.y_dtype = y_dtype if y_dtype is not None else x.Q.dtype
-        self.ws = alloc_workspace(x.S, x.P, x.H, x.Q.dtype, device)
+        self.ws = ws if ws is not None else alloc_workspace(x.S, x.P, x.H, x.Q.dtype, device)
         self.state = RouterState.empty(x.H, device)
         self.logits = torch.empty(x.H, 3, dtype=torch.float32, device=device)
         self.modes = torch.empty(x.H, dtype=torch.uint8, device=device)
         self.buckets = torch.empty(BUCKETS_LEN, dtype=torch.int32, device=device)
-        self.Y = torch.empty(x.N, x.H, HEAD_DIM, dtype=self.y_dtype, device=device)
+        self.Y = Y if Y is not None else torch.empty(x.N, x.H, HEAD_DIM, dtype=self.y_dtype,
+                                                     device=device)
 
     def step(self, Q=None, K=None, V=None, events=None) -> torch.Tensor:
         """One pass of the layer; ``events`` = (start, end) torch.cuda.Events
@@ -470,15 +474,27 @@ class PrimeBlock:
     assign_heads, routed_global_attention) and block_out."""
 
     def __init__(self, layer_inp, block_w: Dict[str, torch.Tensor], pos, device="cuda",
-                 **layer_kw):
+                 shared: Optional[Dict[str, torch.Tensor]] = None, **layer_kw):
+        """``shared``: buffers that blocks run one after another on one stream
+        may share (make_shared()); allocated per block when not given."""
         self.S, self.P = layer_inp.S, layer_inp.P
+        sh = shared if shared is not None else PrimeBlock.make_shared(self.S, self.P, device)
         self.w = {k: v.to(device) for k, v in block_w.items()}
-        self.pos = torch.as_tensor(pos, dtype=torch.int32).to(device)
-        self.layer = RoutedLayer(layer_inp, y_dtype=torch.bfloat16, device=device, **layer_kw)
-        self.ws = torch.empty(block_workspace_bytes(self.S, self.P), dtype=torch.uint8,
-                              device=device)
-        x = self.layer.x
-        self.Q, self.K, self.V = x.Q, x.K, x.V   # the layer's own buffers, overwritten
+        self.pos = pos if isinstance(pos, torch.Tensor) and pos.is_cuda else \
+            torch.as_tensor(pos, dtype=torch.int32).to(device)
+        self.layer = RoutedLayer(layer_inp, y_dtype=torch.bfloat16, device=device,
+                                 ws=sh["layer_ws"], Y=sh["Y"], **layer_kw)
+        self.ws = sh["block_ws"]
+        self.Q, self.K, self.V = sh["Q"], sh["K"], sh["V"]
+
+    @staticmethod
+    def make_shared(S: int, P: int, device="cuda") -> Dict[str, torch.Tensor]:
+        N = S * P
+        e = lambda: torch.empty(N, MAX_HEADS, HEAD_DIM, dtype=torch.bfloat16, device=device)
+        return {"Q": e(), "K": e(), "V": e(), "Y": e(),
+                "layer_ws": alloc_workspace(S, P, MAX_HEADS, torch.bfloat16, device),
+                "block_ws": torch.empty(block_workspace_bytes(S, P), dtype=torch.uint8,
+                                        device=device)}
 
     def step(self, X, X_out=None, events=None):
         """X [N, D] bf16 -> block output [N, D] bf16.  ``events``: optional
