@@ -76,6 +76,7 @@ def _load():
             lib.or_layernorm.argtypes = [P, i64, i32, P, P, dbl, P, i32]
             lib.or_rope2d.argtypes = [P, i64, i32, i32, P, dbl, i32]
             lib.or_gelu.argtypes = [P, i64]
+            lib.or_attention_colmax.argtypes = [P, P, i64, i32, i32, i32, dbl, P, i64, P, i32]
             lib.or_threads_used.argtypes = [i32]
             lib.or_threads_used.restype = i32
             _lib = lib
@@ -351,3 +352,52 @@ def block_out(X, Y, wt, eps=LN_EPS, nthreads=0):
     Z = layernorm(Xa, wt["ln2_w"], wt["ln2_b"], eps, nthreads)
     F = linear(gelu(linear(Z, wt["w_fc1"], wt["b_fc1"])), wt["w_fc2"], wt["b_fc2"])
     return Xa + as_f32(wt["ls2"]).astype(np.float64) * F, Xa
+
+
+# ------------------------------------------ distillation targets and losses
+
+def attention_colmax(Q, K, h, keys=None, scale=None, nthreads=0):
+    """Eq.8: p^T_{h,k} = max over queries q of the teacher's post-softmax
+    attention A_{h,k,q} (every query attends all N keys).  Returns [N] (or the
+    listed keys) float64."""
+    Q, K = as_f32(Q), as_f32(K)
+    N, H, d = Q.shape
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    if keys is None:
+        nk, kp = N, None
+    else:
+        kp = np.ascontiguousarray(keys, dtype=np.int64)
+        nk = kp.shape[0]
+    p = np.zeros(nk, np.float64)
+    _load().or_attention_colmax(_p(Q), _p(K), N, H, d, int(h), float(scale), _p(kp), nk, _p(p),
+                                _nt(nthreads))
+    return p
+
+
+def teacher_delta_rows(Q, K, V, h, rows=None, nthreads=0):
+    """Eq.10: Delta^T_h = (A_h - I) V_h on the given rows: softmax attention of
+    the rows minus their own values.  [R, d] float64."""
+    Y = full_rows(Q, K, V, h, rows, None, nthreads)
+    Vh = as_f32(V)[:, h, :].astype(np.float64)
+    return Y - (Vh if rows is None else Vh[np.asarray(rows)])
+
+
+def router_loss(p, r, lam=1.0):
+    """Eq.9 for one head: KL(p_bar || r_bar) + lam |max p - max r|, with p_bar
+    and r_bar the key distributions p / sum p and r / sum r (0 log 0 = 0)."""
+    p = np.asarray(p, np.float64)
+    r = np.asarray(r, np.float64)
+    pb, rb = p / p.sum(), r / r.sum()
+    nz = pb > 0
+    kl = float(np.sum(pb[nz] * (np.log(pb[nz]) - np.log(rb[nz]))))
+    return kl + lam * abs(float(p.max()) - float(r.max()))
+
+
+def latent_loss(dhat, dT, lam=1.0):
+    """Eq.11 for one head: ||dhat - dT||_2 + lam (1 - cos(dhat, dT)), the norm and
+    the cosine taken over all N x d entries."""
+    a = np.asarray(dhat, np.float64).ravel()
+    b = np.asarray(dT, np.float64).ravel()
+    cos = float(a @ b) / (np.sqrt(float(a @ a)) * np.sqrt(float(b @ b)))
+    return float(np.sqrt(float((a - b) @ (a - b)))) + lam * (1.0 - cos)

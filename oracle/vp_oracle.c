@@ -520,3 +520,67 @@ void or_rope2d(double *T, int64_t N, int H, int d, const int32_t *pos, double ba
 void or_gelu(double *X, int64_t n) {
     for (int64_t i = 0; i < n; ++i) X[i] = 0.5 * X[i] * (1.0 + erf(X[i] / sqrt(2.0)));
 }
+
+/* ------------------------------------------- distillation targets (Eq.8) */
+/*
+ * Teacher attention of head h with every query attending all N keys:
+ * A[k][q] = exp(l_qk - m_q) / sum_k' exp(l_qk' - m_q), l_qk = scale q_q . k_k,
+ * m_q = max_k l_qk.  Eq.8 max-pools it over queries: p[k] = max_q A[k][q].
+ * Pass 1 (independent queries): m_q and the row sum s_q.  Pass 2 (independent
+ * keys; all keys, or the listed ones): the maximum over every query.
+ */
+typedef struct {
+    const float *Q, *K;
+    int64_t N;
+    int H, d, h;
+    double scale;
+    double *m, *s;
+    const int64_t *keys;
+    double *p;
+} colmax_ctx;
+
+static double qk_dot(const colmax_ctx *c, int64_t q, int64_t k) {
+    const float *a = c->Q + (q * c->H + c->h) * (int64_t)c->d;
+    const float *b = c->K + (k * c->H + c->h) * (int64_t)c->d;
+    double dot = 0.0;
+    for (int e = 0; e < c->d; ++e) dot += (double)a[e] * (double)b[e];
+    return dot * c->scale;
+}
+
+static void rowstat_body(void *p, int64_t lo, int64_t hi) {
+    colmax_ctx *c = (colmax_ctx *)p;
+    for (int64_t q = lo; q < hi; ++q) {
+        double m = -INFINITY;
+        for (int64_t k = 0; k < c->N; ++k) {
+            const double l = qk_dot(c, q, k);
+            if (l > m) m = l;
+        }
+        double s = 0.0;
+        for (int64_t k = 0; k < c->N; ++k) s += exp(qk_dot(c, q, k) - m);
+        c->m[q] = m;
+        c->s[q] = s;
+    }
+}
+
+static void colmax_body(void *p, int64_t lo, int64_t hi) {
+    colmax_ctx *c = (colmax_ctx *)p;
+    for (int64_t i = lo; i < hi; ++i) {
+        const int64_t k = c->keys ? c->keys[i] : i;
+        double best = 0.0;
+        for (int64_t q = 0; q < c->N; ++q) {
+            const double a = exp(qk_dot(c, q, k) - c->m[q]) / c->s[q];
+            if (a > best) best = a;
+        }
+        c->p[i] = best;
+    }
+}
+
+void or_attention_colmax(const float *Q, const float *K, int64_t N, int H, int d, int h,
+                         double scale, const int64_t *keys, int64_t nkeys, double *p,
+                         int nthreads) {
+    double *m = (double *)malloc(sizeof(double) * 2 * (N > 0 ? N : 1));
+    colmax_ctx c = {Q, K, N, H, d, h, scale, m, m + N, keys, p};
+    or_parallel_for(N, nthreads, rowstat_body, &c);
+    or_parallel_for(keys ? nkeys : N, nthreads, colmax_body, &c);
+    free(m);
+}

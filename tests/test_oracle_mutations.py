@@ -60,8 +60,17 @@ MUTANTS = {
     "block_gelu_tanh_form": ("X[i] = 0.5 * X[i] * (1.0 + erf(X[i] / sqrt(2.0)));",
                              "X[i] = 0.5 * X[i] * (1.0 + tanh(0.7978845608 * (X[i] + 0.044715 * X[i] * X[i] * X[i])));",
                              "block"),
+    # distillation targets (pins in test_oracle_distill_pins.py)
+    "colmax_key_stat": ("const double a = exp(qk_dot(c, q, k) - c->m[q]) / c->s[q];",
+                        "const double a = exp(qk_dot(c, q, k) - c->m[k]) / c->s[k];", "distill"),
+    "colmax_unnormalised": ("const double a = exp(qk_dot(c, q, k) - c->m[q]) / c->s[q];",
+                            "const double a = exp(qk_dot(c, q, k) - c->m[q]);", "distill"),
+    "colmax_scale_dropped": ("    return dot * c->scale;\n}", "    return dot;\n}", "distill"),
+    "colmax_sum_not_max": ("            if (a > best) best = a;", "            best += a / (double)c->N;",
+                           "distill"),
 }
-PIN_FILES = {"layer": "test_oracle_pins.py", "block": "test_oracle_block_pins.py"}
+PIN_FILES = {"layer": "test_oracle_pins.py", "block": "test_oracle_block_pins.py",
+             "distill": "test_oracle_distill_pins.py"}
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
