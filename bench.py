@@ -254,6 +254,47 @@ def run_stack(S, layers, steps, warmup):
                 total_ms=round(float(per.sum()), 3))
 
 
+def run_teacher(S, steps, warmup):
+    """Distillation targets of a teacher layer (every head FULL; Eq.8, Eq.10)
+    and the two losses (Eq.9, Eq.11) on the same inputs: HIP-event latency
+    and the MFMA work: 2 N^2 d (row statistics) + 2 N^2 d (column maxima) +
+    4 N^2 d (attention for Delta^T) per head."""
+    import torch
+    from paper_2609_23733_amd import synth, vp
+    x = synth.make_layer(S, P_TOKENS, dtype="bf16", key=(S, 9), qkv_device="cuda")
+    Q, K, V = x.Q, x.K, x.V
+    N = S * P_TOKENS
+    shp = vp.make_shape(S, P_TOKENS, HEADS, torch.bfloat16)
+    import ctypes
+    ws = torch.empty(vp.load_library().vp_teacher_workspace_bytes(ctypes.byref(shp)),
+                     dtype=torch.uint8, device="cuda")
+    lws = vp.alloc_workspace(S, P_TOKENS, HEADS, torch.bfloat16)
+    st = vp.router_score(Q, K, V, x.W.cuda(), x.U.cuda(), x.w.cuda(), S, P_TOKENS, lws)
+
+    def timed(f):
+        for _ in range(warmup):
+            f()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            out = f()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps, out
+    t_ms, (colmax, smax, delta) = timed(lambda: vp.teacher_targets(Q, K, V, S, P_TOKENS, ws=ws))
+    r_ms, _ = timed(lambda: vp.router_loss(K, st, colmax, smax, S, P_TOKENS))
+    l_ms, _ = timed(lambda: vp.latent_loss(delta, delta, S, P_TOKENS))
+    fl = 8.0 * N * N * D * HEADS
+    ach = fl / t_ms / 1e9
+    return dict(S=S, N=N, heads=HEADS, teacher_targets_ms=round(t_ms, 3),
+                router_loss_ms=round(r_ms, 4), latent_loss_ms=round(l_ms, 4),
+                roofline={"kernel": "k_rowstats + k_colmax + FULL-head kernels + k_sub_v",
+                          "bound": "mfma", "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS,
+                          "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                          "algorithmic_flop_per_launch": fl})
+
+
 def cpu_baseline(x, rows_per_head=640):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
@@ -297,6 +338,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--no-block", action="store_true")
+    ap.add_argument("--no-teacher", action="store_true")
     ap.add_argument("--stack", type=int, default=0, metavar="S",
                     help="also time a 24-block stack at S views (e.g. 500)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -331,6 +373,10 @@ def main():
     block = None
     if not args.no_block:
         block = run_block(100, args.n_full, args.steps, args.warmup)
+    teacher = None
+    if not args.no_teacher:
+        teacher = run_teacher(100, max(2, args.steps // 4), 1)
+        torch.cuda.empty_cache()
     stack = None
     if args.stack:
         stack = run_stack(args.stack, 24, 2, 1)
@@ -382,6 +428,8 @@ def main():
         out["variants"] = variants
     if block is not None:
         out["block"] = block
+    if teacher is not None:
+        out["teacher"] = teacher
     if stack is not None:
         out["stack"] = stack
     if not args.no_cpu_baseline:

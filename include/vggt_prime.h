@@ -263,6 +263,39 @@ vp_status vp_block_out(const vp_shape *shape, const void *X, const void *Y,
                        const vp_block_weights *w, void *X_out, void *ws, size_t ws_bytes,
                        void *stream);
 
+/* ---------------------------------------------------------------------------
+ * Distillation targets and losses (Section 4.4, Eq.8-11), bf16 layers.  The
+ * teacher is the layer with every head running exact softmax attention,
+ * A_h = softmax over keys of Q_h K_h^T / sqrt(d) (every query attends all N
+ * tokens), written here A_h[k][q].
+ *   vp_teacher_targets writes
+ *     colmax [H, N] fp32  p^T_{h,k} = max_q A_h[k][q]            (Eq.8)
+ *     smax   [H]    fp32  s^attn_h = max_{k,q} A_h[k][q] = max_k p^T_{h,k}
+ *     delta  [N, H, d]    Delta^T_h = (A_h - I) V_h in y_dtype     (Eq.10)
+ *   (two passes over all query-key pairs for colmax, the FULL-head kernels
+ *   for delta; arithmetic in fp32, one rounding of delta).
+ *   vp_router_loss: per head, Eq.9 with p_bar = colmax / sum_k colmax and
+ *     r_bar = r_h, the routing vector of `state` (vp_router_score of the same
+ *     K with the same `scale`, 1/sqrt(d) when 0):
+ *     loss[h] = KL(p_bar || r_bar) + lambda |smax[h] - max_k r_h(k)|.
+ *   vp_latent_loss: per head, Eq.11 over the head's N x d entries:
+ *     loss[h] = ||D_hat - D^T||_2 + lambda (1 - cos(D_hat, D^T)); D_hat, D^T
+ *     [N, H, d] in `dtype`.
+ * Workspaces: vp_teacher_workspace_bytes(shape) for the targets (it includes
+ * the routed layer's), vp_loss_workspace_bytes(shape) for either loss.  The
+ * losses are deterministic (fixed-order sums). */
+size_t vp_teacher_workspace_bytes(const vp_shape *shape);
+size_t vp_loss_workspace_bytes(const vp_shape *shape);
+vp_status vp_teacher_targets(const vp_shape *shape, const void *Q, const void *K, const void *V,
+                             float *colmax, float *smax, void *delta, vp_dtype y_dtype,
+                             void *ws, size_t ws_bytes, void *stream);
+vp_status vp_router_loss(const vp_shape *shape, const void *K, const vp_router_state *state,
+                         float scale, const float *colmax, const float *smax, float lambda,
+                         float *loss, void *ws, size_t ws_bytes, void *stream);
+vp_status vp_latent_loss(const vp_shape *shape, const void *D_hat, const void *D_t,
+                         vp_dtype dtype, float lambda, float *loss, void *ws, size_t ws_bytes,
+                         void *stream);
+
 /* Static description of a status code. */
 const char *vp_status_string(vp_status s);
 

@@ -549,17 +549,19 @@ static double qk_dot(const colmax_ctx *c, int64_t q, int64_t k) {
 
 static void rowstat_body(void *p, int64_t lo, int64_t hi) {
     colmax_ctx *c = (colmax_ctx *)p;
+    double *row = (double *)malloc(sizeof(double) * (c->N > 0 ? c->N : 1));
     for (int64_t q = lo; q < hi; ++q) {
         double m = -INFINITY;
         for (int64_t k = 0; k < c->N; ++k) {
-            const double l = qk_dot(c, q, k);
-            if (l > m) m = l;
+            row[k] = qk_dot(c, q, k);
+            if (row[k] > m) m = row[k];
         }
         double s = 0.0;
-        for (int64_t k = 0; k < c->N; ++k) s += exp(qk_dot(c, q, k) - m);
+        for (int64_t k = 0; k < c->N; ++k) s += exp(row[k] - m);
         c->m[q] = m;
         c->s[q] = s;
     }
+    free(row);
 }
 
 static void colmax_body(void *p, int64_t lo, int64_t hi) {

@@ -439,4 +439,127 @@ vp_status vp_block_out(const vp_shape* shape, const void* X, const void* Y,
     return hip_status("vp_block_out");
 }
 
+// ------------------------------------------- distillation targets and losses
+
+namespace {
+
+struct TeacherLayout {
+    Layout attn;
+    size_t off_off, off_y, off_buckets, total;
+};
+
+bool teacher_layout(const vp_shape* s, TeacherLayout* T) {
+    if (!make_layout(s, &T->attn) || s->dtype != VP_BF16) return false;
+    const size_t N = (size_t)T->attn.N, H = (size_t)s->H;
+    size_t off = T->attn.total;
+    T->off_off = off;
+    off = align_up(off + H * N * sizeof(float));
+    T->off_y = off;
+    off = align_up(off + N * H * VP_HEAD_DIM * sizeof(float));
+    T->off_buckets = off;
+    off = align_up(off + VP_BUCKETS_LEN * sizeof(int32_t));
+    T->total = off;
+    return true;
+}
+
+}  // namespace
+
+size_t vp_teacher_workspace_bytes(const vp_shape* shape) {
+    TeacherLayout T;
+    if (shape_status(shape) != VP_OK || !teacher_layout(shape, &T)) return 0;
+    return T.total;
+}
+
+size_t vp_loss_workspace_bytes(const vp_shape* shape) {
+    if (shape_status(shape) != VP_OK) return 0;
+    return align_up(vp::distill_part_bytes(shape->H));
+}
+
+vp_status vp_teacher_targets(const vp_shape* shape, const void* Q, const void* K, const void* V,
+                             float* colmax, float* smax, void* delta, vp_dtype y_dtype, void* ws,
+                             size_t ws_bytes, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (shape->dtype != VP_BF16) return VP_ERR_UNSUPPORTED;
+    if (!Q || !K || !V || !colmax || !smax || !delta || !aligned16(Q) || !aligned16(K) ||
+        !aligned16(V) || !aligned16(delta) || ((uintptr_t)colmax & 3u) || ((uintptr_t)smax & 3u))
+        return VP_ERR_INVALID_ARG;
+    if (y_dtype != VP_F32 && y_dtype != VP_BF16) return VP_ERR_INVALID_ARG;
+    TeacherLayout T;
+    teacher_layout(shape, &T);
+    if (!ws || ((uintptr_t)ws & (kAlign - 1))) return VP_ERR_INVALID_ARG;
+    if (ws_bytes < T.total) return VP_ERR_WORKSPACE;
+    char* w = (char*)ws;
+    vp::TeacherArgs a;
+    int32_t* buckets = (int32_t*)(w + T.off_buckets);
+    a.attn = attn_args(shape, T.attn, Q, K, V, nullptr, buckets, w + T.off_y, VP_F32, ws);
+    a.off = (float*)(w + T.off_off);
+    a.colmax = colmax;
+    a.smax = smax;
+    a.delta = delta;
+    a.delta_dt = y_dtype == VP_BF16 ? 1 : 0;
+    (void)hipGetLastError();
+    vp::launch_teacher_targets(a, (hipStream_t)stream);
+    return hip_status("vp_teacher_targets");
+}
+
+vp_status vp_router_loss(const vp_shape* shape, const void* K, const vp_router_state* state,
+                         float scale, const float* colmax, const float* smax, float lambda,
+                         float* loss, void* ws, size_t ws_bytes, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (shape->dtype != VP_BF16) return VP_ERR_UNSUPPORTED;
+    if (!K || !aligned16(K) || !state || !state->q_pool || !state->stats || !colmax || !smax ||
+        !loss || ((uintptr_t)state->q_pool & 3u) || ((uintptr_t)state->stats & 3u) ||
+        ((uintptr_t)colmax & 3u) || ((uintptr_t)smax & 3u) || ((uintptr_t)loss & 3u))
+        return VP_ERR_INVALID_ARG;
+    if (!isfinite(scale) || scale < 0.f || !isfinite(lambda)) return VP_ERR_INVALID_ARG;
+    if (!ws || ((uintptr_t)ws & (kAlign - 1))) return VP_ERR_INVALID_ARG;
+    if (ws_bytes < vp_loss_workspace_bytes(shape)) return VP_ERR_WORKSPACE;
+    vp::LossArgs a;
+    memset(&a, 0, sizeof(a));
+    a.dtype = 1;
+    a.A = K;
+    a.q_pool = state->q_pool;
+    a.stats = state->stats;
+    a.colmax = colmax;
+    a.smax = smax;
+    a.scale = scale > 0.f ? scale : 1.f / sqrtf((float)shape->d);
+    a.lambda = lambda;
+    a.N = shape->S * shape->P;
+    a.H = shape->H;
+    a.part = (float*)ws;
+    a.loss = loss;
+    (void)hipGetLastError();
+    vp::launch_router_loss(a, (hipStream_t)stream);
+    return hip_status("vp_router_loss");
+}
+
+vp_status vp_latent_loss(const vp_shape* shape, const void* D_hat, const void* D_t,
+                         vp_dtype dtype, float lambda, float* loss, void* ws, size_t ws_bytes,
+                         void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (dtype != VP_F32 && dtype != VP_BF16) return VP_ERR_INVALID_ARG;
+    if (!D_hat || !D_t || !loss || !aligned16(D_hat) || !aligned16(D_t) ||
+        ((uintptr_t)loss & 3u))
+        return VP_ERR_INVALID_ARG;
+    if (!isfinite(lambda)) return VP_ERR_INVALID_ARG;
+    if (!ws || ((uintptr_t)ws & (kAlign - 1))) return VP_ERR_INVALID_ARG;
+    if (ws_bytes < vp_loss_workspace_bytes(shape)) return VP_ERR_WORKSPACE;
+    vp::LossArgs a;
+    memset(&a, 0, sizeof(a));
+    a.dtype = dtype == VP_BF16 ? 1 : 0;
+    a.A = D_hat;
+    a.B = D_t;
+    a.lambda = lambda;
+    a.N = shape->S * shape->P;
+    a.H = shape->H;
+    a.part = (float*)ws;
+    a.loss = loss;
+    (void)hipGetLastError();
+    vp::launch_latent_loss(a, (hipStream_t)stream);
+    return hip_status("vp_latent_loss");
+}
+
 }  // extern "C"

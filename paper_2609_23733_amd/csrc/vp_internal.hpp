@@ -68,6 +68,30 @@ struct BlockArgs {
 
 void launch_block_qkv(const BlockArgs& a, hipStream_t st);
 void launch_block_out(const BlockArgs& a, hipStream_t st);
+// Distillation targets and losses (bf16 layers).
+struct TeacherArgs {
+    AttnArgs attn;        // every head FULL; Y = fp32 workspace, buckets in the workspace
+    float* off;           // [H, N] per-query softmax offsets (log2 units)
+    float* colmax;        // [H, N]
+    float* smax;          // [H]
+    void* delta;          // [N, H, d]
+    int delta_dt;
+};
+struct LossArgs {
+    int dtype;
+    const void *A, *B;    // router loss: A = K; latent loss: A = D_hat, B = D^T
+    const float *q_pool, *stats, *colmax, *smax;
+    float scale, lambda;
+    int64_t N;
+    int H;
+    float* part;          // partial sums (distill_part_bytes)
+    float* loss;          // [H]
+};
+void launch_teacher_targets(const TeacherArgs& a, hipStream_t st);
+void launch_router_loss(const LossArgs& a, hipStream_t st);
+void launch_latent_loss(const LossArgs& a, hipStream_t st);
+size_t distill_part_bytes(int H);
+
 void launch_router(const RouterArgs& a, hipStream_t st);
 void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,
                           int dtype, float* logits, hipStream_t st);

@@ -31,7 +31,8 @@ TAU_LOW, TAU_HIGH = 0.01, 0.20
 EXPORTS = ("vp_workspace_bytes", "vp_router_score", "vp_router_logits", "vp_assign_heads",
            "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
            "vp_linear_heads", "vp_status_string", "vp_last_error", "vp_block_workspace_bytes",
-           "vp_block_qkv", "vp_block_out")
+           "vp_block_qkv", "vp_block_out", "vp_teacher_workspace_bytes", "vp_loss_workspace_bytes",
+           "vp_teacher_targets", "vp_router_loss", "vp_latent_loss")
 MODEL_DIM = MAX_HEADS * HEAD_DIM
 BLOCK_VECS = ("ln1_w", "ln1_b", "b_qkv", "b_o", "ls1", "ln2_w", "ln2_b", "b_fc1", "b_fc2", "ls2")
 BLOCK_MATS = ("w_qkv", "w_o", "w_fc1", "w_fc2")
@@ -107,9 +108,19 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                  P, P, P, P, ctypes.c_size_t, P]
     lib.vp_block_out.argtypes = [ctypes.POINTER(vp_shape), P, P, ctypes.POINTER(vp_block_weights),
                                  P, P, ctypes.c_size_t, P]
+    for f in ("vp_teacher_workspace_bytes", "vp_loss_workspace_bytes"):
+        getattr(lib, f).argtypes = [ctypes.POINTER(vp_shape)]
+        getattr(lib, f).restype = ctypes.c_size_t
+    lib.vp_teacher_targets.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P, P, ctypes.c_int,
+                                       P, ctypes.c_size_t, P]
+    lib.vp_router_loss.argtypes = [ctypes.POINTER(vp_shape), P, ctypes.POINTER(vp_router_state),
+                                   f32, P, P, f32, P, P, ctypes.c_size_t, P]
+    lib.vp_latent_loss.argtypes = [ctypes.POINTER(vp_shape), P, P, ctypes.c_int, f32, P, P,
+                                   ctypes.c_size_t, P]
     for f in ("vp_router_score", "vp_router_logits", "vp_assign_heads",
               "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
-              "vp_linear_heads", "vp_block_qkv", "vp_block_out"):
+              "vp_linear_heads", "vp_block_qkv", "vp_block_out", "vp_teacher_targets",
+              "vp_router_loss", "vp_latent_loss"):
         getattr(lib, f).restype = ctypes.c_int
     lib.vp_status_string.argtypes = [ctypes.c_int]
     lib.vp_status_string.restype = ctypes.c_char_p
@@ -513,3 +524,63 @@ class PrimeBlock:
         out = block_out(X, Y, self.w, self.S, self.P, self.ws, X_out)
         rec(2, 1)
         return out
+
+
+# ------------------------------------------- distillation targets and losses
+
+def teacher_targets(Q, K, V, S: int, P: int, y_dtype=torch.bfloat16, ws=None):
+    """Eq.8 and Eq.10 of the teacher (every head FULL): (colmax [H, N] fp32,
+    smax [H] fp32, delta [N, H, d] y_dtype)."""
+    N, H = _qkv(Q, K, V, S, P)
+    shp = make_shape(S, P, H, Q.dtype)
+    lib = load_library()
+    if ws is None:
+        n = lib.vp_teacher_workspace_bytes(ctypes.byref(shp))
+        if n == 0:
+            raise ValueError("teacher targets need a bf16 layer")
+        ws = torch.empty(n, dtype=torch.uint8, device=Q.device)
+    colmax = torch.empty(H, N, dtype=torch.float32, device=Q.device)
+    smax = torch.empty(H, dtype=torch.float32, device=Q.device)
+    delta = torch.empty(N, H, HEAD_DIM, dtype=y_dtype, device=Q.device)
+    _check(lib.vp_teacher_targets(ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V), _ptr(colmax),
+                                  _ptr(smax), _ptr(delta), _dt(delta), _ptr(ws),
+                                  ws.numel() * ws.element_size(), _stream()),
+           "vp_teacher_targets")
+    return colmax, smax, delta
+
+
+def _loss_ws(shp, device):
+    n = load_library().vp_loss_workspace_bytes(ctypes.byref(shp))
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def router_loss(K, state: RouterState, colmax, smax, S: int, P: int, lam: float = 1.0,
+                scale: float = 0.0):
+    """Eq.9 per head: [H] fp32."""
+    N, H = S * P, K.shape[1]
+    _need(K, "K", (N, H, HEAD_DIM), torch.bfloat16)
+    _need(colmax, "colmax", (H, N), torch.float32)
+    _need(smax, "smax", (H,), torch.float32)
+    shp = make_shape(S, P, H, K.dtype)
+    ws = _loss_ws(shp, K.device)
+    loss = torch.empty(H, dtype=torch.float32, device=K.device)
+    st = state.c()
+    _check(load_library().vp_router_loss(ctypes.byref(shp), _ptr(K), ctypes.byref(st),
+                                         float(scale), _ptr(colmax), _ptr(smax), float(lam),
+                                         _ptr(loss), _ptr(ws), ws.numel(), _stream()),
+           "vp_router_loss")
+    return loss
+
+
+def latent_loss(D_hat, D_t, S: int, P: int, lam: float = 1.0):
+    """Eq.11 per head: [H] fp32."""
+    N, H = S * P, D_hat.shape[1]
+    _need(D_hat, "D_hat", (N, H, HEAD_DIM))
+    _need(D_t, "D_t", (N, H, HEAD_DIM), D_hat.dtype)
+    shp = make_shape(S, P, H, D_hat.dtype)
+    ws = _loss_ws(shp, D_hat.device)
+    loss = torch.empty(H, dtype=torch.float32, device=D_hat.device)
+    _check(load_library().vp_latent_loss(ctypes.byref(shp), _ptr(D_hat), _ptr(D_t), _dt(D_hat),
+                                         float(lam), _ptr(loss), _ptr(ws), ws.numel(),
+                                         _stream()), "vp_latent_loss")
+    return loss

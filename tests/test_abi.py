@@ -252,3 +252,36 @@ def test_block_validation(lib):
     assert call_qkv(lib, Q=None) == vp.VP_ERR_INVALID_ARG
     assert call_out(lib, Y=None) == vp.VP_ERR_INVALID_ARG
     assert call_out(lib, Xo=FAKE + 2) == vp.VP_ERR_INVALID_ARG
+
+
+# ------------------------------------------------------- distillation
+
+def test_distill_validation(lib):
+    f = lambda s: lib.vp_teacher_workspace_bytes(ctypes.byref(s))
+    assert f(shape(dt=vp.VP_F32)) == 0 and f(shape()) > lib.vp_workspace_bytes(ctypes.byref(shape()))
+    assert lib.vp_loss_workspace_bytes(ctypes.byref(shape())) > 0
+    tt = lambda shp=None, Q=FAKE, cm=FAKE, ydt=vp.VP_BF16, ws=FAKE, nb=1 << 40: \
+        lib.vp_teacher_targets(ctypes.byref(shp or shape()), Q, FAKE, FAKE, cm, FAKE, FAKE, ydt,
+                               ws, nb, None)
+    assert tt(shp=shape(dt=vp.VP_F32)) == vp.VP_ERR_UNSUPPORTED
+    assert tt(Q=None) == vp.VP_ERR_INVALID_ARG
+    assert tt(cm=FAKE + 2) == vp.VP_ERR_INVALID_ARG
+    assert tt(ydt=4) == vp.VP_ERR_INVALID_ARG
+    assert tt(ws=None) == vp.VP_ERR_INVALID_ARG
+    assert tt(nb=100) == vp.VP_ERR_WORKSPACE
+    rl = lambda K=FAKE, st=None, scale=0.0, lam=1.0, nb=1 << 40: \
+        lib.vp_router_loss(ctypes.byref(shape()), K, st if st is not None else ctypes.byref(rs()),
+                           scale, FAKE, FAKE, lam, FAKE, FAKE, nb, None)
+    assert rl(K=None) == vp.VP_ERR_INVALID_ARG
+    assert rl(scale=-1.0) == vp.VP_ERR_INVALID_ARG
+    assert rl(lam=float("inf")) == vp.VP_ERR_INVALID_ARG
+    assert rl(nb=16) == vp.VP_ERR_WORKSPACE
+    assert lib.vp_router_loss(ctypes.byref(shape()), FAKE, None, 0.0, FAKE, FAKE, 1.0, FAKE,
+                              FAKE, 1 << 40, None) == vp.VP_ERR_INVALID_ARG
+    ll = lambda A=FAKE, dt=vp.VP_BF16, lam=1.0, nb=1 << 40: \
+        lib.vp_latent_loss(ctypes.byref(shape()), A, FAKE, dt, lam, FAKE, FAKE, nb, None)
+    assert ll(A=None) == vp.VP_ERR_INVALID_ARG
+    assert ll(A=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+    assert ll(dt=3) == vp.VP_ERR_INVALID_ARG
+    assert ll(lam=float("nan")) == vp.VP_ERR_INVALID_ARG
+    assert ll(nb=16) == vp.VP_ERR_WORKSPACE

@@ -1,0 +1,125 @@
+"""GPU parity of the distillation targets and losses (Section 4.4, Eq.8-11)
+against the fp64 oracle, through the C ABI.
+
+Bars (derived from the arithmetic; the paper states none for these):
+  - column maxima p^T and s^attn: |err| <= 1e-4 |ref| + 1e-9 (bf16 products
+    are exact in fp32; the logit, the per-query log-sum and one exp2 are fp32);
+  - Delta^T = (A - I) V: the layer's attention bar on its A V part,
+    |err| <= 2e-2 RMS(A V), with fp32 output (with bf16 output, as at S = 32,
+    plus the output's half-ulp 2^-8 |ref|, which alone can use the whole
+    term since Delta is dominated by -V);
+  - router loss (Eq.9): |err| <= 1e-3 |ref| + 1e-5, every input computed on
+    each side from the same seeded Q, K, V and router weights;
+  - latent loss (Eq.11): |err| <= 1e-4 |ref|.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_23733_amd import synth
+from test_gpu_parity import log, rms
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_23733_amd import vp
+    vp.load_library()
+
+
+def check_colmax(g, r, label):
+    err = np.abs(g - r)
+    bound = 1e-4 * np.abs(r) + 1e-9
+    ratio = float((err / bound).max())
+    log("%s colmax worst err/bound = %.3f" % (label, ratio))
+    assert (err <= bound).all(), (label, float(err.max()), ratio)
+
+
+def check_delta(g, r, av, label, y_bf16=False):
+    bound = 2e-2 * rms(av) + (2.0 ** -8 * np.abs(r) if y_bf16 else 0.0)
+    err = np.abs(g - r)
+    ratio = float((err / bound).max())
+    log("%s delta worst err/bound = %.3f" % (label, ratio))
+    assert (err <= bound).all(), (label, float(err.max()), ratio)
+
+
+@pytest.mark.parametrize("P,sharp", [(1, False), (65, True), (300, False), (1000, True)])
+def test_teacher_targets(P, sharp):
+    from paper_2609_23733_amd import vp
+    log("teacher targets P=%d sharp=%d" % (P, sharp))
+    x = synth.make_layer(1, P, dtype="bf16", key=(30, P), sharp=sharp)
+    colmax, smax, delta = vp.teacher_targets(x.Q.cuda(), x.K.cuda(), x.V.cuda(), 1, P,
+                                             y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    cm, sm, dl = colmax.cpu().numpy(), smax.cpu().numpy(), delta.double().cpu().numpy()
+    for h in range(16):
+        ref = oracle.attention_colmax(x.Q, x.K, h)
+        check_colmax(cm[h], ref, "P=%d h=%d" % (P, h))
+        check_colmax(sm[h:h + 1], ref.max(keepdims=True), "P=%d h=%d smax" % (P, h))
+        d_ref = oracle.teacher_delta_rows(x.Q, x.K, x.V, h)
+        av = d_ref + x.V[:, h, :].double().numpy()
+        check_delta(dl[:, h, :], d_ref, av, "P=%d h=%d" % (P, h))
+
+
+def test_teacher_targets_s32_sampled():
+    """S = 32 views (N = 43,968): the column maxima of 64 sampled keys of two
+    heads (the oracle still visits every query) and Delta^T on 64 sampled rows."""
+    from paper_2609_23733_amd import vp
+    S = 32
+    log("teacher targets S=32")
+    x = synth.make_layer(S, dtype="bf16", key=(31, 0), qkv_device="cuda")
+    colmax, smax, delta = vp.teacher_targets(x.Q, x.K, x.V, S, synth.TOKENS_PER_VIEW)
+    torch.cuda.synchronize()
+    N = x.N
+    keys = synth.sample_rows(N, 64, synth.derive_seed(31, 0, 20))
+    Qc, Kc, Vc = x.Q.cpu(), x.K.cpu(), x.V.cpu()
+    cm = colmax.cpu().numpy()
+    for h in (3, 11):
+        ref = oracle.attention_colmax(Qc, Kc, h, keys=keys)
+        check_colmax(cm[h][keys], ref, "S=32 h=%d" % h)
+        assert smax[h].item() >= cm[h].max() - 1e-12 and smax[h].item() >= ref.max() * (1 - 1e-4)
+        d_ref = oracle.teacher_delta_rows(Qc, Kc, Vc, h, rows=keys)
+        av = d_ref + Vc[keys, h, :].double().numpy()
+        check_delta(delta[torch.from_numpy(keys).cuda(), h, :].double().cpu().numpy(), d_ref, av,
+                    "S=32 h=%d" % h, y_bf16=True)
+    # every head: the column maxima lie in (0, 1] and sum to at least one
+    assert (cm > 0).all() and (cm <= 1 + 1e-6).all()
+    assert (cm.sum(axis=1) >= 1 - 1e-4).all()
+
+
+def test_router_loss():
+    from paper_2609_23733_amd import vp
+    S, P = 1, 700
+    log("router loss")
+    x = synth.make_layer(S, P, dtype="bf16", key=(32, 0), sharp=True)
+    Q, K, V = x.Q.cuda(), x.K.cuda(), x.V.cuda()
+    ws = vp.alloc_workspace(S, P, 16, torch.bfloat16)
+    st = vp.router_score(Q, K, V, x.W.cuda(), x.U.cuda(), x.w.cuda(), S, P, ws)
+    colmax, smax, _ = vp.teacher_targets(Q, K, V, S, P)
+    lam = 0.5
+    loss = vp.router_loss(K, st, colmax, smax, S, P, lam).cpu().numpy()
+    qp = oracle.router_pool(x.Q, x.W, x.U, x.w)
+    _, _, _, r = oracle.router_route(x.K, x.V, qp, want_r=True)
+    for h in range(16):
+        ref = oracle.router_loss(oracle.attention_colmax(x.Q, x.K, h), r[h], lam)
+        err = abs(loss[h] - ref)
+        log("router loss h=%d gpu %.6f ref %.6f" % (h, loss[h], ref))
+        assert err <= 1e-3 * abs(ref) + 1e-5, (h, loss[h], ref)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_latent_loss(dtype):
+    from paper_2609_23733_amd import vp
+    S, P = 2, 1374
+    log("latent loss %s" % dtype)
+    N = S * P
+    a = synth.stored(synth.normal((N, 16, 64), 71, 1.0), dtype)
+    b = synth.stored(a.float() * 0.8 + synth.normal((N, 16, 64), 72, 0.3), dtype)
+    loss = vp.latent_loss(a.cuda(), b.cuda(), S, P, 0.25).cpu().numpy()
+    for h in range(16):
+        ref = oracle.latent_loss(a[:, h].double().numpy(), b[:, h].double().numpy(), 0.25)
+        assert abs(loss[h] - ref) <= 1e-4 * abs(ref), (h, loss[h], ref)
