@@ -5,13 +5,13 @@
 //   Eq.10 Delta^T_h = (A_h - I) V_h;
 //   Eq.9  router loss  KL(p_bar || r_bar) + lambda |max p^T - max r|;
 //   Eq.11 latent loss  ||D_hat - D^T|| + lambda (1 - cos(D_hat, D^T)).
-// The column maxima take two passes over all (query, key) pairs, both on the
-// bf16 MFMA (bf16 products are exact in fp32):
-//   D1  per query, o_q = m_q + log2 l_q (log2 units): its softmax normaliser;
-//   D2  per key, max over queries of x_qk - o_q (x the logit in log2 units),
-//       exponentiated once at the end: exp2 is monotone, so the maximum can
-//       be taken before it and each score costs one FMA and one max.
-// Delta^T reuses the FULL-head kernels on every head, then subtracts V.
+// The column maxima take two passes over all (query, key) pairs:
+//   D1  per query, o_q = log2 sum_k 2^x_qk (x the logit in log2 units), its
+//       softmax normaliser: written by the teacher instances of the FULL-head
+//       kernels, which compute Delta^T's attention in the same pass;
+//   D2  per key, max over queries of x_qk - o_q, exponentiated once at the
+//       end (exp2 is monotone, so the maximum can be taken before it), on the
+//       bf16 MFMA (bf16 products are exact in fp32).
 #include "vp_device.hpp"
 #include "vp_internal.hpp"
 
@@ -20,151 +20,114 @@ namespace vp {
 constexpr int kDL = 72;   // bf16 LDS row stride (144 B)
 
 // ------------------------------------------------------------------------
-// D1: one workgroup = 4 waves x 64 queries of one head; key tiles of 64
-// staged through LDS (double-buffered); S^T = K Q^T per 32-query block, the
-// running maximum and sum per query (each lane owns a query column and half
-// of its keys; the halves share the maximum through one exchange).
+// D2: one workgroup = kCmWaves waves x (32 kCmKB) keys of one head; each wave
+// keeps its key rows as the MFMA's A operand in registers.  Query tiles of
+// 32 kCmQB (Q rows and -o_q / c) are staged through LDS, double-buffered, and
+// shared by the waves.  The accumulator starts at -o_q / c, so the MFMA
+// returns (x_qk - o_q) / c and a score costs half of a three-way max (two
+// query blocks at once); c > 0 carries the maximum over to x - o.  Queries
+// past N carry -inf; keys past N read row 0 and are not written.
 // ------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_rowstats(const bf16* __restrict__ Q,
-                                                  const bf16* __restrict__ K, int64_t N, int H,
-                                                  float c, float* __restrict__ off) {
-    const int h = blockIdx.y;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, n = lane & 31, hh = lane >> 5;
-    __shared__ __attribute__((aligned(16))) bf16 sK[2][64 * kDL];
-    bf16x8 Qop[2][4];
-    int64_t qidx[2];
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const int64_t qi = (int64_t)blockIdx.x * 256 + wave * 64 + qb * 32 + n;
-        qidx[qb] = qi;
-        const bf16* qp = Q + ((qi < N ? qi : 0) * H + h) * kD + 8 * hh;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) Qop[qb][ks] = load_bf16x8(qp + 16 * ks);
-    }
-    const int lr = threadIdx.x >> 2, lc = (threadIdx.x & 3) * 16;
-    bf16x8 p0, p1;
-    auto gload = [&](int t) {
-        const int64_t key = (int64_t)t * 64 + lr;
-        const bf16* kp = K + ((key < N ? key : 0) * H + h) * kD + lc;
-        p0 = load_bf16x8(kp);
-        p1 = load_bf16x8(kp + 8);
-    };
-    auto lstore = [&](int b) {
-        *reinterpret_cast<bf16x8*>(&sK[b][lr * kDL + lc]) = p0;
-        *reinterpret_cast<bf16x8*>(&sK[b][lr * kDL + lc + 8]) = p1;
-    };
-    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
-    const int nkt = (int)((N + 63) / 64);
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int t = 0; t < nkt; ++t) {
-        const int b = t & 1;
-        if (t + 1 < nkt) gload(t + 1);
-        const bool last = (int64_t)(t + 1) * 64 > N;
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            f32x16 S[2] = {zero_f32x16(), zero_f32x16()};
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks)
-                    S[kb] = mfma_bf16(*reinterpret_cast<const bf16x8*>(
-                                          &sK[b][(32 * kb + n) * kDL + 16 * ks + 8 * hh]),
-                                      Qop[qb][ks], S[kb]);
-            if (last) {
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        if ((int64_t)t * 64 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3) >= N)
-                            S[kb][r] = -INFINITY;
-            }
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, S[kb][r]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
-            const float mn = fmaxf(m[qb], mx);
-            float s = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) s += exp2f_fast(fmaf(S[kb][r], c, -mn));
-            l[qb] = l[qb] * exp2f_fast(m[qb] - mn) + s;
-            m[qb] = mn;
-        }
-        if (t + 1 < nkt) lstore(b ^ 1);
-        __syncthreads();
-    }
-#pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-        const float lt = l[qb] + __shfl_xor(l[qb], 32);
-        if (hh == 0 && qidx[qb] < N) off[(int64_t)h * N + qidx[qb]] = m[qb] + __log2f(lt);
-    }
-}
+constexpr int kCmWaves = 8;
+constexpr int kCmKB = 2;                            // 32-key blocks per wave
+constexpr int kCmQB = 2;                            // 32-query blocks per tile (even)
+constexpr int kCmKeys = 32 * kCmKB * kCmWaves;      // keys per workgroup
+constexpr int kCmQ = 32 * kCmQB;                    // queries per LDS tile
 
-// ------------------------------------------------------------------------
-// D2: one workgroup = one 64-key tile of one head, 4 waves; the key rows are
-// the MFMA's A operand, held in registers; wave w streams query blocks of 32
-// (w, w + 4, ...) with the next block's operands loading during the current
-// block's MFMAs.  acc keeps max_q (x_qk - o_q) per key row and lane; the
-// maximum over the 32 query lanes, then over the waves, then one exp2.
-// ------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_colmax(const bf16* __restrict__ Q,
-                                                const bf16* __restrict__ K,
-                                                const float* __restrict__ off, int64_t N, int H,
-                                                float c, float* __restrict__ colmax) {
+__global__ __launch_bounds__(64 * kCmWaves) void k_colmax(const bf16* __restrict__ Q,
+                                                          const bf16* __restrict__ K,
+                                                          const float* __restrict__ off,
+                                                          int64_t N, int H, float c,
+                                                          float* __restrict__ colmax) {
+    constexpr int kThreads = 64 * kCmWaves;
+    constexpr int kSegs = kCmQ * 8 / kThreads;   // 16-byte tile segments per thread
+    static_assert(kSegs * kThreads == kCmQ * 8 && kCmQ <= kThreads && kCmQB % 2 == 0, "tile");
     const int h = blockIdx.y;
-    const int64_t k0 = (int64_t)blockIdx.x * 64;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, n = lane & 31, hh = lane >> 5;
-    bf16x8 Ka[2][4];
+    const int64_t k0 = (int64_t)blockIdx.x * kCmKeys + wave * 32 * kCmKB;
+    bf16x8 Ka[kCmKB][4];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < kCmKB; ++kb) {
         const int64_t key = k0 + 32 * kb + n;
         const bf16* kp = K + ((key < N ? key : 0) * H + h) * kD + 8 * hh;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) Ka[kb][ks] = load_bf16x8(kp + 16 * ks);
     }
+    __shared__ __attribute__((aligned(16))) bf16 sQ[2][kCmQ * kDL];
+    __shared__ float sO[2][kCmQ];
     const float* oh = off + (int64_t)h * N;
-    const int64_t nqb = (N + 31) / 32;
-    float acc[2][16];
+    const float ninv = -1.f / c;
+    bf16x8 gq[kSegs];
+    float go = 0.f;
+    auto gload = [&](int64_t t) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+        for (int i = 0; i < kSegs; ++i) {
+            const int sg = threadIdx.x + i * kThreads;
+            const int64_t q = t * kCmQ + (sg >> 3);
+            gq[i] = load_bf16x8(Q + ((q < N ? q : 0) * H + h) * kD + (sg & 7) * 8);
+        }
+        // (scaled at the store, so that nothing waits for the load here)
+        if (threadIdx.x < kCmQ) {
+            const int64_t qq = t * kCmQ + threadIdx.x;
+            go = oh[qq < N ? qq : N - 1];
+        }
+    };
+    auto lstore = [&](int64_t t, int b) {
+#pragma unroll
+        for (int i = 0; i < kSegs; ++i) {
+            const int sg = threadIdx.x + i * kThreads;
+            *reinterpret_cast<bf16x8*>(&sQ[b][(sg >> 3) * kDL + (sg & 7) * 8]) = gq[i];
+        }
+        if (threadIdx.x < kCmQ)
+            sO[b][threadIdx.x] = t * kCmQ + threadIdx.x < N ? go * ninv : -INFINITY;
+    };
+    float acc[kCmKB][16];
+#pragma unroll
+    for (int kb = 0; kb < kCmKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[kb][r] = -INFINITY;
-    bf16x8 qn[4];
-    float on = INFINITY;
-    auto qload = [&](int64_t qb) {
-        const int64_t qi = qb * 32 + n;
-        const bool ok = qi < N;
-        const bf16* qp = Q + ((ok ? qi : 0) * H + h) * kD + 8 * hh;
+    const int64_t nt = (N + kCmQ - 1) / kCmQ;
+    gload(0);
+    lstore(0, 0);
+    __syncthreads();
+    for (int64_t t = 0; t < nt; ++t) {
+        const int b = (int)(t & 1);
+        if (t + 1 < nt) gload(t + 1);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) qn[ks] = load_bf16x8(qp + 16 * ks);
-        on = ok ? oh[qi] : INFINITY;   // queries past N contribute -inf
-    };
-    int64_t qb = wave;
-    if (qb < nqb) qload(qb);
-    for (; qb < nqb; qb += 4) {
-        bf16x8 qc[4];
+        for (int qp = 0; qp < kCmQB; qp += 2) {
+            // lanes: query (qp + u) * 32 + n of the tile, features 16 ks + 8 hh ..
+            bf16x8 qv[2][4];
+            f32x16 ci[2];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) qc[ks] = qn[ks];
-        const float oc = on;
-        if (qb + 4 < nqb) qload(qb + 4);
-        f32x16 S[2] = {zero_f32x16(), zero_f32x16()};
+            for (int u = 0; u < 2; ++u) {
+                const int row = (qp + u) * 32 + n;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+                for (int ks = 0; ks < 4; ++ks)
+                    qv[u][ks] = *reinterpret_cast<const bf16x8*>(&sQ[b][row * kDL + 16 * ks + 8 * hh]);
+                const float o = sO[b][row];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) S[kb] = mfma_bf16(Ka[kb][ks], qc[ks], S[kb]);
+                for (int r = 0; r < 16; ++r) ci[u][r] = o;
+            }
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < kCmKB; ++kb) {
+                f32x16 Sa = mfma_bf16(Ka[kb][0], qv[0][0], ci[0]);
+                f32x16 Sb = mfma_bf16(Ka[kb][0], qv[1][0], ci[1]);
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[kb][r] = fmaxf(acc[kb][r], fmaf(S[kb][r], c, -oc));
+                for (int ks = 1; ks < 4; ++ks) {
+                    Sa = mfma_bf16(Ka[kb][ks], qv[0][ks], Sa);
+                    Sb = mfma_bf16(Ka[kb][ks], qv[1][ks], Sb);
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[kb][r] = fmaxf(acc[kb][r], fmaxf(Sa[r], Sb[r]));
+            }
+        }
+        if (t + 1 < nt) lstore(t + 1, b ^ 1);
+        __syncthreads();
     }
-    // Maximum over the 32 query lanes of each half (same key rows).
+    // Maximum over the 32 query lanes of each half (same key rows), then
+    // 2^(c max).
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < kCmKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             float v = acc[kb][r];
@@ -172,18 +135,14 @@ __global__ __launch_bounds__(256) void k_colmax(const bf16* __restrict__ Q,
             for (int o = 1; o < 32; o <<= 1) v = fmaxf(v, __shfl_xor(v, o));
             acc[kb][r] = v;
         }
-    __shared__ float sred[4][64];
     if (n == 0) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < kCmKB; ++kb)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) sred[wave][32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3)] = acc[kb][r];
-    }
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        const int k = threadIdx.x;
-        const float v = fmaxf(fmaxf(sred[0][k], sred[1][k]), fmaxf(sred[2][k], sred[3][k]));
-        if (k0 + k < N) colmax[(int64_t)h * N + k0 + k] = exp2f(v);
+            for (int r = 0; r < 16; ++r) {
+                const int64_t key = k0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
+                if (key < N) colmax[(int64_t)h * N + key] = exp2f(c * acc[kb][r]);
+            }
     }
 }
 
@@ -375,17 +334,18 @@ size_t distill_part_bytes(int H) { return (size_t)H * kLossChunks * 4 * sizeof(f
 void launch_teacher_targets(const TeacherArgs& a, hipStream_t st) {
     const float c = kLog2e / sqrtf((float)kD);
     const bf16 *Q = (const bf16*)a.attn.Q, *K = (const bf16*)a.attn.K;
-    hipLaunchKernelGGL(k_rowstats, dim3((unsigned)((a.attn.N + 255) / 256), a.attn.H), dim3(256),
-                       0, st, Q, K, a.attn.N, a.attn.H, c, a.off);
-    hipLaunchKernelGGL(k_colmax, dim3((unsigned)((a.attn.N + 63) / 64), a.attn.H), dim3(256), 0,
-                       st, Q, K, (const float*)a.off, a.attn.N, a.attn.H, c, a.colmax);
-    hipLaunchKernelGGL(k_colmax_max, dim3(a.attn.H), dim3(256), 0, st, (const float*)a.colmax,
-                       a.attn.N, a.smax);
-    // Delta^T: FULL attention of every head into fp32, then minus V.
+    // D1 with Delta^T's attention: every head FULL into fp32 Y, offsets into
+    // attn.off.
     hipLaunchKernelGGL(k_all_full, dim3(1), dim3(64), 0, st, a.attn.H,
                        const_cast<int32_t*>(a.attn.buckets));
     launch_gather(a.attn, st);
     launch_flash(a.attn, st);
+    hipLaunchKernelGGL(k_colmax, dim3((unsigned)((a.attn.N + kCmKeys - 1) / kCmKeys), a.attn.H),
+                       dim3(64 * kCmWaves), 0, st, Q, K, (const float*)a.attn.off, a.attn.N,
+                       a.attn.H, c, a.colmax);
+    hipLaunchKernelGGL(k_colmax_max, dim3(a.attn.H), dim3(256), 0, st, (const float*)a.colmax,
+                       a.attn.N, a.smax);
+    // Delta^T = Y - V.
     const int64_t n = a.attn.N * a.attn.H * kD;
     hipLaunchKernelGGL(k_sub_v, dim3((unsigned)((n / 8 + 255) / 256)), dim3(256), 0, st,
                        (const float*)a.attn.Y, (const bf16*)a.attn.V, n, a.delta, a.delta_dt);

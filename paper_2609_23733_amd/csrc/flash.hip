@@ -187,6 +187,21 @@ constexpr int kBQ16 = 256;
 constexpr float kSlack = 8.f;        // log2 headroom above a running reference point
 constexpr float kFastBound = 14.f;   // |logit| bound (log2 units) for reference point 0
 constexpr float kF16Safe = 4096.f;   // |c q|, |k| limit for the fp16 logit path
+// Teacher instances (row offsets o_q = log2 sum_k 2^x_qk wanted exactly) add
+// the fp16 residual of c q as a second MFMA operand: per component the
+// logit then errs by at most 2^-22 |c q_i| + 2^-25 (the residual's fp16
+// subnormal spacing), i.e. by 2^-22 * 14 + 2^-25 * 8 max|k| over a work item,
+// which stays below 2^-15.9 when max|k| <= kTeachKmax; items past it go to
+// the exact bf16 kernel.
+constexpr float kTeachKmax = 64.f;
+
+// Kahan step: adds x to the sum s with compensation e (the sum is s - e).
+__device__ __forceinline__ void kahan_add(float& s, float& e, float x) {
+    const float y = x - e;
+    const float t = s + y;
+    e = (t - s) - y;
+    s = t;
+}
 
 __device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
     const f16x2 v = __builtin_bit_cast(f16x2, pair);
@@ -223,6 +238,18 @@ __device__ __forceinline__ void store_rows(const f32x16 (&O)[2][2], const float 
                     }
                 }
         }
+    }
+}
+
+// o_q = m + log2 l per query of the wave's two blocks (teacher instances).
+// (m is the same in both lane halves.)
+__device__ __forceinline__ void store_offsets(const float (&l)[2], const float (&m)[2],
+                                              const int64_t (&qidx)[2], int64_t N, int h, int hh,
+                                              float* __restrict__ off) {
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+        const float lt = l[qb] + __shfl_xor(l[qb], 32);
+        if (hh == 0 && qidx[qb] < N) off[(int64_t)h * N + qidx[qb]] = m[qb] + __log2f(lt);
     }
 }
 
@@ -271,6 +298,7 @@ __device__ __forceinline__ int tail_owner(int64_t x, int64_t T, int G) {
     return (int)(((x + 1) * G + T - 1) / T) - 1;
 }
 
+template <bool kTeach>
 __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ Q,
                                                        const f16* __restrict__ Kh,
                                                        const f16* __restrict__ Vt,
@@ -280,7 +308,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        int32_t* __restrict__ wide_items,
                                                        float* __restrict__ part, int G,
-                                                       void* __restrict__ Y, int ydt) {
+                                                       void* __restrict__ Y, int ydt,
+                                                       float* __restrict__ off) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
     if (active == 0) return;
@@ -296,6 +325,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
     __shared__ __attribute__((aligned(16))) f16 sV[2][kD * kLdsRow];
     __shared__ float sKmax[8];
     __shared__ int sWide[8];
+    // Teacher instances: each wave's fp16 residual operands of c Q, in lane
+    // order ([wave][qb][ks][lane]), read back in every matrix phase (registers
+    // are full).
+    __shared__ __attribute__((aligned(16))) f16x8 sQlo[kTeach ? 8 * 2 * 4 * 64 : 1];
 
     // One segment: key tiles [t0, t1) of item L; written to partial slot
     // pslot of this workgroup if the segment is not the whole item.
@@ -331,7 +364,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const float x = ok ? bf16_to_f32(raw[j]) * c : 0.f;
-                    Qop[qb][ks][j] = (f16)x;
+                    const f16 hi = (f16)x;
+                    Qop[qb][ks][j] = hi;
+                    if (kTeach)   // x - hi is exact
+                        sQlo[((wave * 2 + qb) * 4 + ks) * 64 + lane][j] = (f16)(x - (float)hi);
                     n2 = fmaf(x, x, n2);
                 }
             }
@@ -345,7 +381,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
             for (int v = 1; v < 8; ++v) km = fmaxf(km, sKmax[v]);
             const float qm = fmaxf(qn[0], qn[1]);
             // Written as "not within" so that a NaN norm also goes to K6b.
-            const bool out = !(qm * km <= kFastBound && qm <= kF16Safe && km <= kF16Safe);
+            const bool out = !(qm * km <= kFastBound && qm <= kF16Safe &&
+                               km <= (kTeach ? kTeachKmax : kF16Safe));
             const bool wave_out = __builtin_amdgcn_ballot_w64(out) != 0;
             if (lane == 0) sWide[wave] = wave_out;
         }
@@ -381,12 +418,12 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 
         f32x16 O[2][2], S[2][2];
         f16x8 P[2][2][2];
-        float l[2];
+        float l[2], le[2];   // le: Kahan compensation of l (teacher instances)
         const f16x8 zp = {};
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
             O[qb][0] = O[qb][1] = zero_f32x16();
-            l[qb] = 0.f;
+            l[qb] = le[qb] = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) P[qb][kb][0] = P[qb][kb][1] = zp;
         }
@@ -445,8 +482,27 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     S[0][kb] = mfma_f16(ka[kb][ks], Qop[0][ks], S[0][kb]);
                     S[1][kb] = mfma_f16(ka[kb][ks], Qop[1][ks], S[1][kb]);
                 }
-            __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
-            __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
+            if (kTeach) {
+                const f16x8* ql = &sQlo[wave * 2 * 4 * 64 + lane];
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const f16x8 q0 = ql[ks * 64], q1 = ql[(4 + ks) * 64];
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb) {
+                        S[0][kb] = mfma_f16(ka[kb][ks], q0, S[0][kb]);
+                        S[1][kb] = mfma_f16(ka[kb][ks], q1, S[1][kb]);
+                    }
+                }
+                // V and K operands, the PV products, the residual operands
+                // (V's registers are free by then), the S products.
+                __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
+            } else {
+                __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+                __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
+            }
         };
         // Vector phase of tile r: S(r) -> P(r), l += row sums.  The segment's
         // last tile masks keys >= N to weight 0 (a separate instance, so that
@@ -482,7 +538,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         }
                         P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                     }
-                l[qb] += ls0 + ls1;
+                if (kTeach)
+                    kahan_add(l[qb], le[qb], ls0 + ls1);
+                else
+                    l[qb] += ls0 + ls1;
             }
         };
         const std::false_type body{};
@@ -546,8 +605,16 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         }
         pv(ns & 1);   // O += V(ns-1) P(ns-1)
 
+        if (kTeach) {
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) l[qb] -= le[qb];
+        }
         if (t0 == 0 && t1 == nkt) {
             store_rows(O, l, qidx, N, H, h, hh, vsc[2 * slot + 1], Y, ydt);
+            if (kTeach) {
+                const float zero[2] = {0.f, 0.f};
+                store_offsets(l, zero, qidx, N, h, hh, off);
+            }
         } else {
             // Partial slot: O[q][d] unnormalized, then l[q], q = row in item.
             float* ps = part + (int64_t)(w * 2 + pslot) * kPartFloats;
@@ -598,7 +665,8 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
                                                        const int32_t* __restrict__ wide_items,
                                                        const float* __restrict__ part,
                                                        const float* __restrict__ vsc, int G,
-                                                       void* __restrict__ Y, int ydt) {
+                                                       void* __restrict__ Y, int ydt,
+                                                       float* __restrict__ off) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
     const int full = active / G * G, R = active - full;
@@ -625,6 +693,7 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
         if (qi >= N) continue;
         float lt = 0.f;
         for (int v = wf; v <= wl; ++v) lt += pslot(v)[kBQf * kD + qr];
+        if (off) off[(int64_t)h * N + qi] = __log2f(lt);
         const float inv = vsc[2 * slot + 1] / lt;
 #pragma unroll 1
         for (int d0 = 0; d0 < kD; d0 += 8) {
@@ -674,6 +743,7 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
 // below fp16's normal range add at most 2^-25 each.  O / l is unchanged by
 // the choice of reference point.
 // ------------------------------------------------------------------------
+template <bool kTeach>
 __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restrict__ Q,
                                                        const bf16* __restrict__ K,
                                                        const f16* __restrict__ Vt,
@@ -682,7 +752,8 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
                                                        const int32_t* __restrict__ wide_items,
-                                                       int nqt_fast, void* __restrict__ Y, int ydt) {
+                                                       int nqt_fast, void* __restrict__ Y, int ydt,
+                                                       float* __restrict__ off) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
     if ((int)blockIdx.x >= active) return;
@@ -750,12 +821,12 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
     };
 
     f32x16 O[2][2];
-    float m[2], l[2];
+    float m[2], l[2], le[2];   // le: Kahan compensation of l (teacher instances)
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
         O[qb][0] = O[qb][1] = zero_f32x16();
         m[qb] = -INFINITY;
-        l[qb] = 0.f;
+        l[qb] = le[qb] = 0.f;
     }
 
     gload(0);
@@ -808,13 +879,15 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
                 const float al = move ? exp2f_fast(m[qb] - mn) : 1.f;
                 m[qb] = mn;
                 l[qb] *= al;
+                le[qb] *= al;
 #pragma unroll
                 for (int db = 0; db < 2; ++db)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) O[qb][db][r] *= al;
             }
-            // p = 2^(s c - m), packed to fp16; row sums from the packed values,
-            // per tile from zero, then added to l.
+            // p = 2^(s c - m), packed to fp16; row sums per tile from zero, then
+            // added to l: from the packed values, or in teacher instances from
+            // the fp32 values with a compensated add.
             const float nm = -m[qb];
             float ls = 0.f;
 #pragma unroll
@@ -828,11 +901,17 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
                         e[0] = exp2f_fast(fmaf(S[kb][8 * b + 2 * j], c, nm));
                         e[1] = exp2f_fast(fmaf(S[kb][8 * b + 2 * j + 1], c, nm));
                         pk[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(e, f16x2));
-                        ls = dot2_ones(pk[j], ls);
+                        if (kTeach)
+                            ls += e[0] + e[1];
+                        else
+                            ls = dot2_ones(pk[j], ls);
                     }
                     P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                 }
-            l[qb] += ls;
+            if (kTeach)
+                kahan_add(l[qb], le[qb], ls);
+            else
+                l[qb] += ls;
         }
 
         // O^T += V^T P^T
@@ -852,7 +931,12 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
         __syncthreads();
     }
 
+    if (kTeach) {
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) l[qb] -= le[qb];
+    }
     store_rows(O, l, qidx, N, H, h, hh, vsc[2 * slot + 1], Y, ydt);
+    if (kTeach) store_offsets(l, m, qidx, N, h, hh, off);
 }
 
 // ------------------------------------------------------------------------
@@ -1039,17 +1123,17 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
     if (a.dtype == DT_BF16) {
         const int nqf = (int)((a.N + kBQf - 1) / kBQf);
         const int G = flash_stream_groups(a.N, a.H);
-        hipLaunchKernelGGL(k_flash_bf16, dim3(G), dim3(512), 0, st, (const bf16*)a.Q,
-                           (const f16*)a.kh, (const f16*)a.vt, (const float*)a.kmax,
-                           (const float*)a.vsc, a.buckets, a.N, a.H, nqf, nkt, c, a.qflag, a.part,
-                           G, a.Y, a.ydt);
+        hipLaunchKernelGGL(a.off ? k_flash_bf16<true> : k_flash_bf16<false>, dim3(G), dim3(512),
+                           0, st, (const bf16*)a.Q, (const f16*)a.kh, (const f16*)a.vt,
+                           (const float*)a.kmax, (const float*)a.vsc, a.buckets, a.N, a.H, nqf,
+                           nkt, c, a.qflag, a.part, G, a.Y, a.ydt, a.off);
         hipLaunchKernelGGL(k_flash_combine, dim3(G), dim3(256), 0, st, a.buckets, a.N, a.H, nqf,
                            nkt, (const int32_t*)a.qflag, (const float*)a.part,
-                           (const float*)a.vsc, G, a.Y, a.ydt);
-        hipLaunchKernelGGL(k_flash_bf16_wide, dim3(nqt * a.H), dim3(256), 0, st,
-                           (const bf16*)a.Q, (const bf16*)a.K, (const f16*)a.vt,
-                           (const float*)a.kmax, (const float*)a.vsc, a.buckets, a.N, a.H, nqt,
-                           nkt, c, a.qflag, nqf, a.Y, a.ydt);
+                           (const float*)a.vsc, G, a.Y, a.ydt, a.off);
+        hipLaunchKernelGGL(a.off ? k_flash_bf16_wide<true> : k_flash_bf16_wide<false>,
+                           dim3(nqt * a.H), dim3(256), 0, st, (const bf16*)a.Q, (const bf16*)a.K,
+                           (const f16*)a.vt, (const float*)a.kmax, (const float*)a.vsc, a.buckets,
+                           a.N, a.H, nqt, nkt, c, a.qflag, nqf, a.Y, a.ydt, a.off);
     } else
         hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
                            (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,

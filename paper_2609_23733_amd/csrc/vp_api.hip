@@ -493,7 +493,7 @@ vp_status vp_teacher_targets(const vp_shape* shape, const void* Q, const void* K
     vp::TeacherArgs a;
     int32_t* buckets = (int32_t*)(w + T.off_buckets);
     a.attn = attn_args(shape, T.attn, Q, K, V, nullptr, buckets, w + T.off_y, VP_F32, ws);
-    a.off = (float*)(w + T.off_off);
+    a.attn.off = (float*)(w + T.off_off);
     a.colmax = colmax;
     a.smax = smax;
     a.delta = delta;

@@ -44,6 +44,8 @@ struct AttnArgs {
     int64_t n3, chunk3;   // linear-attention token chunks
     float* lpart;         // linear-attention partial sums [H][n3][kLinSums]
     float* lsum;          // linear-attention sums [H][kLinSums]
+    float* off;           // null, or [H, N]: per query o = log2 sum_k 2^x_qk (x the logit
+                          // in log2 units), written by the FULL-head kernels (bf16 only)
 };
 
 // Per head: the 64 x 64 sum of phi(k) v^T followed by the 64 sums of phi(k).
@@ -70,8 +72,8 @@ void launch_block_qkv(const BlockArgs& a, hipStream_t st);
 void launch_block_out(const BlockArgs& a, hipStream_t st);
 // Distillation targets and losses (bf16 layers).
 struct TeacherArgs {
-    AttnArgs attn;        // every head FULL; Y = fp32 workspace, buckets in the workspace
-    float* off;           // [H, N] per-query softmax offsets (log2 units)
+    AttnArgs attn;        // every head FULL; Y = fp32 workspace, buckets and attn.off
+                          // ([H, N] per-query softmax offsets) in the workspace
     float* colmax;        // [H, N]
     float* smax;          // [H]
     void* delta;          // [N, H, d]

@@ -65,6 +65,26 @@ def test_teacher_targets(P, sharp):
         check_delta(dl[:, h, :], d_ref, av, "P=%d h=%d" % (P, h))
 
 
+def test_teacher_targets_large_keys():
+    """K scaled by 2^7 and Q by 2^-7 (exact in bf16): the logits are those of
+    a mild layer, but the key norms leave the fp16 residual's error bound, so
+    the exact-logit kernel computes the offsets."""
+    from paper_2609_23733_amd import vp
+    log("teacher targets large keys")
+    x = synth.make_layer(1, 700, dtype="bf16", key=(33, 0))
+    Q = (x.Q.float() * 2.0 ** -7).to(torch.bfloat16)
+    K = (x.K.float() * 2.0 ** 7).to(torch.bfloat16)
+    colmax, smax, delta = vp.teacher_targets(Q.cuda(), K.cuda(), x.V.cuda(), 1, 700,
+                                             y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    cm, dl = colmax.cpu().numpy(), delta.double().cpu().numpy()
+    for h in range(16):
+        ref = oracle.attention_colmax(Q, K, h)
+        check_colmax(cm[h], ref, "large keys h=%d" % h)
+        d_ref = oracle.teacher_delta_rows(Q, K, x.V, h)
+        check_delta(dl[:, h, :], d_ref, d_ref + x.V[:, h, :].double().numpy(), "large keys h=%d" % h)
+
+
 def test_teacher_targets_s32_sampled():
     """S = 32 views (N = 43,968): the column maxima of 64 sampled keys of two
     heads (the oracle still visits every query) and Delta^T on 64 sampled rows."""
