@@ -18,6 +18,10 @@ fixes it -- parity unpinned as to the architecture itself.  Likewise the
 feature map of the linear-attention ablation (phi = elu + 1, the map of the
 kernelised attention the paper cites) is a reading: the computation given phi
 is pinned against its explicit-matrix form, the choice of phi is unpinned.
+The paper gives no steps for its token-merging combination either: the merging
+rule here (ToMe's bipartite soft matching on the head-summed keys) is a
+reading, its computation pinned by a brute force and planted decisions, the
+choice of rule parity unpinned.
 """
 from __future__ import annotations
 
@@ -40,6 +44,7 @@ POOL_GATED, POOL_MEAN = 0, 1
 SURR_EQ7, SURR_MEAN_CONTEXT, SURR_NO_RESIDUAL, SURR_ADD_IDENTITY, SURR_LINEAR_ATTN = 0, 1, 2, 3, 4
 ACT_GELU, ACT_RELU = 0, 1
 TAU_LOW, TAU_HIGH = 0.01, 0.20   # Section 4.2 and implementation details
+TOME_SPECIAL = 5                 # special tokens per view (camera + registers), never merged
 LN_EPS, ROPE_BASE = 1e-6, 100.0  # readings for the block around the layer
 
 
@@ -77,6 +82,14 @@ def _load():
             lib.or_rope2d.argtypes = [P, i64, i32, i32, P, dbl, i32]
             lib.or_gelu.argtypes = [P, i64]
             lib.or_attention_colmax.argtypes = [P, P, i64, i32, i32, i32, dbl, P, i64, P, i32]
+            lib.or_tome_metric.argtypes = [P, i64, i32, i32, P]
+            lib.or_tome_split.argtypes = [i64, i64, i64, i64, P]
+            lib.or_tome_split.restype = i64
+            lib.or_tome_match.argtypes = [P, i64, i32, P, P, i64, P, P, i32]
+            lib.or_tome_select.argtypes = [P, P, i64, i64, P]
+            lib.or_tome_rows.argtypes = [i64, P, P, P, i64, P]
+            lib.or_tome_rows.restype = i64
+            lib.or_tome_merge.argtypes = [P, i64, i64, P, i64, P]
             lib.or_threads_used.argtypes = [i32]
             lib.or_threads_used.restype = i32
             _lib = lib
@@ -401,3 +414,89 @@ def latent_loss(dhat, dT, lam=1.0):
     b = np.asarray(dT, np.float64).ravel()
     cos = float(a @ b) / (np.sqrt(float(a @ a)) * np.sqrt(float(b @ b)))
     return float(np.sqrt(float((a - b) @ (a - b)))) + lam * (1.0 - cos)
+
+
+# ----------------------------------------------------------- token merging
+# ToMe's bipartite soft matching (Bolya et al., ICLR 2023) before the routed
+# attention, in the reading stated in vp_oracle.c: head-sum key metric rounded
+# to bf16, destinations = view 0 + special tokens + a stride-g patch lattice,
+# cosine matching, the M most similar sources merged by mean, unmerge by copy.
+
+def tome_metric(K):
+    """m_i = bf16(sum over heads of K_{i,h}) (fp32 head-order sum): [N, d] float64."""
+    K = as_f32(K)
+    N, H, d = K.shape
+    m = np.empty((N, d), np.float64)
+    _load().or_tome_metric(_p(K), N, H, d, _p(m))
+    return m
+
+
+def tome_split(S, P, M, nspecial=TOME_SPECIAL):
+    """(is_dst [S*P] bool, g): the destination set for merging M tokens."""
+    is_dst = np.zeros(S * P, np.uint8)
+    g = _load().or_tome_split(int(S), int(P), int(nspecial), int(M), _p(is_dst))
+    if g < 0:
+        raise ValueError("cannot merge %d of %d tokens" % (M, S * P))
+    return is_dst.astype(bool), int(g)
+
+
+def tome_match(K, S, P, M, srcs=None, nspecial=TOME_SPECIAL, nthreads=0):
+    """Most similar destination token and its cosine similarity for the listed
+    source tokens (all sources when srcs is None): (srcs, best, score)."""
+    is_dst, _ = tome_split(S, P, M, nspecial)
+    m = tome_metric(K)
+    if srcs is None:
+        srcs = np.nonzero(~is_dst)[0]
+    srcs = np.ascontiguousarray(srcs, dtype=np.int64)
+    best = np.empty(srcs.shape[0], np.int64)
+    score = np.empty(srcs.shape[0], np.float64)
+    _load().or_tome_match(_p(m), m.shape[0], m.shape[1], _p(is_dst.astype(np.uint8)), _p(srcs),
+                          srcs.shape[0], _p(best), _p(score), _nt(nthreads))
+    return srcs, best, score
+
+
+def tome_select(srcs, score, M):
+    """merged [nsrc] bool: the M sources ranked first by (similarity desc, token asc)."""
+    srcs = np.ascontiguousarray(srcs, dtype=np.int64)
+    score = np.ascontiguousarray(score, dtype=np.float64)
+    merged = np.zeros(srcs.shape[0], np.uint8)
+    _load().or_tome_select(_p(srcs), _p(score), srcs.shape[0], int(M), _p(merged))
+    return merged.astype(bool)
+
+
+def tome_rows(N, srcs, best, merged):
+    """(row [N] int64, nrows): merged-sequence row of every token."""
+    srcs = np.ascontiguousarray(srcs, dtype=np.int64)
+    best = np.ascontiguousarray(best, dtype=np.int64)
+    row = np.empty(int(N), np.int64)
+    n = _load().or_tome_rows(int(N), _p(srcs), _p(best),
+                             _p(np.ascontiguousarray(merged, dtype=np.uint8)), srcs.shape[0],
+                             _p(row))
+    return row, int(n)
+
+
+def tome_plan(K, S, P, M, nspecial=TOME_SPECIAL, nthreads=0):
+    """The whole merge plan for merging M of the S*P tokens."""
+    is_dst, g = tome_split(S, P, M, nspecial)
+    srcs, best, score = tome_match(K, S, P, M, None, nspecial, nthreads)
+    merged = tome_select(srcs, score, M)
+    row, nrows = tome_rows(S * P, srcs, best, merged)
+    return dict(is_dst=is_dst, g=g, srcs=srcs, best=best, score=score, merged=merged, row=row,
+                nrows=nrows)
+
+
+def tome_merge(X, row, nrows):
+    """Rows of the merged sequence: the mean of each row's tokens.  X [N, ...]
+    -> [nrows, ...] float64."""
+    X = as_f32(X)
+    N = X.shape[0]
+    F = int(np.prod(X.shape[1:])) if X.ndim > 1 else 1
+    out = np.empty((int(nrows), F), np.float64)
+    _load().or_tome_merge(_p(np.ascontiguousarray(X.reshape(N, F))), N, F,
+                          _p(np.ascontiguousarray(row, dtype=np.int64)), int(nrows), _p(out))
+    return out.reshape((int(nrows),) + X.shape[1:])
+
+
+def tome_unmerge(Y, row):
+    """Every token takes its row's output: Y [nrows, ...] -> [N, ...]."""
+    return np.asarray(Y)[np.asarray(row)]

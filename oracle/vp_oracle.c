@@ -586,3 +586,182 @@ void or_attention_colmax(const float *Q, const float *K, int64_t N, int H, int d
     or_parallel_for(keys ? nkeys : N, nthreads, colmax_body, &c);
     free(m);
 }
+
+/* -------------------------------------------------------- token merging
+ * Token merging before the routed attention.  The paper combines its layer
+ * with ToMe (as FastVGGT uses it, at merging ratios of 75 % and 90 %) and
+ * gives no steps of its own; the steps here are ToMe's bipartite soft
+ * matching (Bolya et al., ICLR 2023) applied to the layer's Q, K, V:
+ *   metric  m_i = bf16(sum over heads of K_{i,h}): the head sum in fp32, in
+ *           head order, rounded once to bf16 (ToMe matches tokens by their
+ *           keys; rounding the metric fixes the precision in which both
+ *           implementations take their decisions);
+ *   split   destinations: every token of view 0, the nspecial special tokens
+ *           of every view, and in views 1.. the patches whose index within
+ *           the view's patches is a multiple of g, g the smallest stride
+ *           that leaves at least M sources; sources: all other tokens;
+ *   match   each source's most similar destination by cosine similarity
+ *           (the first in token order on ties; 0 for a zero vector);
+ *   select  the M sources with the largest similarity are merged (the lower
+ *           token index first on ties);
+ *   rows    the kept tokens (destinations and unmerged sources) in token
+ *           order are the rows of the merged sequence; a merged source joins
+ *           its destination's row;
+ *   merge   a row is the mean of its tokens; unmerging gives every token its
+ *           row's output.
+ * --------------------------------------------------------------------- */
+
+/* x rounded to bf16 (nearest, ties to even), as a double. */
+static double bf16_rne(float x) {
+    uint32_t u;
+    memcpy(&u, &x, sizeof(u));
+    if ((u & 0x7f800000u) != 0x7f800000u) u += 0x7fffu + ((u >> 16) & 1u);
+    u &= 0xffff0000u;
+    float y;
+    memcpy(&y, &u, sizeof(y));
+    return (double)y;
+}
+
+void or_tome_metric(const float *K, int64_t N, int H, int d, double *m) {
+    for (int64_t i = 0; i < N; ++i)
+        for (int e = 0; e < d; ++e) {
+            float s = 0.f;
+            for (int h = 0; h < H; ++h) s += K[(i * H + h) * (int64_t)d + e];
+            m[i * d + e] = bf16_rne(s);
+        }
+}
+
+/* Destination flags; returns g, or -1 when fewer than M sources exist. */
+int64_t or_tome_split(int64_t S, int64_t P, int64_t nspecial, int64_t M, uint8_t *is_dst) {
+    const int64_t np = P - nspecial;
+    if (S < 1 || np < 1 || M < 0) return -1;
+    int64_t g = 1;
+    for (; g <= np; ++g) {
+        const int64_t ndst = (np + g - 1) / g;
+        if ((S - 1) * (np - ndst) >= M) break;
+    }
+    if (g > np) return -1;
+    for (int64_t v = 0; v < S; ++v)
+        for (int64_t j = 0; j < P; ++j) {
+            const int64_t k = j - nspecial;
+            is_dst[v * P + j] = (uint8_t)(v == 0 || k < 0 || k % g == 0);
+        }
+    return g;
+}
+
+typedef struct {
+    const double *m;
+    int d;
+    const int64_t *dst;   /* destination tokens, ascending */
+    int64_t ndst;
+    const double *dnorm;  /* |m| of each destination */
+    const int64_t *src;   /* sources to match */
+    int64_t *best;        /* [nsrc] most similar destination token */
+    double *score;        /* [nsrc] its cosine similarity */
+} tome_ctx;
+
+static double vnorm(const double *x, int d) {
+    double s = 0.0;
+    for (int e = 0; e < d; ++e) s += x[e] * x[e];
+    return sqrt(s);
+}
+
+static void match_body(void *p, int64_t lo, int64_t hi) {
+    tome_ctx *c = (tome_ctx *)p;
+    for (int64_t i = lo; i < hi; ++i) {
+        const double *a = c->m + c->src[i] * c->d;
+        const double na = vnorm(a, c->d);
+        int64_t best = -1;
+        double bs = 0.0;
+        for (int64_t j = 0; j < c->ndst; ++j) {
+            const double *b = c->m + c->dst[j] * c->d;
+            double dot = 0.0;
+            for (int e = 0; e < c->d; ++e) dot += a[e] * b[e];
+            const double cs = (na == 0.0 || c->dnorm[j] == 0.0) ? 0.0 : dot / (na * c->dnorm[j]);
+            if (best < 0 || cs > bs) {
+                bs = cs;
+                best = c->dst[j];
+            }
+        }
+        c->best[i] = best;
+        c->score[i] = bs;
+    }
+}
+
+void or_tome_match(const double *m, int64_t N, int d, const uint8_t *is_dst, const int64_t *src,
+                   int64_t nsrc, int64_t *best, double *score, int nthreads) {
+    int64_t ndst = 0;
+    for (int64_t t = 0; t < N; ++t) ndst += is_dst[t];
+    int64_t *dst = (int64_t *)malloc(sizeof(int64_t) * (ndst > 0 ? ndst : 1));
+    double *dn = (double *)malloc(sizeof(double) * (ndst > 0 ? ndst : 1));
+    for (int64_t t = 0, j = 0; t < N; ++t)
+        if (is_dst[t]) {
+            dst[j] = t;
+            dn[j] = vnorm(m + t * d, d);
+            ++j;
+        }
+    tome_ctx c = {m, d, dst, ndst, dn, src, best, score};
+    or_parallel_for(nsrc, nthreads, match_body, &c);
+    free(dst);
+    free(dn);
+}
+
+typedef struct {
+    double score;
+    int64_t tok;
+    int64_t pos;
+} tome_item;
+
+static int by_score(const void *x, const void *y) {
+    const tome_item *a = (const tome_item *)x, *b = (const tome_item *)y;
+    if (a->score > b->score) return -1;
+    if (a->score < b->score) return 1;
+    return a->tok < b->tok ? -1 : (a->tok > b->tok ? 1 : 0);
+}
+
+/* merged[i] = 1 for the M sources ranked first by (similarity desc, token asc). */
+void or_tome_select(const int64_t *src, const double *score, int64_t nsrc, int64_t M,
+                    uint8_t *merged) {
+    tome_item *it = (tome_item *)malloc(sizeof(tome_item) * (nsrc > 0 ? nsrc : 1));
+    for (int64_t i = 0; i < nsrc; ++i) {
+        it[i].score = score[i];
+        it[i].tok = src[i];
+        it[i].pos = i;
+        merged[i] = 0;
+    }
+    qsort(it, (size_t)nsrc, sizeof(tome_item), by_score);
+    for (int64_t i = 0; i < M && i < nsrc; ++i) merged[it[i].pos] = 1;
+    free(it);
+}
+
+/* row[t]: the merged-sequence row of every token; returns the row count. */
+int64_t or_tome_rows(int64_t N, const int64_t *src, const int64_t *best, const uint8_t *merged,
+                     int64_t nsrc, int64_t *row) {
+    int64_t *into = (int64_t *)malloc(sizeof(int64_t) * (N > 0 ? N : 1));
+    for (int64_t t = 0; t < N; ++t) into[t] = -1;
+    for (int64_t i = 0; i < nsrc; ++i)
+        if (merged[i]) into[src[i]] = best[i];
+    int64_t r = 0;
+    for (int64_t t = 0; t < N; ++t)
+        if (into[t] < 0) row[t] = r++;
+    for (int64_t t = 0; t < N; ++t)
+        if (into[t] >= 0) row[t] = row[into[t]];
+    free(into);
+    return r;
+}
+
+/* Xm[r] = mean of X[t] over the tokens t with row[t] = r; X is [N, F]. */
+void or_tome_merge(const float *X, int64_t N, int64_t F, const int64_t *row, int64_t nrows,
+                   double *Xm) {
+    int64_t *cnt = (int64_t *)calloc((size_t)(nrows > 0 ? nrows : 1), sizeof(int64_t));
+    memset(Xm, 0, sizeof(double) * (size_t)(nrows * F));
+    for (int64_t t = 0; t < N; ++t) {
+        double *y = Xm + row[t] * F;
+        const float *x = X + t * F;
+        for (int64_t f = 0; f < F; ++f) y[f] += (double)x[f];
+        cnt[row[t]]++;
+    }
+    for (int64_t r = 0; r < nrows; ++r)
+        for (int64_t f = 0; f < F; ++f) Xm[r * F + f] /= (double)cnt[r];
+    free(cnt);
+}

@@ -68,9 +68,27 @@ MUTANTS = {
     "colmax_scale_dropped": ("    return dot * c->scale;\n}", "    return dot;\n}", "distill"),
     "colmax_sum_not_max": ("            if (a > best) best = a;", "            best += a / (double)c->N;",
                            "distill"),
+    # token merging (pins in test_oracle_tome_pins.py)
+    "tome_metric_one_head": ("for (int h = 0; h < H; ++h) s += K[(i * H + h) * (int64_t)d + e];",
+                             "for (int h = 0; h < 1; ++h) s += K[(i * H + h) * (int64_t)d + e];",
+                             "tome"),
+    "tome_metric_truncated": ("u += 0x7fffu + ((u >> 16) & 1u);", "u += 0u;", "tome"),
+    "tome_stride_not_smallest": ("if ((S - 1) * (np - ndst) >= M) break;",
+                                 "if ((S - 1) * (np - ndst) > M) break;", "tome"),
+    "tome_view0_merged": ("(uint8_t)(v == 0 || k < 0 || k % g == 0)", "(uint8_t)(k < 0 || k % g == 0)",
+                          "tome"),
+    "tome_dot_not_cosine": ("dot / (na * c->dnorm[j]);", "dot / na;", "tome"),
+    "tome_match_last_tie": ("if (best < 0 || cs > bs) {", "if (best < 0 || cs >= bs) {", "tome"),
+    "tome_select_least_similar": ("if (a->score > b->score) return -1;\n    if (a->score < b->score) return 1;",
+                                  "if (a->score > b->score) return 1;\n    if (a->score < b->score) return -1;",
+                                  "tome"),
+    "tome_select_tie_high_index": ("return a->tok < b->tok ? -1 : (a->tok > b->tok ? 1 : 0);",
+                                   "return a->tok > b->tok ? -1 : (a->tok < b->tok ? 1 : 0);", "tome"),
+    "tome_merge_sum_not_mean": ("Xm[r * F + f] /= (double)cnt[r];", "Xm[r * F + f] /= 1.0;", "tome"),
+    "tome_rows_count_merged": ("if (into[t] < 0) row[t] = r++;", "row[t] = r++;", "tome"),
 }
 PIN_FILES = {"layer": "test_oracle_pins.py", "block": "test_oracle_block_pins.py",
-             "distill": "test_oracle_distill_pins.py"}
+             "distill": "test_oracle_distill_pins.py", "tome": "test_oracle_tome_pins.py"}
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
