@@ -272,8 +272,9 @@ vp_status vp_block_out(const vp_shape *shape, const void *X, const void *Y,
  *     colmax [H, N] fp32  p^T_{h,k} = max_q A_h[k][q]            (Eq.8)
  *     smax   [H]    fp32  s^attn_h = max_{k,q} A_h[k][q] = max_k p^T_{h,k}
  *     delta  [N, H, d]    Delta^T_h = (A_h - I) V_h in y_dtype     (Eq.10)
- *   (two passes over all query-key pairs for colmax, the FULL-head kernels
- *   for delta; arithmetic in fp32, one rounding of delta).
+ *   (the FULL-head kernels give delta's attention and every query's softmax
+ *   normaliser, then one pass over all query-key pairs gives colmax;
+ *   arithmetic in fp32, one rounding of delta).
  *   vp_router_loss: per head, Eq.9 with p_bar = colmax / sum_k colmax and
  *     r_bar = r_h, the routing vector of `state` (vp_router_score of the same
  *     K with the same `scale`, 1/sqrt(d) when 0):
@@ -295,6 +296,61 @@ vp_status vp_router_loss(const vp_shape *shape, const void *K, const vp_router_s
 vp_status vp_latent_loss(const vp_shape *shape, const void *D_hat, const void *D_t,
                          vp_dtype dtype, float lambda, float *loss, void *ws, size_t ws_bytes,
                          void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Token merging before the routed attention (the paper's combination of the
+ * layer with ToMe, section "VGGT-Prime & Token Merging", at merging ratios of
+ * 75 % and 90 %; the paper gives no steps, these are ToMe's bipartite soft
+ * matching run on the layer's inputs):
+ *   metric  m_i = bf16(sum over heads of K_{i,h}), the sum in fp32 in head
+ *           order;
+ *   split   destinations: every token of view 0, the first `nspecial` tokens
+ *           of every view, and in views 1.. the patches (the tokens after the
+ *           special ones) whose index among the view's patches is a multiple
+ *           of g, g the smallest stride that leaves at least M sources;
+ *           sources: all other tokens;
+ *   match   each source's most similar destination by cosine similarity of
+ *           the metric (the first in token order on ties; 0 for a zero
+ *           vector);
+ *   select  the M most similar sources are merged (the lower token index
+ *           first on ties);
+ *   rows    the kept tokens (destinations and unmerged sources) in token
+ *           order are the nrows = N - M rows of the merged sequence; a merged
+ *           source joins its destination's row.
+ * The routed layer then runs on the nrows rows as one sequence (S = 1,
+ * P = nrows) and vp_tome_unmerge gives every token its row's output.
+ *
+ * vp_tome_split (host only, no device work): g and nrows for merging M of the
+ *   shape's S * P tokens; VP_ERR_INVALID_ARG when M sources do not exist
+ *   (M >= 0, nspecial in [0, P)).
+ * vp_tome_plan (bf16 K [N, H, 64]) writes, all device int32 / fp32:
+ *   row       [N]          the row of every token;
+ *   row_start [nrows + 1], members [N]: the tokens of row r are
+ *             members[row_start[r] .. row_start[r + 1]): its own kept token
+ *             first, then the sources merged into it in token order;
+ *   best      [N] (may be null): a source's most similar destination token,
+ *             -1 for destinations;
+ *   score     [N] (may be null): that cosine similarity (fp32), 0 for
+ *             destinations.
+ *   Workspace: vp_tome_workspace_bytes(shape) (~190 bytes per token).
+ * vp_tome_merge: Xm[r] = mean of X[t] over the members of row r, fp32 sums
+ *   in member order, one rounding; X [N, H * 64] -> Xm [nrows, H * 64] in the
+ *   shape's dtype.  Member entries outside [0, N) are skipped.
+ * vp_tome_unmerge: Y[t] = Ym[row[t]] ([nrows, H * 64] -> [N, H * 64], the
+ *   shape's dtype); a row outside [0, nrows) gives zeros.
+ * All three enqueue on `stream`, allocate nothing and are deterministic
+ * (fixed-order sums, no float atomics). */
+vp_status vp_tome_split(const vp_shape *shape, int64_t M, int32_t nspecial, int64_t *g,
+                        int64_t *nrows);
+size_t vp_tome_workspace_bytes(const vp_shape *shape);
+vp_status vp_tome_plan(const vp_shape *shape, const void *K, int64_t M, int32_t nspecial,
+                       int32_t *row, int32_t *row_start, int32_t *members, int32_t *best,
+                       float *score, void *ws, size_t ws_bytes, void *stream);
+vp_status vp_tome_merge(const vp_shape *shape, const void *X, int64_t nrows,
+                        const int32_t *row_start, const int32_t *members, void *Xm,
+                        void *stream);
+vp_status vp_tome_unmerge(const vp_shape *shape, const void *Ym, int64_t nrows,
+                          const int32_t *row, void *Y, void *stream);
 
 /* Static description of a status code. */
 const char *vp_status_string(vp_status s);

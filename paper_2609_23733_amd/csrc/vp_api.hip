@@ -563,3 +563,112 @@ vp_status vp_latent_loss(const vp_shape* shape, const void* D_hat, const void* D
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------ token merging
+
+namespace {
+
+int64_t tome_sources(int64_t S, int64_t np, int64_t g) {
+    return (S - 1) * (np - (np + g - 1) / g);
+}
+
+bool tome_geom(const vp_shape* s, int64_t M, int32_t nsp, vp::TomeGeom* G) {
+    if (shape_status(s) != VP_OK) return false;
+    const int64_t S = s->S, P = s->P, N = S * P;
+    if (nsp < 0 || nsp >= P || M < 0) return false;
+    const int64_t np = P - nsp;
+    if (M > tome_sources(S, np, np)) return false;
+    // smallest g in [1, np] with at least M sources (the count grows with g)
+    int64_t lo = 1, hi = np;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (tome_sources(S, np, mid) >= M) hi = mid;
+        else lo = mid + 1;
+    }
+    G->N = N;
+    G->P = P;
+    G->nsp = nsp;
+    G->np = np;
+    G->g = lo;
+    G->ndp = (np + lo - 1) / lo;
+    G->nsv = np - G->ndp;
+    G->nA = (S - 1) * G->nsv;
+    G->nD = N - G->nA;
+    return true;
+}
+
+}  // namespace
+
+vp_status vp_tome_split(const vp_shape* shape, int64_t M, int32_t nspecial, int64_t* g,
+                        int64_t* nrows) {
+    vp::TomeGeom G;
+    if (!tome_geom(shape, M, nspecial, &G)) return VP_ERR_INVALID_ARG;
+    if (g) *g = G.g;
+    if (nrows) *nrows = G.N - M;
+    return VP_OK;
+}
+
+size_t vp_tome_workspace_bytes(const vp_shape* shape) {
+    if (shape_status(shape) != VP_OK) return 0;
+    return align_up(vp::tome_workspace_bytes(shape->S * shape->P));
+}
+
+vp_status vp_tome_plan(const vp_shape* shape, const void* K, int64_t M, int32_t nspecial,
+                       int32_t* row, int32_t* row_start, int32_t* members, int32_t* best,
+                       float* score, void* ws, size_t ws_bytes, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (shape->dtype != VP_BF16) return VP_ERR_UNSUPPORTED;
+    vp::TomeGeom G;
+    if (!tome_geom(shape, M, nspecial, &G)) return VP_ERR_INVALID_ARG;
+    if (!K || !aligned16(K) || !row || !row_start || !members || !aligned4(row) ||
+        !aligned4(row_start) || !aligned4(members) || (best && !aligned4(best)) ||
+        (score && !aligned4(score)))
+        return VP_ERR_INVALID_ARG;
+    if (!ws || ((uintptr_t)ws & (kAlign - 1))) return VP_ERR_INVALID_ARG;
+    if (ws_bytes < vp::tome_workspace_bytes(G.N)) return VP_ERR_WORKSPACE;
+    vp::TomeArgs a;
+    a.G = G;
+    a.M = M;
+    a.K = (const __bf16*)K;
+    a.H = shape->H;
+    a.row = row;
+    a.row_start = row_start;
+    a.members = members;
+    a.best = best;
+    a.score = score;
+    a.ws = ws;
+    (void)hipGetLastError();
+    vp::launch_tome_plan(a, (hipStream_t)stream);
+    return hip_status("vp_tome_plan");
+}
+
+vp_status vp_tome_merge(const vp_shape* shape, const void* X, int64_t nrows,
+                        const int32_t* row_start, const int32_t* members, void* Xm,
+                        void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    const int64_t N = shape->S * shape->P;
+    if (!X || !Xm || !aligned16(X) || !aligned16(Xm) || !row_start || !members ||
+        !aligned4(row_start) || !aligned4(members) || nrows < 1 || nrows > N)
+        return VP_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    vp::launch_tome_merge(shape->dtype == VP_BF16 ? 1 : 0, X, N, shape->H * VP_HEAD_DIM, nrows,
+                          row_start, members, Xm, (hipStream_t)stream);
+    return hip_status("vp_tome_merge");
+}
+
+vp_status vp_tome_unmerge(const vp_shape* shape, const void* Ym, int64_t nrows,
+                          const int32_t* row, void* Y, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    const int64_t N = shape->S * shape->P;
+    if (!Ym || !Y || !aligned16(Ym) || !aligned16(Y) || !row || !aligned4(row) || nrows < 1 ||
+        nrows > N)
+        return VP_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    vp::launch_tome_unmerge(shape->dtype == VP_BF16 ? 1 : 0, Ym, nrows, row, N,
+                            shape->H * VP_HEAD_DIM, Y, (hipStream_t)stream);
+    return hip_status("vp_tome_unmerge");
+}
+

@@ -94,6 +94,58 @@ void launch_router_loss(const LossArgs& a, hipStream_t st);
 void launch_latent_loss(const LossArgs& a, hipStream_t st);
 size_t distill_part_bytes(int H);
 
+// Token merging before the routed attention: the destination / source
+// lattice of the bipartite matching, in closed form.  Destinations: every
+// token of view 0, the nsp special tokens of every view, and in views 1..
+// the patches k (index among the view's np patches) with k % g == 0;
+// sources: the other patches.  Destination slots and source indices both
+// follow token order.
+struct TomeGeom {
+    int64_t N, P;     // tokens, tokens per view
+    int64_t nsp, np;  // special tokens and patches per view
+    int64_t g;        // patch stride of the destinations
+    int64_t ndp;      // destination patches per view (views 1..)
+    int64_t nsv;      // sources per view (views 1..)
+    int64_t nD, nA;   // destinations, sources
+};
+__host__ __device__ inline int64_t tome_dst_token(const TomeGeom& G, int64_t j) {
+    if (j < G.P) return j;
+    const int64_t per = G.nsp + G.ndp, jj = j - G.P, q = jj / per, w = jj - q * per;
+    return (1 + q) * G.P + (w < G.nsp ? w : G.nsp + (w - G.nsp) * G.g);
+}
+__host__ __device__ inline int64_t tome_src_token(const TomeGeom& G, int64_t i) {
+    const int64_t q = i / G.nsv, w = i - q * G.nsv;
+    const int64_t b = w / (G.g - 1), o = w - b * (G.g - 1);
+    return (1 + q) * G.P + G.nsp + b * G.g + 1 + o;
+}
+// Destination slot of token t (>= 0), or -1 - (source index) for a source.
+__host__ __device__ inline int64_t tome_slot(const TomeGeom& G, int64_t t) {
+    if (t < G.P) return t;
+    const int64_t v = t / G.P, j = t - v * G.P, per = G.nsp + G.ndp;
+    if (j < G.nsp) return G.P + (v - 1) * per + j;
+    const int64_t k = j - G.nsp, q = k / G.g, r = k - q * G.g;
+    if (r == 0) return G.P + (v - 1) * per + G.nsp + q;
+    return -1 - ((v - 1) * G.nsv + q * (G.g - 1) + r - 1);
+}
+struct TomeArgs {
+    TomeGeom G;
+    int64_t M;             // sources to merge (rows = N - M)
+    const __bf16* K;       // [N, H, 64]
+    int H;
+    int32_t* row;          // [N]
+    int32_t* row_start;    // [N - M + 1]
+    int32_t* members;      // [N]
+    int32_t* best;         // [N] or null
+    float* score;          // [N] or null
+    void* ws;              // tome_workspace_bytes(N)
+};
+size_t tome_workspace_bytes(int64_t N);
+void launch_tome_plan(const TomeArgs& a, hipStream_t st);
+void launch_tome_merge(int dt, const void* X, int64_t N, int F, int64_t nrows,
+                       const int32_t* row_start, const int32_t* members, void* Xm, hipStream_t st);
+void launch_tome_unmerge(int dt, const void* Ym, int64_t nrows, const int32_t* row, int64_t N,
+                         int F, void* Y, hipStream_t st);
+
 void launch_router(const RouterArgs& a, hipStream_t st);
 void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,
                           int dtype, float* logits, hipStream_t st);

@@ -32,7 +32,9 @@ EXPORTS = ("vp_workspace_bytes", "vp_router_score", "vp_router_logits", "vp_assi
            "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
            "vp_linear_heads", "vp_status_string", "vp_last_error", "vp_block_workspace_bytes",
            "vp_block_qkv", "vp_block_out", "vp_teacher_workspace_bytes", "vp_loss_workspace_bytes",
-           "vp_teacher_targets", "vp_router_loss", "vp_latent_loss")
+           "vp_teacher_targets", "vp_router_loss", "vp_latent_loss", "vp_tome_split",
+           "vp_tome_workspace_bytes", "vp_tome_plan", "vp_tome_merge", "vp_tome_unmerge")
+TOME_SPECIAL = 5   # special tokens per view (camera + registers), never merged
 MODEL_DIM = MAX_HEADS * HEAD_DIM
 BLOCK_VECS = ("ln1_w", "ln1_b", "b_qkv", "b_o", "ls1", "ln2_w", "ln2_b", "b_fc1", "b_fc2", "ls2")
 BLOCK_MATS = ("w_qkv", "w_o", "w_fc1", "w_fc2")
@@ -117,6 +119,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    f32, P, P, f32, P, P, ctypes.c_size_t, P]
     lib.vp_latent_loss.argtypes = [ctypes.POINTER(vp_shape), P, P, ctypes.c_int, f32, P, P,
                                    ctypes.c_size_t, P]
+    lib.vp_tome_split.argtypes = [ctypes.POINTER(vp_shape), i64, i32, ctypes.POINTER(i64),
+                                  ctypes.POINTER(i64)]
+    lib.vp_tome_workspace_bytes.argtypes = [ctypes.POINTER(vp_shape)]
+    lib.vp_tome_workspace_bytes.restype = ctypes.c_size_t
+    lib.vp_tome_plan.argtypes = [ctypes.POINTER(vp_shape), P, i64, i32, P, P, P, P, P, P,
+                                 ctypes.c_size_t, P]
+    lib.vp_tome_merge.argtypes = [ctypes.POINTER(vp_shape), P, i64, P, P, P, P]
+    lib.vp_tome_unmerge.argtypes = [ctypes.POINTER(vp_shape), P, i64, P, P, P]
+    for f in ("vp_tome_split", "vp_tome_plan", "vp_tome_merge", "vp_tome_unmerge"):
+        getattr(lib, f).restype = ctypes.c_int
     for f in ("vp_router_score", "vp_router_logits", "vp_assign_heads",
               "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
               "vp_linear_heads", "vp_block_qkv", "vp_block_out", "vp_teacher_targets",
@@ -584,3 +596,108 @@ def latent_loss(D_hat, D_t, S: int, P: int, lam: float = 1.0):
                                          float(lam), _ptr(loss), _ptr(ws), ws.numel(),
                                          _stream()), "vp_latent_loss")
     return loss
+
+
+# ------------------------------------------------------------ token merging
+
+def tome_split(S: int, P: int, M: int, nspecial: int = TOME_SPECIAL):
+    """(g, nrows) for merging M of the S*P tokens (host only)."""
+    shp = make_shape(S, P, MAX_HEADS, torch.bfloat16)
+    g, nrows = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(load_library().vp_tome_split(ctypes.byref(shp), int(M), int(nspecial),
+                                        ctypes.byref(g), ctypes.byref(nrows)), "vp_tome_split")
+    return g.value, nrows.value
+
+
+def tome_workspace_bytes(S: int, P: int) -> int:
+    return load_library().vp_tome_workspace_bytes(
+        ctypes.byref(make_shape(S, P, MAX_HEADS, torch.bfloat16)))
+
+
+class TomePlan:
+    """Device arrays of a merge plan: row [N], row_start [nrows + 1], members
+    [N] (int32), and optionally best [N] int32 / score [N] fp32."""
+
+    def __init__(self, S, P, M, nspecial=TOME_SPECIAL, device="cuda", want_best=False):
+        self.S, self.P, self.M, self.nspecial = S, P, M, nspecial
+        self.g, self.nrows = tome_split(S, P, M, nspecial)
+        N = S * P
+        self.row = torch.empty(N, dtype=torch.int32, device=device)
+        self.row_start = torch.empty(self.nrows + 1, dtype=torch.int32, device=device)
+        self.members = torch.empty(N, dtype=torch.int32, device=device)
+        self.best = torch.empty(N, dtype=torch.int32, device=device) if want_best else None
+        self.score = torch.empty(N, dtype=torch.float32, device=device) if want_best else None
+        self.ws = torch.empty(tome_workspace_bytes(S, P), dtype=torch.uint8, device=device)
+
+
+def tome_plan(K, plan: TomePlan) -> TomePlan:
+    """Fill `plan` from the keys K [N, H, 64] (bf16)."""
+    S, P = plan.S, plan.P
+    N, H = S * P, K.shape[1]
+    _need(K, "K", (N, H, HEAD_DIM), torch.bfloat16)
+    shp = make_shape(S, P, H, K.dtype)
+    _check(load_library().vp_tome_plan(ctypes.byref(shp), _ptr(K), int(plan.M),
+                                       int(plan.nspecial), _ptr(plan.row), _ptr(plan.row_start),
+                                       _ptr(plan.members), _ptr(plan.best), _ptr(plan.score),
+                                       _ptr(plan.ws), plan.ws.numel(), _stream()), "vp_tome_plan")
+    return plan
+
+
+def tome_merge(X, plan: TomePlan, out=None):
+    """Rows of the merged sequence: X [N, H, 64] -> [nrows, H, 64] (means)."""
+    N, H = plan.S * plan.P, X.shape[1]
+    _need(X, "X", (N, H, HEAD_DIM))
+    if out is None:
+        out = torch.empty(plan.nrows, H, HEAD_DIM, dtype=X.dtype, device=X.device)
+    _need(out, "out", (plan.nrows, H, HEAD_DIM), X.dtype)
+    shp = make_shape(plan.S, plan.P, H, X.dtype)
+    _check(load_library().vp_tome_merge(ctypes.byref(shp), _ptr(X), plan.nrows,
+                                        _ptr(plan.row_start), _ptr(plan.members), _ptr(out),
+                                        _stream()), "vp_tome_merge")
+    return out
+
+
+def tome_unmerge(Ym, plan: TomePlan, out=None):
+    """Every token takes its row's output: [nrows, H, 64] -> [N, H, 64]."""
+    N, H = plan.S * plan.P, Ym.shape[1]
+    _need(Ym, "Ym", (plan.nrows, H, HEAD_DIM))
+    if out is None:
+        out = torch.empty(N, H, HEAD_DIM, dtype=Ym.dtype, device=Ym.device)
+    _need(out, "out", (N, H, HEAD_DIM), Ym.dtype)
+    shp = make_shape(plan.S, plan.P, H, Ym.dtype)
+    _check(load_library().vp_tome_unmerge(ctypes.byref(shp), _ptr(Ym), plan.nrows,
+                                          _ptr(plan.row), _ptr(out), _stream()),
+           "vp_tome_unmerge")
+    return out
+
+
+class TomeLayer:
+    """Token merging around a routed layer: the plan from K, Q/K/V merged, the
+    routed layer on the nrows merged rows (one sequence), its output unmerged
+    to all S*P tokens."""
+
+    def __init__(self, inp, M: int, nspecial: int = TOME_SPECIAL, device="cuda",
+                 want_best=False, **layer_kw):
+        import dataclasses
+        x = inp.to(device)
+        self.x = x
+        self.plan = TomePlan(x.S, x.P, M, nspecial, device, want_best)
+        nr = self.plan.nrows
+        mk = lambda: torch.empty(nr, x.H, HEAD_DIM, dtype=x.Q.dtype, device=device)
+        self.Qm, self.Km, self.Vm = mk(), mk(), mk()
+        merged = dataclasses.replace(x, S=1, P=nr, Q=self.Qm, K=self.Km, V=self.Vm)
+        self.layer = RoutedLayer(merged, device=device, **layer_kw)
+        self.Y = torch.empty(x.N, x.H, HEAD_DIM, dtype=self.layer.y_dtype, device=device)
+
+    def step(self, Q=None, K=None, V=None, events=None) -> torch.Tensor:
+        x = self.x
+        Q = x.Q if Q is None else Q
+        K = x.K if K is None else K
+        V = x.V if V is None else V
+        tome_plan(K, self.plan)
+        tome_merge(Q, self.plan, self.Qm)
+        tome_merge(K, self.plan, self.Km)
+        tome_merge(V, self.plan, self.Vm)
+        Ym = self.layer.step(events=events)
+        return tome_unmerge(Ym, self.plan, self.Y)
+

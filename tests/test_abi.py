@@ -285,3 +285,45 @@ def test_distill_validation(lib):
     assert ll(dt=3) == vp.VP_ERR_INVALID_ARG
     assert ll(lam=float("nan")) == vp.VP_ERR_INVALID_ARG
     assert ll(nb=16) == vp.VP_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("S,P,M", [(3, 15, 12), (3, 15, 10), (2, 1374, 1000), (4, 9, 0),
+                                   (100, 1374, 123660), (100, 1374, 103050), (500, 1374, 515250)])
+def test_tome_split_matches_oracle(lib, S, P, M):
+    import oracle
+    is_dst, g = oracle.tome_split(S, P, M)
+    gg, nrows = vp.tome_split(S, P, M)
+    assert gg == g and nrows == S * P - M
+
+
+def test_tome_validation(lib):
+    g, nr = ctypes.c_int64(0), ctypes.c_int64(0)
+    sp = lambda shp=None, M=12, ns=5: lib.vp_tome_split(ctypes.byref(shp or shape(S=3, P=15)), M,
+                                                        ns, ctypes.byref(g), ctypes.byref(nr))
+    assert sp() == vp.VP_OK and g.value == 3 and nr.value == 33
+    # 10 patches per view: at most 2 x 9 sources (patch 0 of a view is always a destination)
+    assert sp(M=18) == vp.VP_OK and g.value == 10 and sp(M=19) == vp.VP_ERR_INVALID_ARG
+    assert sp(M=-1) == vp.VP_ERR_INVALID_ARG
+    assert sp(ns=15) == vp.VP_ERR_INVALID_ARG and sp(ns=-1) == vp.VP_ERR_INVALID_ARG
+    assert sp(shp=shape(S=1, P=15), M=1) == vp.VP_ERR_INVALID_ARG
+    assert sp(shp=shape(S=1, P=15), M=0) == vp.VP_OK and nr.value == 15
+    assert lib.vp_tome_workspace_bytes(ctypes.byref(shape(S=3, P=15))) > 0
+    pl = lambda shp=None, K=FAKE, M=12, row=FAKE, rs_=FAKE, mem=FAKE, best=None, ws=FAKE, \
+        nb=1 << 40: lib.vp_tome_plan(ctypes.byref(shp or shape(S=3, P=15)), K, M, 5, row, rs_,
+                                     mem, best, None, ws, nb, None)
+    assert pl(shp=shape(S=3, P=15, dt=vp.VP_F32)) == vp.VP_ERR_UNSUPPORTED
+    assert pl(K=None) == vp.VP_ERR_INVALID_ARG and pl(K=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+    assert pl(M=40) == vp.VP_ERR_INVALID_ARG
+    assert pl(row=None) == vp.VP_ERR_INVALID_ARG and pl(mem=FAKE + 2) == vp.VP_ERR_INVALID_ARG
+    assert pl(best=FAKE + 1) == vp.VP_ERR_INVALID_ARG
+    assert pl(ws=None) == vp.VP_ERR_INVALID_ARG and pl(ws=FAKE + 64) == vp.VP_ERR_INVALID_ARG
+    assert pl(nb=1024) == vp.VP_ERR_WORKSPACE
+    mg = lambda X=FAKE, nrows=33, rs_=FAKE, out=FAKE: lib.vp_tome_merge(
+        ctypes.byref(shape(S=3, P=15)), X, nrows, rs_, FAKE, out, None)
+    assert mg(X=None) == vp.VP_ERR_INVALID_ARG and mg(out=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+    assert mg(nrows=0) == vp.VP_ERR_INVALID_ARG and mg(nrows=46) == vp.VP_ERR_INVALID_ARG
+    assert mg(rs_=None) == vp.VP_ERR_INVALID_ARG
+    um = lambda Y=FAKE, nrows=33, row=FAKE: lib.vp_tome_unmerge(
+        ctypes.byref(shape(S=3, P=15)), FAKE, nrows, row, Y, None)
+    assert um(Y=None) == vp.VP_ERR_INVALID_ARG and um(row=FAKE + 2) == vp.VP_ERR_INVALID_ARG
+    assert um(nrows=-1) == vp.VP_ERR_INVALID_ARG
