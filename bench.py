@@ -297,6 +297,57 @@ def run_teacher(S, steps, warmup):
                           "algorithmic_flop_per_launch": fl})
 
 
+def run_tome(S, n_full, ratios, steps, warmup, unmerged_ms):
+    """Token merging around the routed layer (the paper's ToMe combination):
+    plan, merge of Q/K/V, the routed layer on the merged rows, unmerge; HIP-
+    event time of each stage, and the speedup over the unmerged layer."""
+    import torch
+    from paper_2609_23733_amd import synth, vp
+    x = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=n_full, key=(S, 0), qkv_device="cuda")
+    N = S * P_TOKENS
+    out = []
+    for ratio in ratios:
+        M = int(ratio * N)
+        tl = vp.TomeLayer(x, M, y_dtype=torch.bfloat16)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+
+        def step(rec):
+            if rec:
+                ev[0].record()
+            vp.tome_plan(x.K, tl.plan)
+            if rec:
+                ev[1].record()
+            vp.tome_merge(x.Q, tl.plan, tl.Qm)
+            vp.tome_merge(x.K, tl.plan, tl.Km)
+            vp.tome_merge(x.V, tl.plan, tl.Vm)
+            if rec:
+                ev[2].record()
+            Ym = tl.layer.step()
+            if rec:
+                ev[3].record()
+            vp.tome_unmerge(Ym, tl.plan, tl.Y)
+            if rec:
+                ev[4].record()
+        for _ in range(warmup):
+            step(False)
+        torch.cuda.synchronize()
+        acc = [0.0] * 4
+        for _ in range(steps):
+            step(True)
+            torch.cuda.synchronize()
+            for i in range(4):
+                acc[i] += ev[i].elapsed_time(ev[i + 1])
+        t = [a / steps for a in acc]
+        tot = sum(t)
+        out.append(dict(ratio=ratio, M=M, rows=tl.plan.nrows, stride_g=tl.plan.g,
+                        plan_ms=round(t[0], 4), merge_ms=round(t[1], 4), layer_ms=round(t[2], 4),
+                        unmerge_ms=round(t[3], 4), total_ms=round(tot, 4),
+                        speedup_vs_unmerged=round(unmerged_ms / tot, 2)))
+        del tl
+        torch.cuda.empty_cache()
+    return dict(S=S, N=N, n_full=n_full, unmerged_layer_ms=round(unmerged_ms, 4), by_ratio=out)
+
+
 def cpu_baseline(x, rows_per_head=640):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
@@ -341,6 +392,7 @@ def main():
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--no-block", action="store_true")
     ap.add_argument("--no-teacher", action="store_true")
+    ap.add_argument("--no-tome", action="store_true")
     ap.add_argument("--stack", type=int, default=0, metavar="S",
                     help="also time a 24-block stack at S views (e.g. 500)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -375,6 +427,10 @@ def main():
     block = None
     if not args.no_block:
         block = run_block(100, args.n_full, args.steps, args.warmup)
+    tome = None
+    if not args.no_tome:
+        tome = run_tome(100, args.n_full, (0.75, 0.9), max(3, args.steps // 2), 2, head["ms"])
+        torch.cuda.empty_cache()
     teacher = None
     if not args.no_teacher:
         teacher = run_teacher(100, max(2, args.steps // 4), 1)
@@ -430,6 +486,8 @@ def main():
         out["variants"] = variants
     if block is not None:
         out["block"] = block
+    if tome is not None:
+        out["tome"] = tome
     if teacher is not None:
         out["teacher"] = teacher
     if stack is not None:

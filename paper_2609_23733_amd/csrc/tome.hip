@@ -78,22 +78,27 @@ __global__ __launch_bounds__(256) void k_tome_metric(const bf16* __restrict__ K,
 }
 
 // ---------------------------------------------------------------- T2
-// One workgroup = kTmWaves waves x 64 sources; each wave keeps its source
-// rows as the MFMA's A operand.  Destination tiles of 64 rows (metric,
-// 1 / |m| and a -inf bias past the last destination) stream through LDS,
-// double-buffered.  Per score: v = dot / |m_d| (an FMA with the bias), a
-// compare and two selects; each lane sees its destinations in increasing
-// slot order and keeps the first maximum, the final reduction over lanes
-// prefers the lower slot on equal values.
+// One workgroup = kTmWaves waves x 64 sources and one chunk of the
+// destination tiles (blockIdx.y; chunks split the work finely enough to fill
+// the chip); each wave keeps its source rows as the MFMA's A operand.
+// Destination tiles of 64 rows (metric, 1 / |m| and a -inf bias past the last
+// destination) stream through LDS, double-buffered.  Per score:
+// v = dot / |m_d| (an FMA with the bias), a compare and two selects; each
+// lane sees its destinations in increasing slot order and keeps the first
+// maximum, the final reduction over lanes prefers the lower slot on equal
+// values.  The chunk's (value, slot) per source goes to a partial record;
+// k_tome_match_final takes the chunks in order (a later chunk wins only when
+// strictly larger), so ties still go to the lowest slot.
 constexpr int kTmWaves = 4;
 constexpr int kTmSrc = 64 * kTmWaves;
+constexpr int kTmChunks = 4;          // most destination chunks
+constexpr int kTmTargetGroups = 1024; // workgroups the split aims for
 
 __global__ __launch_bounds__(64 * kTmWaves) void k_tome_match(const bf16* __restrict__ m,
                                                               const float* __restrict__ invn,
                                                               TomeGeom G,
-                                                              int32_t* __restrict__ best,
-                                                              float* __restrict__ score,
-                                                              uint64_t* __restrict__ key) {
+                                                              float* __restrict__ pval,
+                                                              int32_t* __restrict__ pidx) {
     constexpr int kThreads = 64 * kTmWaves;
     constexpr int kSegs = 64 * 8 / kThreads;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, n = lane & 31, hh = lane >> 5;
@@ -144,11 +149,12 @@ __global__ __launch_bounds__(64 * kTmWaves) void k_tome_match(const bf16* __rest
             acc[kb][r] = -INFINITY;
             idx[kb][r] = 0;
         }
-    const int64_t nt = (G.nD + 63) / 64;
-    gload(0);
-    lstore(0, 0);
+    const int64_t ntt = (G.nD + 63) / 64, C = gridDim.y;
+    const int64_t t0 = blockIdx.y * ntt / C, nt = (blockIdx.y + 1) * ntt / C;
+    gload(t0);
+    lstore(t0, (int)(t0 & 1));
     __syncthreads();
-    for (int64_t t = 0; t < nt; ++t) {
+    for (int64_t t = t0; t < nt; ++t) {
         const int b = (int)(t & 1);
         if (t + 1 < nt) gload(t + 1);
 #pragma unroll
@@ -197,20 +203,45 @@ __global__ __launch_bounds__(64 * kTmWaves) void k_tome_match(const bf16* __rest
             idx[kb][r] = j;
         }
     if (n == 0) {
+        const int64_t base = (int64_t)blockIdx.y * G.nA;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int64_t i = i0 + 32 * kb + 8 * (r >> 2) + 4 * hh + (r & 3);
                 if (i < G.nA) {
-                    const int64_t tok = tome_src_token(G, i);
-                    const float sc = acc[kb][r] * invn[tok] + 0.f;   // + 0: no -0
-                    best[i] = idx[kb][r];
-                    score[i] = sc;
-                    key[i] = ((uint64_t)float_order(sc) << 32) | (uint64_t)(~(uint32_t)tok);
+                    pval[base + i] = acc[kb][r];
+                    pidx[base + i] = idx[kb][r];
                 }
             }
     }
+}
+
+// Per source: the best over the chunks, its cosine similarity and its
+// selection key (similarity, then the lower token).
+__global__ __launch_bounds__(256) void k_tome_match_final(TomeGeom G, int C,
+                                                          const float* __restrict__ pval,
+                                                          const int32_t* __restrict__ pidx,
+                                                          const float* __restrict__ invn,
+                                                          int32_t* __restrict__ best,
+                                                          float* __restrict__ score,
+                                                          uint64_t* __restrict__ key) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= G.nA) return;
+    float v = pval[i];
+    int32_t j = pidx[i];
+    for (int c = 1; c < C; ++c) {
+        const float w = pval[(int64_t)c * G.nA + i];
+        if (w > v) {
+            v = w;
+            j = pidx[(int64_t)c * G.nA + i];
+        }
+    }
+    const int64_t tok = tome_src_token(G, i);
+    const float sc = v * invn[tok] + 0.f;   // + 0: no -0
+    best[i] = j;
+    score[i] = sc;
+    key[i] = ((uint64_t)float_order(sc) << 32) | (uint64_t)(~(uint32_t)tok);
 }
 
 // ---------------------------------------------------------------- T3
@@ -557,7 +588,7 @@ __global__ __launch_bounds__(256) void k_tome_unmerge(const u32x4* __restrict__ 
 // Workspace of the plan for N tokens.
 struct TomeWs {
     size_t m, invn, bslot, score, key, st, ghist, mflag, pos, kept, cnt, off, size, lk0, lv0,
-        lk1, lv1, bsum, hist, total;
+        lk1, lv1, bsum, hist, pval, pidx, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -592,6 +623,8 @@ TomeWs tome_ws(int64_t N) {
     w.lv1 = take(n * 4);
     w.bsum = take(((256 * nbr > n ? 256 * nbr : n) / kScanBlock + 2) * 4 + nbs * 4);
     w.hist = take(256 * nbr * 4);
+    w.pval = take(n * kTmChunks * 4);
+    w.pidx = take(n * kTmChunks * 4);
     w.total = o;
     return w;
 }
@@ -627,9 +660,17 @@ void launch_tome_plan(const TomeArgs& a, hipStream_t st) {
     if (G.nA > 0) {
         hipLaunchKernelGGL(k_tome_metric, dim3(grid256(N * 8)), dim3(256), 0, st, a.K, N, a.H, m,
                            invn);
-        hipLaunchKernelGGL(k_tome_match, dim3((unsigned)((G.nA + kTmSrc - 1) / kTmSrc)),
-                           dim3(64 * kTmWaves), 0, st, (const bf16*)m, (const float*)invn, G,
-                           bslot, score, key);
+        const int64_t ns = (G.nA + kTmSrc - 1) / kTmSrc, ntt = (G.nD + 63) / 64;
+        int64_t C = (kTmTargetGroups + ns - 1) / ns;
+        C = C < 1 ? 1 : (C > kTmChunks ? kTmChunks : C);
+        C = C > ntt ? ntt : C;
+        float* pval = (float*)(ws + w.pval);
+        int32_t* pidx = (int32_t*)(ws + w.pidx);
+        hipLaunchKernelGGL(k_tome_match, dim3((unsigned)ns, (unsigned)C), dim3(64 * kTmWaves), 0,
+                           st, (const bf16*)m, (const float*)invn, G, pval, pidx);
+        hipLaunchKernelGGL(k_tome_match_final, dim3(grid256(G.nA)), dim3(256), 0, st, G, (int)C,
+                           (const float*)pval, (const int32_t*)pidx, (const float*)invn, bslot,
+                           score, key);
         if (M > 0) {
             const unsigned gh = (unsigned)((G.nA + 4095) / 4096);
             for (int shift = 56; shift >= 0; shift -= 8) {
