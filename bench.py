@@ -211,10 +211,12 @@ def run_block(S, n_full, steps, warmup):
                           "algorithmic_flop_per_launch": fl})
 
 
-def run_stack(S, layers, steps, warmup):
+def run_stack(S, layers, steps, warmup, tome_ratio=None):
     """A stack of global blocks with independent seeded weights, layer l + 1
     taking layer l's output; FULL-head counts drawn from {1, ..., 6} per
-    layer.  Per-layer latency from HIP events around each block."""
+    layer.  Per-layer latency from HIP events around each block.  With
+    ``tome_ratio``, every block merges that fraction of its tokens before its
+    routed layer and unmerges after it."""
     import numpy as np
     import torch
     from paper_2609_23733_amd import synth, vp
@@ -222,9 +224,10 @@ def run_stack(S, layers, steps, warmup):
     n_full = rng.integers(1, 7, size=layers)
     sh = vp.PrimeBlock.make_shared(S, P_TOKENS)
     pos = torch.from_numpy(synth.token_positions(S, P_TOKENS)).cuda()
+    M = None if tome_ratio is None else int(tome_ratio * S * P_TOKENS)
     blocks = [vp.PrimeBlock(synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=int(n_full[l]),
                                              key=(S, 100 + l), with_qkv=False),
-                            synth.make_block_weights((S, 100 + l)), pos, shared=sh)
+                            synth.make_block_weights((S, 100 + l)), pos, shared=sh, tome_M=M)
               for l in range(layers)]
     X0 = synth.make_block_input(S, P_TOKENS, key=(S, 100), device="cuda")
     X = torch.empty_like(X0)
@@ -249,9 +252,15 @@ def run_stack(S, layers, steps, warmup):
         per += [a.elapsed_time(b) for a, b in evs]
     per /= steps
     got = [int((b.layer.modes == 2).sum()) for b in blocks]
-    return dict(S=S, N=S * P_TOKENS, layers=layers, n_full=got,
-                per_layer_ms=[round(float(v), 3) for v in per],
-                total_ms=round(float(per.sum()), 3))
+    out = dict(S=S, N=S * P_TOKENS, layers=layers, n_full=got,
+               per_layer_ms=[round(float(v), 3) for v in per],
+               total_ms=round(float(per.sum()), 3))
+    if tome_ratio is not None:
+        out = dict(tome_ratio=tome_ratio, merged_rows=blocks[0].tome.plan.nrows,
+                   total_ms=out["total_ms"], per_layer_ms=out["per_layer_ms"], n_full=got)
+    del blocks, sh
+    torch.cuda.empty_cache()
+    return out
 
 
 def run_teacher(S, steps, warmup):
@@ -438,6 +447,9 @@ def main():
     stack = None
     if args.stack:
         stack = run_stack(args.stack, 24, 2, 1)
+        stack["tome"] = [run_stack(args.stack, 24, 2, 1, r) for r in (0.75, 0.9)]
+        for t in stack["tome"]:
+            t["speedup_vs_unmerged_stack"] = round(stack["total_ms"] / t["total_ms"], 2)
     if not args.no_sweep:
         for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16), (500, 4)):
             r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 0))

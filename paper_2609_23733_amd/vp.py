@@ -494,10 +494,13 @@ def block_out(X, Y, w, S: int, P: int, ws: torch.Tensor, X_out=None):
 class PrimeBlock:
     """One global-attention block of Algorithm 1 on the GPU: block_qkv, the
     routed layer on the block's own Q, K, V (router_score, [router_logits],
-    assign_heads, routed_global_attention) and block_out."""
+    assign_heads, routed_global_attention) and block_out; with ``tome_M``, the
+    routed layer runs on the block's tokens merged down by tome_M (TomeLayer)
+    and its output is unmerged before block_out."""
 
     def __init__(self, layer_inp, block_w: Dict[str, torch.Tensor], pos, device="cuda",
-                 shared: Optional[Dict[str, torch.Tensor]] = None, **layer_kw):
+                 shared: Optional[Dict[str, torch.Tensor]] = None,
+                 tome_M: Optional[int] = None, **layer_kw):
         """``shared``: buffers that blocks run one after another on one stream
         may share (make_shared()); allocated per block when not given."""
         self.S, self.P = layer_inp.S, layer_inp.P
@@ -505,8 +508,14 @@ class PrimeBlock:
         self.w = {k: v.to(device) for k, v in block_w.items()}
         self.pos = pos if isinstance(pos, torch.Tensor) and pos.is_cuda else \
             torch.as_tensor(pos, dtype=torch.int32).to(device)
-        self.layer = RoutedLayer(layer_inp, y_dtype=torch.bfloat16, device=device,
-                                 ws=sh["layer_ws"], Y=sh["Y"], **layer_kw)
+        if tome_M is None:
+            self.tome = None
+            self.layer = RoutedLayer(layer_inp, y_dtype=torch.bfloat16, device=device,
+                                     ws=sh["layer_ws"], Y=sh["Y"], **layer_kw)
+        else:
+            self.tome = TomeLayer(layer_inp, tome_M, device=device, y_dtype=torch.bfloat16,
+                                  Y=sh["Y"], **layer_kw)
+            self.layer = self.tome.layer
         self.ws = sh["block_ws"]
         self.Q, self.K, self.V = sh["Q"], sh["K"], sh["V"]
 
@@ -530,7 +539,10 @@ class PrimeBlock:
         block_qkv(X, self.pos, self.w, self.S, self.P, self.ws, self.Q, self.K, self.V)
         rec(0, 1)
         rec(1, 0)
-        Y = self.layer.step(self.Q, self.K, self.V)
+        if self.tome is None:
+            Y = self.layer.step(self.Q, self.K, self.V)
+        else:
+            Y = self.tome.step(self.Q, self.K, self.V)
         rec(1, 1)
         rec(2, 0)
         out = block_out(X, Y, self.w, self.S, self.P, self.ws, X_out)
@@ -677,17 +689,20 @@ class TomeLayer:
     to all S*P tokens."""
 
     def __init__(self, inp, M: int, nspecial: int = TOME_SPECIAL, device="cuda",
-                 want_best=False, **layer_kw):
+                 want_best=False, Y: Optional[torch.Tensor] = None, **layer_kw):
+        """``Y``: the unmerged output [N, H, 64] (allocated when not given)."""
         import dataclasses
         x = inp.to(device)
         self.x = x
         self.plan = TomePlan(x.S, x.P, M, nspecial, device, want_best)
         nr = self.plan.nrows
-        mk = lambda: torch.empty(nr, x.H, HEAD_DIM, dtype=x.Q.dtype, device=device)
+        dt = x.Q.dtype if x.Q is not None else torch.bfloat16
+        mk = lambda: torch.empty(nr, x.H, HEAD_DIM, dtype=dt, device=device)
         self.Qm, self.Km, self.Vm = mk(), mk(), mk()
         merged = dataclasses.replace(x, S=1, P=nr, Q=self.Qm, K=self.Km, V=self.Vm)
         self.layer = RoutedLayer(merged, device=device, **layer_kw)
-        self.Y = torch.empty(x.N, x.H, HEAD_DIM, dtype=self.layer.y_dtype, device=device)
+        self.Y = Y if Y is not None else torch.empty(x.N, x.H, HEAD_DIM,
+                                                     dtype=self.layer.y_dtype, device=device)
 
     def step(self, Q=None, K=None, V=None, events=None) -> torch.Tensor:
         x = self.x

@@ -143,3 +143,36 @@ def test_whole_block(dtype_note):
     np.testing.assert_array_equal(ref_l["modes"], modes)
     ref, _ = oracle.block_out(X, ref_l["Y"].reshape(S * P, D), wt)
     check_update(out, X, ref, "whole block")
+
+
+def test_whole_block_tome():
+    """The block with token merging before its routed layer: qkv on all
+    tokens, the plan on the block's K, the routed layer on the merged rows,
+    unmerge, out -- against the oracle's composition of the same steps with
+    the GPU's merge decisions (checked for validity against the oracle)."""
+    from paper_2609_23733_amd import vp
+    from test_gpu_tome import check_plan
+    S, P = 4, synth.TOKENS_PER_VIEW
+    M = (S * P) // 2
+    log("whole block with token merging S=4")
+    modes = np.array([2, 1, 0, 2, 2, 1, 0, 0, 1, 2, 0, 1, 2, 0, 1, 2], np.uint8)
+    lay = synth.make_layer(S, P, dtype="bf16", key=(25, 0), modes=modes)
+    wt = synth.make_block_weights((25, 0))
+    X = synth.make_block_input(S, P, key=(25, 0))
+    pos = synth.token_positions(S, P)
+    blk = vp.PrimeBlock(lay, wt, pos, tome_M=M)
+    blk.tome.plan = vp.TomePlan(S, P, M, want_best=True)
+    out = blk.step(X.cuda())
+    torch.cuda.synchronize()
+    check_plan(blk.K.cpu(), S, P, M, blk.tome.plan, "block plan")
+    row = blk.tome.plan.row.cpu().numpy().astype(np.int64)
+    nrows = blk.tome.plan.nrows
+    rq, rk, rv = oracle.block_qkv(X, pos, wt)
+    mq, mk, mv = (oracle.tome_merge(t.astype(np.float32), row, nrows) for t in (rq, rk, rv))
+    ref_l = oracle.routed_layer(mq, mk, mv, lay.W, lay.U, lay.w, lay.surr, u=lay.u, Wr=lay.Wr,
+                                br=lay.br, rule=oracle.RULE_ARGMAX)
+    np.testing.assert_array_equal(ref_l["modes"], modes)
+    Y = oracle.tome_unmerge(ref_l["Y"], row)
+    ref, _ = oracle.block_out(X, Y.reshape(S * P, D), wt)
+    check_update(out, X, ref, "whole block with merging")
+
