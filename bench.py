@@ -326,9 +326,7 @@ def run_tome(S, n_full, ratios, steps, warmup, unmerged_ms):
             vp.tome_plan(x.K, tl.plan)
             if rec:
                 ev[1].record()
-            vp.tome_merge(x.Q, tl.plan, tl.Qm)
-            vp.tome_merge(x.K, tl.plan, tl.Km)
-            vp.tome_merge(x.V, tl.plan, tl.Vm)
+            vp.tome_merge_qkv(x.Q, x.K, x.V, tl.plan, tl.Qm, tl.Km, tl.Vm)
             if rec:
                 ev[2].record()
             Ym = tl.layer.step()

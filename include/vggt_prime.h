@@ -336,6 +336,8 @@ vp_status vp_latent_loss(const vp_shape *shape, const void *D_hat, const void *D
  * vp_tome_merge: Xm[r] = mean of X[t] over the members of row r, fp32 sums
  *   in member order, one rounding; X [N, H * 64] -> Xm [nrows, H * 64] in the
  *   shape's dtype.  Member entries outside [0, N) are skipped.
+ * vp_tome_merge_qkv: vp_tome_merge of Q, K and V (bf16) in one pass over the
+ *   member lists (the same sums, in the same order).
  * vp_tome_unmerge: Y[t] = Ym[row[t]] ([nrows, H * 64] -> [N, H * 64], the
  *   shape's dtype); a row outside [0, nrows) gives zeros.
  * All three enqueue on `stream`, allocate nothing and are deterministic
@@ -349,6 +351,9 @@ vp_status vp_tome_plan(const vp_shape *shape, const void *K, int64_t M, int32_t 
 vp_status vp_tome_merge(const vp_shape *shape, const void *X, int64_t nrows,
                         const int32_t *row_start, const int32_t *members, void *Xm,
                         void *stream);
+vp_status vp_tome_merge_qkv(const vp_shape *shape, const void *Q, const void *K, const void *V,
+                            int64_t nrows, const int32_t *row_start, const int32_t *members,
+                            void *Qm, void *Km, void *Vm, void *stream);
 vp_status vp_tome_unmerge(const vp_shape *shape, const void *Ym, int64_t nrows,
                           const int32_t *row, void *Y, void *stream);
 

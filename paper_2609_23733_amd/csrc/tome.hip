@@ -573,6 +573,60 @@ __global__ __launch_bounds__(256) void k_tome_merge(const void* __restrict__ X, 
     }
 }
 
+// Q, K and V of a row at once (bf16, F = 1024 or less): the row's member
+// indices are staged in LDS first (256 per pass), so the loads of the three
+// tensors do not wait on one index each; sums in member order, as above.
+__global__ __launch_bounds__(256) void k_tome_merge_qkv(const bf16* __restrict__ Q,
+                                                        const bf16* __restrict__ K,
+                                                        const bf16* __restrict__ V, int64_t N,
+                                                        int F, const int32_t* __restrict__ row_start,
+                                                        const int32_t* __restrict__ members,
+                                                        bf16* __restrict__ Qm, bf16* __restrict__ Km,
+                                                        bf16* __restrict__ Vm) {
+    __shared__ int32_t sm[256];
+    const int64_t r = blockIdx.x;
+    int64_t b = row_start[r], e = row_start[r + 1];
+    b = b < 0 ? 0 : (b > N ? N : b);
+    e = e < b ? b : (e > N ? N : e);
+    const int f0 = threadIdx.x * 4;
+    const bool act = f0 < F;
+    float aq[4] = {0.f, 0.f, 0.f, 0.f}, ak[4] = {0.f, 0.f, 0.f, 0.f}, av[4] = {0.f, 0.f, 0.f, 0.f};
+    int c = 0;
+    for (int64_t p0 = b; p0 < e; p0 += 256) {
+        const int cnt = (int)((e - p0) < 256 ? (e - p0) : 256);
+        __syncthreads();
+        if ((int)threadIdx.x < cnt) sm[threadIdx.x] = members[p0 + threadIdx.x];
+        __syncthreads();
+        for (int j = 0; j < cnt; ++j) {
+            const int64_t t = sm[j];
+            if (t < 0 || t >= N) continue;
+            ++c;
+            if (!act) continue;
+            const bf16x4 q = *reinterpret_cast<const bf16x4*>(Q + t * F + f0);
+            const bf16x4 k = *reinterpret_cast<const bf16x4*>(K + t * F + f0);
+            const bf16x4 v = *reinterpret_cast<const bf16x4*>(V + t * F + f0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                aq[i] += bf16_to_f32(q[i]);
+                ak[i] += bf16_to_f32(k[i]);
+                av[i] += bf16_to_f32(v[i]);
+            }
+        }
+    }
+    if (!act) return;
+    const float cf = c > 0 ? (float)c : 1.f;
+    bf16x4 oq, ok, ov;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        oq[i] = (bf16)(aq[i] / cf);
+        ok[i] = (bf16)(ak[i] / cf);
+        ov[i] = (bf16)(av[i] / cf);
+    }
+    *reinterpret_cast<bf16x4*>(Qm + r * F + f0) = oq;
+    *reinterpret_cast<bf16x4*>(Km + r * F + f0) = ok;
+    *reinterpret_cast<bf16x4*>(Vm + r * F + f0) = ov;
+}
+
 // 16-byte chunks: Y[t] = Ym[row[t]] (zero for a row outside [0, nrows)).
 __global__ __launch_bounds__(256) void k_tome_unmerge(const u32x4* __restrict__ Ym, int64_t nrows,
                                                       const int32_t* __restrict__ row, int64_t N,
@@ -737,6 +791,15 @@ void launch_tome_merge(int dt, const void* X, int64_t N, int F, int64_t nrows,
     else
         hipLaunchKernelGGL(k_tome_merge<DT_F32>, dim3((unsigned)nrows), dim3(256), 0, st, X, N, F,
                            row_start, members, Xm);
+}
+
+void launch_tome_merge_qkv(const void* Q, const void* K, const void* V, int64_t N, int F,
+                           int64_t nrows, const int32_t* row_start, const int32_t* members,
+                           void* Qm, void* Km, void* Vm, hipStream_t st) {
+    if (nrows <= 0) return;
+    hipLaunchKernelGGL(k_tome_merge_qkv, dim3((unsigned)nrows), dim3(256), 0, st, (const bf16*)Q,
+                       (const bf16*)K, (const bf16*)V, N, F, row_start, members, (bf16*)Qm,
+                       (bf16*)Km, (bf16*)Vm);
 }
 
 void launch_tome_unmerge(int dt, const void* Ym, int64_t nrows, const int32_t* row, int64_t N,

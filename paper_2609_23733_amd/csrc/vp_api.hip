@@ -658,6 +658,23 @@ vp_status vp_tome_merge(const vp_shape* shape, const void* X, int64_t nrows,
     return hip_status("vp_tome_merge");
 }
 
+vp_status vp_tome_merge_qkv(const vp_shape* shape, const void* Q, const void* K, const void* V,
+                            int64_t nrows, const int32_t* row_start, const int32_t* members,
+                            void* Qm, void* Km, void* Vm, void* stream) {
+    vp_status st = shape_status(shape);
+    if (st != VP_OK) return st;
+    if (shape->dtype != VP_BF16) return VP_ERR_UNSUPPORTED;
+    const int64_t N = shape->S * shape->P;
+    if (!Q || !K || !V || !Qm || !Km || !Vm || !aligned16(Q) || !aligned16(K) || !aligned16(V) ||
+        !aligned16(Qm) || !aligned16(Km) || !aligned16(Vm) || !row_start || !members ||
+        !aligned4(row_start) || !aligned4(members) || nrows < 1 || nrows > N)
+        return VP_ERR_INVALID_ARG;
+    (void)hipGetLastError();
+    vp::launch_tome_merge_qkv(Q, K, V, N, shape->H * VP_HEAD_DIM, nrows, row_start, members, Qm,
+                              Km, Vm, (hipStream_t)stream);
+    return hip_status("vp_tome_merge_qkv");
+}
+
 vp_status vp_tome_unmerge(const vp_shape* shape, const void* Ym, int64_t nrows,
                           const int32_t* row, void* Y, void* stream) {
     vp_status st = shape_status(shape);

@@ -145,6 +145,9 @@ void launch_tome_merge(int dt, const void* X, int64_t N, int F, int64_t nrows,
                        const int32_t* row_start, const int32_t* members, void* Xm, hipStream_t st);
 void launch_tome_unmerge(int dt, const void* Ym, int64_t nrows, const int32_t* row, int64_t N,
                          int F, void* Y, hipStream_t st);
+void launch_tome_merge_qkv(const void* Q, const void* K, const void* V, int64_t N, int F,
+                           int64_t nrows, const int32_t* row_start, const int32_t* members,
+                           void* Qm, void* Km, void* Vm, hipStream_t st);
 
 void launch_router(const RouterArgs& a, hipStream_t st);
 void launch_router_logits(const float* u, const void* Wr, const float* br, int R, int Din,

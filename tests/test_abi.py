@@ -327,3 +327,12 @@ def test_tome_validation(lib):
         ctypes.byref(shape(S=3, P=15)), FAKE, nrows, row, Y, None)
     assert um(Y=None) == vp.VP_ERR_INVALID_ARG and um(row=FAKE + 2) == vp.VP_ERR_INVALID_ARG
     assert um(nrows=-1) == vp.VP_ERR_INVALID_ARG
+
+
+def test_tome_merge_qkv_validation(lib):
+    f = lambda shp=None, Q=FAKE, Km=FAKE, nrows=33: lib.vp_tome_merge_qkv(
+        ctypes.byref(shp or shape(S=3, P=15)), Q, FAKE, FAKE, nrows, FAKE, FAKE, FAKE, Km, FAKE,
+        None)
+    assert f(shp=shape(S=3, P=15, dt=vp.VP_F32)) == vp.VP_ERR_UNSUPPORTED
+    assert f(Q=None) == vp.VP_ERR_INVALID_ARG and f(Km=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+    assert f(nrows=0) == vp.VP_ERR_INVALID_ARG and f(nrows=46) == vp.VP_ERR_INVALID_ARG

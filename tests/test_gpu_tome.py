@@ -169,6 +169,13 @@ def test_merge_unmerge(dtype):
     log("merge worst err/bound = %.3f" % float((err / bound).max()))
     assert (err <= bound).all()
     assert torch.equal(back, Xm[plan.row.long()])
+    if dtype == "bf16":   # the fused Q/K/V merge gives the same rows, bitwise
+        X2 = synth.stored(synth.normal((S * P, 16, 64), 44, 1.0), dtype).cuda()
+        X3 = synth.stored(synth.normal((S * P, 16, 64), 45, 1.0), dtype).cuda()
+        out = [torch.empty_like(Xm) for _ in range(3)]
+        vp.tome_merge_qkv(X.cuda(), X2, X3, plan, *out)
+        assert torch.equal(out[0], Xm) and torch.equal(out[1], vp.tome_merge(X2, plan))
+        assert torch.equal(out[2], vp.tome_merge(X3, plan))
     # deterministic: a second plan and merge are bitwise equal
     plan2 = run_plan(K, S, P, M)
     assert torch.equal(plan2.members, plan.members) and torch.equal(plan2.row, plan.row)
