@@ -97,25 +97,6 @@ struct GemmArgs {
     float log2_base;      // QKV: log2 of the rotary base
 };
 
-// GELU(x) = x Phi(x) = (x / 2) (1 + erf(x / sqrt 2)), with erf from the rational
-// approximation 7.1.26 of Abramowitz and Stegun (Handbook of Mathematical
-// Functions): erf(z) = 1 - (a1 t + ... + a5 t^5) e^{-z^2}, t = 1 / (1 + p z),
-// z >= 0, absolute error <= 1.5e-7, odd extension for z < 0.  About a dozen
-// instructions (one exp2, one reciprocal) against ~30 for the library erf;
-// the error is far below the output's bf16 rounding.
-__device__ __forceinline__ float gelu_erf(float x) {
-    const float z = fabsf(x) * 0.70710678118654752f;
-    const float t = rcp_fast(fmaf(0.3275911f, z, 1.f));
-    float q = fmaf(1.061405429f, t, -1.453152027f);
-    q = fmaf(q, t, 1.421413741f);
-    q = fmaf(q, t, -0.284496736f);
-    q = fmaf(q, t, 0.254829592f);
-    q *= t;
-    const float e = exp2f_fast(-z * z * kLog2e);
-    const float erfz = fmaf(-q, e, 1.f);                       // erf(|x| / sqrt 2)
-    const float phi2 = 1.f + (x < 0.f ? -erfz : erfz);         // 1 + erf(x / sqrt 2)
-    return 0.5f * x * phi2;
-}
 
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void k_gemm(GemmArgs g) {

@@ -18,7 +18,7 @@ namespace vp {
 
 __device__ __forceinline__ float act_fn(float x, int act) {
     if (act == 1) return fmaxf(x, 0.f);
-    return 0.5f * x * (1.f + erff(x * 0.70710678118654752f));
+    return gelu_erf(x);
 }
 
 __device__ __forceinline__ float sigmoid_fast(float x) {
