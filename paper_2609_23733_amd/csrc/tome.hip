@@ -725,16 +725,12 @@ void launch_tome_plan(const TomeArgs& a, hipStream_t st) {
         hipLaunchKernelGGL(k_tome_match_final, dim3(grid256(G.nA)), dim3(256), 0, st, G, (int)C,
                            (const float*)pval, (const int32_t*)pidx, (const float*)invn, bslot,
                            score, key);
-        if (M > 0) {
-            const unsigned gh = (unsigned)((G.nA + 4095) / 4096);
-            for (int shift = 56; shift >= 0; shift -= 8) {
-                hipLaunchKernelGGL(k_rsel_hist, dim3(gh), dim3(256), 0, st, (const uint64_t*)key,
-                                   G.nA, shift, (const uint64_t*)sel, ghist);
-                hipLaunchKernelGGL(k_rsel_pick, dim3(1), dim3(256), 0, st, sel, ghist, shift);
-            }
-        } else {
-            // nothing merged: a threshold above every key
-            hipLaunchKernelGGL(k_fill_i32, dim3(1), dim3(256), 0, st, (int32_t*)sel, 2, -1);
+        // (M > 0 here: M = 0 leaves stride 1, hence no sources)
+        const unsigned gh = (unsigned)((G.nA + 4095) / 4096);
+        for (int shift = 56; shift >= 0; shift -= 8) {
+            hipLaunchKernelGGL(k_rsel_hist, dim3(gh), dim3(256), 0, st, (const uint64_t*)key, G.nA,
+                               shift, (const uint64_t*)sel, ghist);
+            hipLaunchKernelGGL(k_rsel_pick, dim3(1), dim3(256), 0, st, sel, ghist, shift);
         }
     }
     hipLaunchKernelGGL(k_tome_flags, dim3(grid256(N)), dim3(256), 0, st, G, (const uint64_t*)key,

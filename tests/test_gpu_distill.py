@@ -65,6 +65,23 @@ def test_teacher_targets(P, sharp):
         check_delta(dl[:, h, :], d_ref, av, "P=%d h=%d" % (P, h))
 
 
+def test_teacher_targets_few_heads():
+    """H = 3 heads (the teacher takes any head count up to 16)."""
+    from paper_2609_23733_amd import vp
+    log("teacher targets H=3")
+    x = synth.make_layer(1, 500, dtype="bf16", key=(34, 0), H=3, n_full=1)
+    colmax, smax, delta = vp.teacher_targets(x.Q.cuda(), x.K.cuda(), x.V.cuda(), 1, 500,
+                                             y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    cm, dl = colmax.cpu().numpy(), delta.double().cpu().numpy()
+    assert cm.shape == (3, 500) and dl.shape == (500, 3, 64)
+    for h in range(3):
+        ref = oracle.attention_colmax(x.Q, x.K, h)
+        check_colmax(cm[h], ref, "H=3 h=%d" % h)
+        d_ref = oracle.teacher_delta_rows(x.Q, x.K, x.V, h)
+        check_delta(dl[:, h, :], d_ref, d_ref + x.V[:, h, :].double().numpy(), "H=3 h=%d" % h)
+
+
 def test_teacher_targets_large_keys():
     """K scaled by 2^7 and Q by 2^-7 (exact in bf16): the logits are those of
     a mild layer, but the key norms leave the fp16 residual's error bound, so

@@ -104,6 +104,30 @@ def test_plan_random(S, P, M):
     check_plan(K, S, P, M, plan, "S=%d P=%d M=%d" % (S, P, M))
 
 
+@pytest.mark.parametrize("S,P,M,nspecial", [(3, 40, 78, 0), (4, 20, 42, 5), (5, 1374, 5472, 5),
+                                            (3, 8, 0, 3)])
+def test_plan_edges(S, P, M, nspecial):
+    """No special tokens; every possible source merged (each later view keeps
+    only patch 0: 2 x 39, 3 x 14 and 4 x 1368 sources); nothing merged."""
+    from paper_2609_23733_amd import vp
+    log("tome edges S=%d P=%d M=%d nspecial=%d" % (S, P, M, nspecial))
+    K = synth.stored(synth.normal((S * P, 16, 64), synth.derive_seed(47, S, M), 1.0), "bf16")
+    plan = vp.TomePlan(S, P, M, nspecial, want_best=True)
+    vp.tome_plan(K.cuda(), plan)
+    torch.cuda.synchronize()
+    ref = oracle.tome_plan(K, S, P, M, nspecial)
+    assert plan.g == ref["g"] and plan.nrows == ref["nrows"] == S * P - M
+    best = plan.best.cpu().numpy()
+    np.testing.assert_array_equal(best == -1, ref["is_dst"])
+    if M == (~ref["is_dst"]).sum():   # every source merged: rows are decided by the choices
+        srcs = ref["srcs"]
+        r_exp, _ = oracle.tome_rows(S * P, srcs, best[srcs], np.ones(srcs.shape[0], bool))
+        np.testing.assert_array_equal(plan.row.cpu().numpy(), r_exp)
+    if M == 0:
+        np.testing.assert_array_equal(plan.row.cpu().numpy(), np.arange(S * P))
+        np.testing.assert_array_equal(plan.members.cpu().numpy(), np.arange(S * P))
+
+
 def planted_keys(S, P, seed):
     """Random keys; 40 sources are power-of-two multiples of one destination
     (exact cosine ties on both sides), 100 more are noisy copies of other
