@@ -355,7 +355,7 @@ def run_tome(S, n_full, ratios, steps, warmup, unmerged_ms):
     return dict(S=S, N=N, n_full=n_full, unmerged_layer_ms=round(unmerged_ms, 4), by_ratio=out)
 
 
-def cpu_baseline(x, rows_per_head=640):
+def cpu_baseline(x, rows_per_head=800):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
     extrapolated linearly to all N rows (every row costs the same)."""
