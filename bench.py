@@ -12,6 +12,7 @@ the FULL-head kernel, and the fp64 CPU oracle timed on a bounded sample.
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -263,6 +264,57 @@ def run_stack(S, layers, steps, warmup, tome_ratio=None):
     return out
 
 
+def run_layer_stack(S, layers, steps, warmup):
+    """A stack of routed layers at S views with independent router and
+    surrogate weights per layer and FULL-head counts drawn from {1, ..., 6}
+    per layer.  The layers read one seeded Q/K/V (the attention's cost does
+    not depend on the values) and share one workspace and output buffer.
+    HIP events around each layer; MFMA work 4 N^2 d per FULL head."""
+    import numpy as np
+    import torch
+    from paper_2609_23733_amd import synth, vp
+    rng = np.random.Generator(np.random.PCG64(synth.derive_seed(S, 600)))
+    n_full = rng.integers(1, 7, size=layers)
+    base = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=int(n_full[0]), key=(S, 600),
+                            qkv_device="cuda")
+    N = S * P_TOKENS
+    ws = vp.alloc_workspace(S, P_TOKENS, HEADS, torch.bfloat16)
+    Y = torch.empty(N, HEADS, D, dtype=torch.bfloat16, device="cuda")
+    lys = []
+    for l in range(layers):
+        x = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=int(n_full[l]), key=(S, 600 + l),
+                             with_qkv=False)
+        x = dataclasses.replace(x, Q=base.Q, K=base.K, V=base.V)
+        lys.append(vp.RoutedLayer(x, y_dtype=torch.bfloat16, ws=ws, Y=Y))
+
+    def once(evs=None):
+        for l, ly in enumerate(lys):
+            if evs is not None:
+                evs[l][0].record()
+            ly.step()
+            if evs is not None:
+                evs[l][1].record()
+    for _ in range(warmup):
+        once()
+    torch.cuda.synchronize()
+    per = np.zeros(layers)
+    for _ in range(steps):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(layers)]
+        once(evs)
+        torch.cuda.synchronize()
+        per += [a.elapsed_time(b) for a, b in evs]
+    per /= steps
+    got = [int((ly.modes == 2).sum()) for ly in lys]
+    fl = sum(flops_full(N, n) for n in got)
+    tot = float(per.sum())
+    del lys, ws, Y, base
+    torch.cuda.empty_cache()
+    return dict(S=S, N=N, layers=layers, n_full=got, per_layer_ms=[round(float(v), 2) for v in per],
+                total_ms=round(tot, 1), tflops=round(fl / tot / 1e9, 1),
+                frac_bf16_peak=round(fl / tot / 1e9 / PEAK_BF16_TFLOPS, 4))
+
+
 def run_teacher(S, steps, warmup):
     """Distillation targets of a teacher layer (every head FULL; Eq.8, Eq.10)
     and the two losses (Eq.9, Eq.11) on the same inputs: HIP-event latency
@@ -400,6 +452,8 @@ def main():
     ap.add_argument("--no-block", action="store_true")
     ap.add_argument("--no-teacher", action="store_true")
     ap.add_argument("--no-tome", action="store_true")
+    ap.add_argument("--no-stack500", action="store_true",
+                    help="skip the 24-layer routed stack at S=500")
     ap.add_argument("--stack", type=int, default=0, metavar="S",
                     help="also time a 24-block stack at S views (e.g. 500)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -442,6 +496,9 @@ def main():
     if not args.no_teacher:
         teacher = run_teacher(100, max(2, args.steps // 4), 1)
         torch.cuda.empty_cache()
+    stack500 = None
+    if not args.no_stack500:
+        stack500 = run_layer_stack(500, 24, 1, 1)
     stack = None
     if args.stack:
         stack = run_stack(args.stack, 24, 2, 1)
@@ -500,6 +557,8 @@ def main():
         out["tome"] = tome
     if teacher is not None:
         out["teacher"] = teacher
+    if stack500 is not None:
+        out["layer_stack_s500"] = stack500
     if stack is not None:
         out["stack"] = stack
     if not args.no_cpu_baseline:
