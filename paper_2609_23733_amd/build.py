@@ -23,15 +23,18 @@ ARCH = "gfx950"
 CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # MFMA results in arch VGPRs: the softmax reads S directly instead of
-    # copying it out of accumulation registers every tile.
-    "-mllvm", "-amdgpu-mfma-vgpr-form=true",
 ]
+# MFMA results in arch VGPRs: the softmax reads S directly instead of copying
+# it out of accumulation registers every tile.  Not for the block GEMM, whose
+# 256 accumulators per lane live in the AGPRs.
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=true"]
+AGPR_ACC_SOURCES = {"block.hip"}
 
 
 def _compile(src: str, extra) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + CFLAGS + list(extra) + ["-c", src, "-o", obj]
+    form = [] if os.path.basename(src) in AGPR_ACC_SOURCES else VGPR_FORM
+    cmd = [HIPCC] + CFLAGS + form + list(extra) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     msgs = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
                      if "packed-fp32-ops" not in l)

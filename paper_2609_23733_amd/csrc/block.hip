@@ -69,17 +69,19 @@ __global__ __launch_bounds__(256) void k_layernorm(const bf16* __restrict__ X,
 // B2: D^T = W X^T for W [F, Kd] (weights as stored, [out, in]) and X [T, Kd]
 // (token rows), bf16 operands, fp32 accumulation: both operands are
 // Kd-contiguous, as the MFMA wants them.  Workgroup tile 256 features x 256
-// tokens, 8 waves of 128 x 64 (4 x 2 blocks of 32 x 32), Kd in stages of 64
-// double-buffered through LDS (144-byte rows: conflict-free 16-byte reads),
-// one barrier per stage.  Output features are the MFMA rows, so lane l holds
-// token l % 32 of a block and features 8 (r / 4) + 4 (l / 32) + r % 4 in its
-// register r: four consecutive features per store, and the rotary pair
+// tokens, Kd in stages of 64 through two LDS buffers (144-byte rows:
+// conflict-free 16-byte reads).  Output features are the MFMA rows, so lane l
+// holds token l % 32 of a block and features 8 (r / 4) + 4 (l / 32) + r % 4 in
+// its register r: four consecutive features per store, and the rotary pair
 // (j, j + 16) of a 32-feature half in registers r and r + 8 of one lane.
 // Tiles are ordered in groups of four feature tiles per token tile, and
 // consecutive tiles share an XCD, so an XCD's L2 keeps a token tile for four
 // feature tiles and a group of weight tiles for all its token tiles.
+// Every output sums its Kd products in the same order (stage by stage, 16 per
+// MFMA) in both kernels below, so they produce identical bits.
 // ------------------------------------------------------------------------
 constexpr int kGM = 256, kGN = 256, kGK = 64, kGRow = 72, kGGroup = 4;
+constexpr int kGemmWG = 256;   // persistent workgroups: one per CU
 
 enum { EPI_QKV = 0, EPI_GELU = 1, EPI_RESID = 2 };
 
@@ -97,80 +99,21 @@ struct GemmArgs {
     float log2_base;      // QKV: log2 of the rotary base
 };
 
-
-template <int EPI>
-__global__ __launch_bounds__(512, 1) void k_gemm(GemmArgs g) {
-    const int nft = g.F / kGM;
-    const int ntt = (int)((g.T + kGN - 1) / kGN);
-    const int total = nft * ntt;
-    const int L = xcd_remap(blockIdx.x, total);
+// Tile (L) of the grouped order: features f0.., tokens t0...
+__device__ __forceinline__ void gemm_tile(int L, int ntt, int& f0, int64_t& t0) {
     const int grp = L / (kGGroup * ntt), in = L - grp * kGGroup * ntt;
     const int tt = in / kGGroup, ft = grp * kGGroup + in % kGGroup;
-    const int f0 = ft * kGM;
-    const int64_t t0 = (int64_t)tt * kGN;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int n = lane & 31, hh = lane >> 5;
-    const int wm = wave >> 2, wn = wave & 3;
+    f0 = ft * kGM;
+    t0 = (int64_t)tt * kGN;
+}
 
-    __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
-    __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
-
-    // Stage copy: 4 chunks of 16 bytes of W and 4 of X per thread; chunk
-    // c = tid + 512 i is row c / 8, bytes 16 (c % 8) of the stage's 128.
-    // Token rows past T read row T - 1; their outputs are never stored.
-    u32x4 rw[4], rx[4];
-    auto gload = [&](int kt) {
-        const int k0 = kt * kGK;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = tid + 512 * i, row = c >> 3, seg = (c & 7) * 8;
-            rw[i] = *reinterpret_cast<const u32x4*>(g.W + (int64_t)(f0 + row) * g.Kd + k0 + seg);
-            const int64_t tr = t0 + row < g.T ? t0 + row : g.T - 1;
-            rx[i] = *reinterpret_cast<const u32x4*>(g.X + tr * g.Kd + k0 + seg);
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int c = tid + 512 * i, row = c >> 3, seg = (c & 7) * 8;
-            *reinterpret_cast<u32x4*>(&sW[buf][row * kGRow + seg]) = rw[i];
-            *reinterpret_cast<u32x4*>(&sX[buf][row * kGRow + seg]) = rx[i];
-        }
-    };
-
-    f32x16 acc[4][2];
-#pragma unroll
-    for (int fb = 0; fb < 4; ++fb) acc[fb][0] = acc[fb][1] = zero_f32x16();
-
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    const int nk = g.Kd / kGK;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-        for (int ks = 0; ks < kGK / 16; ++ks) {
-            bf16x8 a[4], b[2];
-#pragma unroll
-            for (int fb = 0; fb < 4; ++fb)
-                a[fb] = *reinterpret_cast<const bf16x8*>(
-                    &sW[buf][(128 * wm + 32 * fb + n) * kGRow + 16 * ks + 8 * hh]);
-#pragma unroll
-            for (int tb = 0; tb < 2; ++tb)
-                b[tb] = *reinterpret_cast<const bf16x8*>(
-                    &sX[buf][(64 * wn + 32 * tb + n) * kGRow + 16 * ks + 8 * hh]);
-#pragma unroll
-            for (int fb = 0; fb < 4; ++fb)
-#pragma unroll
-                for (int tb = 0; tb < 2; ++tb) acc[fb][tb] = mfma_bf16(a[fb], b[tb], acc[fb][tb]);
-        }
-        if (kt + 1 < nk) lstore(buf ^ 1);
-        __syncthreads();
-    }
-
-    // Epilogue.  Lane: token t of block tb, features fbase + 8 gq + 4 hh + i
-    // in register r = 4 gq + i.
+// Epilogue of a wave's 128 features x (32 NTB) tokens: lane (n, hh) holds, in
+// acc[fb][tb] register r = 4 gq + i, feature f0 + 128 wm + 32 fb + 8 gq + 4 hh
+// + i of token tl + tok0 + 32 tb + n.  Tokens outside [t0, T) are not stored.
+template <int EPI, int NTB>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4][NTB], int f0,
+                                              int64_t t0, int64_t tl, int wm, int tok0, int n,
+                                              int hh) {
     float omega[8];   // rotary frequencies of features j = 8 (r / 4) + 4 hh + r % 4, r < 8
     if (EPI == EPI_QKV) {
 #pragma unroll
@@ -180,9 +123,9 @@ __global__ __launch_bounds__(512, 1) void k_gemm(GemmArgs g) {
         }
     }
 #pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-        const int64_t t = t0 + 64 * wn + 32 * tb + n;
-        if (t >= g.T) continue;
+    for (int tb = 0; tb < NTB; ++tb) {
+        const int64_t t = tl + tok0 + 32 * tb + n;
+        if (t < t0 || t >= g.T) continue;
         int2 p = make_int2(0, 0);
         if (EPI == EPI_QKV) p = *reinterpret_cast<const int2*>(g.pos + 2 * t);
 #pragma unroll
@@ -244,17 +187,256 @@ __global__ __launch_bounds__(512, 1) void k_gemm(GemmArgs g) {
     }
 }
 
+// B2a (T >= 256): persistent, one workgroup of 4 waves per CU, each wave a
+// 128 x 128 block of the tile with its 256 accumulators in AGPRs.  Workgroup b
+// takes tiles i G + slot(b), slot grouping the workgroups of an XCD, so the 32
+// tiles an XCD runs at once are 8 token tiles x 4 feature tiles.  A partial
+// last token tile reads rows T - 256 .. T - 1 (every read in bounds) and
+// stores only its own tokens.
+// Pipeline: stage s + 2 is loaded into registers while stage s is multiplied
+// (two register sets, so two stages are in flight), stage s + 1 goes to LDS
+// during the last k-step of stage s, and the next tile's first stages are in
+// flight during a tile's epilogue.  Per stage a wave issues 64 MFMAs
+// (4 k-steps x 16), 32 LDS fragment reads (each k-step reads the next one's),
+// 16 global loads and 16 LDS stores, interleaved one for one with the MFMAs
+// by scheduling barriers; the one barrier per stage sits between the two
+// halves of the last k-step, whose second half covers the first reads of the
+// next stage.
+template <int EPI>
+__global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
+    // Make the AGPRs available to the register allocator (accumulators).
+    asm volatile("" ::: "a0");
+    const int nft = g.F / kGM;
+    const int ntt = (int)((g.T + kGN - 1) / kGN);
+    const int total = nft * ntt;
+    const int nk = g.Kd / kGK;
+    const int G = gridDim.x, b = blockIdx.x;
+    const int slot = (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+    const int ntile = slot < total ? (total - 1 - slot) / G + 1 : 0;
+    if (ntile == 0) return;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = lane & 31, hh = lane >> 5;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
+    __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
+
+    auto tile_of = [&](int i, int& f0, int64_t& t0, int64_t& tl) {
+        gemm_tile(i * G + slot, ntt, f0, t0);
+        tl = t0 + kGN <= g.T ? t0 : g.T - kGN;
+    };
+
+    // Load state: the next stage to load (tile li, stage lkt).  Past the last
+    // stage the bases keep pointing at a valid stage; those loads go unused.
+    int li = 0, lkt = 0, lf0;
+    int64_t lt0, ltl;
+    tile_of(0, lf0, lt0, ltl);
+    const char* wb;
+    const char* xb;
+    auto next_bases = [&]() {
+        wb = reinterpret_cast<const char*>(g.W + (int64_t)lf0 * g.Kd + lkt * kGK);
+        xb = reinterpret_cast<const char*>(g.X + ltl * g.Kd + lkt * kGK);
+        if (++lkt == nk) {
+            lkt = 0;
+            if (++li < ntile) tile_of(li, lf0, lt0, ltl);
+        }
+    };
+    // Thread tid moves row (tid / 8) + 32 j, bytes 16 (tid % 8) of the
+    // stage's 128, j = 0..7, of both operands.
+    const uint32_t voff = (uint32_t)(tid >> 3) * (uint32_t)g.Kd * 2u + (uint32_t)(tid & 7) * 16u;
+    const int64_t jstride = (int64_t)32 * g.Kd * 2;
+    auto gload = [&](int h, u32x4 (&rw)[8], u32x4 (&rx)[8]) {
+#pragma unroll
+        for (int j = 4 * h; j < 4 * h + 4; ++j) {
+            rw[j] = *reinterpret_cast<const u32x4*>(wb + j * jstride + voff);
+            rx[j] = *reinterpret_cast<const u32x4*>(xb + j * jstride + voff);
+        }
+    };
+    const int lsoff = (tid >> 3) * kGRow + (tid & 7) * 8;
+    auto lstore = [&](int buf, u32x4 (&rw)[8], u32x4 (&rx)[8]) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            *reinterpret_cast<u32x4*>(&sW[buf][lsoff + 32 * j * kGRow]) = rw[j];
+            *reinterpret_cast<u32x4*>(&sX[buf][lsoff + 32 * j * kGRow]) = rx[j];
+        }
+    };
+    const int aoff = (128 * wm + n) * kGRow + 8 * hh, xoff = (128 * wn + n) * kGRow + 8 * hh;
+    auto lread = [&](int buf, int ks, bf16x8 (&a)[4], bf16x8 (&x)[4]) {
+#pragma unroll
+        for (int fb = 0; fb < 4; ++fb)
+            a[fb] = *reinterpret_cast<const bf16x8*>(&sW[buf][aoff + 32 * fb * kGRow + 16 * ks]);
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb)
+            x[tb] = *reinterpret_cast<const bf16x8*>(&sX[buf][xoff + 32 * tb * kGRow + 16 * ks]);
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int fb = 0; fb < 4; ++fb)
+#pragma unroll
+        for (int tb = 0; tb < 4; ++tb) acc[fb][tb] = zero_f32x16();
+
+    u32x4 ra[8], xa[8], rb[8], xb8[8];   // the two register sets
+    next_bases();
+    gload(0, ra, xa);
+    gload(1, ra, xa);
+    next_bases();
+    gload(0, rb, xb8);
+    gload(1, rb, xb8);
+    lstore(0, ra, xa);
+    __syncthreads();
+    bf16x8 fa0[4], fx0[4], fa1[4], fx1[4];
+    lread(0, 0, fa0, fx0);
+    int buf = 0;
+
+#define VP_SGB(mask, cnt) __builtin_amdgcn_sched_group_barrier(mask, cnt, 0)
+#define VP_MMA(A, X, FB0, FB1)                                                          \
+    _Pragma("unroll") for (int fb = FB0; fb < FB1; ++fb)                               \
+        _Pragma("unroll") for (int tb = 0; tb < 4; ++tb) acc[fb][tb] =                  \
+            mfma_bf16(A[fb], X[tb], acc[fb][tb]);
+    // One stage: load the stage after next into (LW, LX), store the next
+    // stage from (SW, SX).  Masks: 0x008 MFMA, 0x020 global load, 0x100 LDS
+    // read, 0x200 LDS write.
+#define VP_STAGE(LW, LX, SW, SX)                                                        \
+    {                                                                                   \
+        next_bases();                                                                   \
+        lread(buf, 1, fa1, fx1);                                                        \
+        gload(0, LW, LX);                                                               \
+        VP_MMA(fa0, fx0, 0, 4);                                                         \
+        for (int q = 0; q < 8; ++q) { VP_SGB(0x008, 1); VP_SGB(0x100, 1); VP_SGB(0x020, 1); } \
+        VP_SGB(0x008, 8);                                                               \
+        lread(buf, 2, fa0, fx0);                                                        \
+        gload(1, LW, LX);                                                               \
+        VP_MMA(fa1, fx1, 0, 4);                                                         \
+        for (int q = 0; q < 8; ++q) { VP_SGB(0x008, 1); VP_SGB(0x100, 1); VP_SGB(0x020, 1); } \
+        VP_SGB(0x008, 8);                                                               \
+        lread(buf, 3, fa1, fx1);                                                        \
+        VP_MMA(fa0, fx0, 0, 4);                                                         \
+        for (int q = 0; q < 8; ++q) { VP_SGB(0x008, 1); VP_SGB(0x100, 1); }             \
+        VP_SGB(0x008, 8);                                                               \
+        VP_MMA(fa1, fx1, 0, 2);                                                         \
+        lstore(buf ^ 1, SW, SX);                                                        \
+        for (int q = 0; q < 8; ++q) { VP_SGB(0x008, 1); VP_SGB(0x200, 2); }             \
+        __syncthreads();                                                                \
+        lread(buf ^ 1, 0, fa0, fx0);                                                    \
+        VP_MMA(fa1, fx1, 2, 4);                                                         \
+        for (int q = 0; q < 8; ++q) { VP_SGB(0x008, 1); VP_SGB(0x100, 1); }             \
+        buf ^= 1;                                                                       \
+    }
+    for (int i = 0; i < ntile; ++i) {
+        for (int kt = 0; kt < nk; kt += 2) {   // nk is even
+            VP_STAGE(ra, xa, rb, xb8);
+            VP_STAGE(rb, xb8, ra, xa);
+        }
+        int f0;
+        int64_t t0, tl;
+        tile_of(i, f0, t0, tl);
+        gemm_epilogue<EPI, 4>(g, acc, f0, t0, tl, wm, 128 * wn, n, hh);
+#pragma unroll
+        for (int fb = 0; fb < 4; ++fb)
+#pragma unroll
+            for (int tb = 0; tb < 4; ++tb) acc[fb][tb] = zero_f32x16();
+    }
+#undef VP_STAGE
+#undef VP_MMA
+#undef VP_SGB
+}
+
+// B2b (T < 256, a single partial token tile): 8 waves of 128 x 64, the stage
+// copy through registers one stage ahead, token rows past T reading row T - 1
+// (their outputs are never stored).
+template <int EPI>
+__global__ __launch_bounds__(512, 1) void k_gemm_small(GemmArgs g) {
+    const int nft = g.F / kGM;
+    const int ntt = (int)((g.T + kGN - 1) / kGN);
+    const int total = nft * ntt;
+    int f0;
+    int64_t t0;
+    gemm_tile(xcd_remap(blockIdx.x, total), ntt, f0, t0);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = lane & 31, hh = lane >> 5;
+    const int wm = wave >> 2, wn = wave & 3;
+
+    __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
+    __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
+
+    // Stage copy: 4 chunks of 16 bytes of W and 4 of X per thread; chunk
+    // c = tid + 512 i is row c / 8, bytes 16 (c % 8) of the stage's 128.
+    u32x4 rw[4], rx[4];
+    auto gload = [&](int kt) {
+        const int k0 = kt * kGK;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 512 * i, row = c >> 3, seg = (c & 7) * 8;
+            rw[i] = *reinterpret_cast<const u32x4*>(g.W + (int64_t)(f0 + row) * g.Kd + k0 + seg);
+            const int64_t tr = t0 + row < g.T ? t0 + row : g.T - 1;
+            rx[i] = *reinterpret_cast<const u32x4*>(g.X + tr * g.Kd + k0 + seg);
+        }
+    };
+    auto lstore = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int c = tid + 512 * i, row = c >> 3, seg = (c & 7) * 8;
+            *reinterpret_cast<u32x4*>(&sW[buf][row * kGRow + seg]) = rw[i];
+            *reinterpret_cast<u32x4*>(&sX[buf][row * kGRow + seg]) = rx[i];
+        }
+    };
+
+    f32x16 acc[4][2];
+#pragma unroll
+    for (int fb = 0; fb < 4; ++fb) acc[fb][0] = acc[fb][1] = zero_f32x16();
+
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    const int nk = g.Kd / kGK;
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < nk) gload(kt + 1);
+#pragma unroll
+        for (int ks = 0; ks < kGK / 16; ++ks) {
+            bf16x8 a[4], x[2];
+#pragma unroll
+            for (int fb = 0; fb < 4; ++fb)
+                a[fb] = *reinterpret_cast<const bf16x8*>(
+                    &sW[buf][(128 * wm + 32 * fb + n) * kGRow + 16 * ks + 8 * hh]);
+#pragma unroll
+            for (int tb = 0; tb < 2; ++tb)
+                x[tb] = *reinterpret_cast<const bf16x8*>(
+                    &sX[buf][(64 * wn + 32 * tb + n) * kGRow + 16 * ks + 8 * hh]);
+#pragma unroll
+            for (int fb = 0; fb < 4; ++fb)
+#pragma unroll
+                for (int tb = 0; tb < 2; ++tb) acc[fb][tb] = mfma_bf16(a[fb], x[tb], acc[fb][tb]);
+        }
+        if (kt + 1 < nk) lstore(buf ^ 1);
+        __syncthreads();
+    }
+    gemm_epilogue<EPI, 2>(g, acc, f0, t0, t0, wm, 64 * wn, n, hh);
+}
+
 // ------------------------------------------------------------------ launchers
 
-static void gemm(int epi, const GemmArgs& a, hipStream_t st) {
-    const unsigned grid =
-        (unsigned)((a.F / kGM) * ((a.T + kGN - 1) / kGN));
-    if (epi == EPI_QKV)
-        hipLaunchKernelGGL(k_gemm<EPI_QKV>, dim3(grid), dim3(512), 0, st, a);
-    else if (epi == EPI_GELU)
-        hipLaunchKernelGGL(k_gemm<EPI_GELU>, dim3(grid), dim3(512), 0, st, a);
+template <int EPI>
+static void gemm_launch(const GemmArgs& a, hipStream_t st) {
+    const int total = (a.F / kGM) * (int)((a.T + kGN - 1) / kGN);
+    if (a.T >= kGN)
+        hipLaunchKernelGGL(k_gemm<EPI>, dim3(total < kGemmWG ? total : kGemmWG), dim3(256), 0, st,
+                           a);
     else
-        hipLaunchKernelGGL(k_gemm<EPI_RESID>, dim3(grid), dim3(512), 0, st, a);
+        hipLaunchKernelGGL(k_gemm_small<EPI>, dim3(total), dim3(512), 0, st, a);
+}
+
+// F a multiple of 4 x 256 (whole groups of feature tiles), Kd of 128 (the
+// persistent kernel takes stages in pairs); the block's shapes are 1024 x
+// {3, 1, 4} by 1024 and 1024 by 4096.
+static void gemm(int epi, const GemmArgs& a, hipStream_t st) {
+    if (epi == EPI_QKV)
+        gemm_launch<EPI_QKV>(a, st);
+    else if (epi == EPI_GELU)
+        gemm_launch<EPI_GELU>(a, st);
+    else
+        gemm_launch<EPI_RESID>(a, st);
 }
 
 static void layernorm(const bf16* X, const bf16* X2, int64_t T, const float* g, const float* b,

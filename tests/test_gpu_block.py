@@ -47,7 +47,7 @@ def check_update(out_g, X, ref, label, rows=None):
     assert (err <= bound).all(), "%s: max err %.3e, ratio %.3f" % (label, err.max(), ratio)
 
 
-@pytest.mark.parametrize("S,P", [(1, 1), (1, 5), (1, 300), (1, 1374), (2, 1374)])
+@pytest.mark.parametrize("S,P", [(1, 1), (1, 5), (1, 256), (1, 300), (1, 513), (1, 1374), (2, 1374)])
 def test_block_qkv(S, P):
     from paper_2609_23733_amd import vp
     log("block qkv S=%d P=%d" % (S, P))
@@ -63,7 +63,7 @@ def test_block_qkv(S, P):
         check_y(g.double().cpu().numpy(), r, "bf16", True, label="qkv %s S=%d P=%d" % (nm, S, P))
 
 
-@pytest.mark.parametrize("S,P", [(1, 1), (1, 300), (2, 1374)])
+@pytest.mark.parametrize("S,P", [(1, 1), (1, 255), (1, 300), (1, 513), (2, 1374)])
 def test_block_out(S, P):
     from paper_2609_23733_amd import vp
     log("block out S=%d P=%d" % (S, P))
