@@ -122,12 +122,25 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
             omega[r] = exp2f(-(float)j * (1.f / 16.f) * g.log2_base);
         }
     }
+    // All of a wave's features lie in one of Q, K, V (f0 is a multiple of
+    // 256); Q and K are rotated, the first 32 features of each 64 by the row
+    // coordinate and the next 32 by the column coordinate.
+    const bool rotate = EPI == EPI_QKV && (f0 + 128 * wm) / kDm < 2;
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
         const int64_t t = tl + tok0 + 32 * tb + n;
         if (t < t0 || t >= g.T) continue;
-        int2 p = make_int2(0, 0);
-        if (EPI == EPI_QKV) p = *reinterpret_cast<const int2*>(g.pos + 2 * t);
+        // (sin, cos) of this token's angles, once per token: half 0 takes the
+        // row coordinate, half 1 the column coordinate
+        float rs[2][8], rc[2][8];
+        if (rotate) {
+            const int2 p = *reinterpret_cast<const int2*>(g.pos + 2 * t);
+#pragma unroll
+            for (int r = 0; r < 8; ++r) {
+                __sincosf((float)p.x * omega[r], &rs[0][r], &rc[0][r]);
+                __sincosf((float)p.y * omega[r], &rs[1][r], &rc[1][r]);
+            }
+        }
 #pragma unroll
         for (int fb = 0; fb < 4; ++fb) {
             const int fbase = f0 + 128 * wm + 32 * fb;
@@ -138,12 +151,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
             bf16* dst;
             if (EPI == EPI_QKV) {
                 const int which = fbase / kDm, fin = fbase - which * kDm;
-                if (which < 2) {   // Q, K: rotate the planes (j, j + 16) of this half
-                    const float coord = (float)((fin & 32) ? p.y : p.x);
+                if (rotate) {   // Q, K: rotate the planes (j, j + 16) of this half
+                    const int half = (fin & 32) ? 1 : 0;   // fb & 1
 #pragma unroll
                     for (int r = 0; r < 8; ++r) {
-                        float sn, cs;
-                        __sincosf(coord * omega[r], &sn, &cs);
+                        const float sn = rs[half][r], cs = rc[half][r];
                         const float u = v[r], w = v[r + 8];
                         v[r] = u * cs - w * sn;
                         v[r + 8] = u * sn + w * cs;
@@ -187,7 +199,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     }
 }
 
-// B2a (T >= 256): persistent, one workgroup of 4 waves per CU, each wave a
+// B2a (W_O and FFN projections, T >= 256): persistent, one workgroup of 4
+// waves per CU, each wave a
 // 128 x 128 block of the tile with its 256 accumulators in AGPRs.  Workgroup b
 // takes tiles i G + slot(b), slot grouping the workgroups of an XCD, so the 32
 // tiles an XCD runs at once are 8 token tiles x 4 feature tiles.  A partial
@@ -342,11 +355,13 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
 #undef VP_SGB
 }
 
-// B2b (T < 256, a single partial token tile): 8 waves of 128 x 64, the stage
+// B2b: one workgroup per tile, 8 waves of 128 x 64 (two per SIMD), the stage
 // copy through registers one stage ahead, token rows past T reading row T - 1
-// (their outputs are never stored).
+// (their outputs are never stored).  Used for the QKV projection, whose
+// rotary epilogue (16 sincos per token) the second wave on each SIMD helps
+// to hide (3-8 % faster than B2a at S = 100), and for T < 256.
 template <int EPI>
-__global__ __launch_bounds__(512, 1) void k_gemm_small(GemmArgs g) {
+__global__ __launch_bounds__(512, 1) void k_gemm_w8(GemmArgs g) {
     const int nft = g.F / kGM;
     const int ntt = (int)((g.T + kGN - 1) / kGN);
     const int total = nft * ntt;
@@ -420,11 +435,14 @@ __global__ __launch_bounds__(512, 1) void k_gemm_small(GemmArgs g) {
 template <int EPI>
 static void gemm_launch(const GemmArgs& a, hipStream_t st) {
     const int total = (a.F / kGM) * (int)((a.T + kGN - 1) / kGN);
-    if (a.T >= kGN)
-        hipLaunchKernelGGL(k_gemm<EPI>, dim3(total < kGemmWG ? total : kGemmWG), dim3(256), 0, st,
-                           a);
-    else
-        hipLaunchKernelGGL(k_gemm_small<EPI>, dim3(total), dim3(512), 0, st, a);
+    if constexpr (EPI != EPI_QKV) {
+        if (a.T >= kGN) {
+            hipLaunchKernelGGL(k_gemm<EPI>, dim3(total < kGemmWG ? total : kGemmWG), dim3(256), 0,
+                               st, a);
+            return;
+        }
+    }
+    hipLaunchKernelGGL(k_gemm_w8<EPI>, dim3(total), dim3(512), 0, st, a);
 }
 
 // F a multiple of 4 x 256 (whole groups of feature tiles), Kd of 128 (the
