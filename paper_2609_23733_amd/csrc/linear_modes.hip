@@ -36,12 +36,13 @@ constexpr int kW = 72;           // bf16 LDS row stride
 // hidden units arrive eight-consecutive per lane-half, the K order of the
 // second MFMA.
 // ------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_surrogate_bf16(
+template <int ACT>
+__global__ __launch_bounds__(256, 4) void k_surrogate_bf16(
     const bf16* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
     const bf16* __restrict__ gw1, const float* __restrict__ gb1, const bf16* __restrict__ gw2,
     const float* __restrict__ gb2, const bf16* __restrict__ dw1, const float* __restrict__ db1,
-    const bf16* __restrict__ dw2, const float* __restrict__ db2, int act, int add_v, int64_t N,
-    int H, void* __restrict__ Y, int ydt) {
+    const bf16* __restrict__ dw2, const float* __restrict__ db2, int add_v, int64_t N, int H,
+    void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
     const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
@@ -59,13 +60,17 @@ __global__ __launch_bounds__(256) void k_surrogate_bf16(
         sB2g[tid] = gb2[h * kD + tid];
         sB2d[tid] = db2[h * kD + tid];
     }
-    // Context half of layer 1 plus bias: c1[u] = b1[u] + sum_c W1[u][64 + c] C[c].
+    // Context half of layer 1 plus bias: c1[u] = b1[u] + sum_c W1[u][64 + c] C[c],
+    // summed in c order.  Threads 0..127 load their row's 64 weights now and
+    // sum once C is in LDS.
+    bf16x8 wc[8];
+    float c1acc = 0.f;
     if (tid < 128) {
         const int u = tid & 63;
-        const bf16* w1 = (tid < 64 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD;
-        float acc = (tid < 64 ? gb1 : db1)[h * kL + u];
-        for (int cc = 0; cc < kD; ++cc) acc = fmaf(bf16_to_f32(w1[kD + cc]), C[cc], acc);
-        sC1[tid] = acc;
+        const bf16* w1 = (tid < 64 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD + kD;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) wc[k] = load_bf16x8(w1 + 8 * k);
+        c1acc = (tid < 64 ? gb1 : db1)[h * kL + u];
     }
     // W1_v rows (value half) into LDS, rows permuted within 32-blocks.
     for (int i = tid; i < 128 * 8; i += 256) {
@@ -80,56 +85,75 @@ __global__ __launch_bounds__(256) void k_surrogate_bf16(
         *reinterpret_cast<bf16x8*>(&sW2[which][r * kW + seg]) = load_bf16x8(w2);
     }
     __syncthreads();
-
-    // c1 values this lane needs: hidden u = 32 mb + 16 (r / 8) + 8 hh + r % 8.
-    float c1[4][16];
+    if (tid < 128) {
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) c1[mb][r] = sC1[32 * mb + 16 * (r >> 3) + 8 * hh + (r & 7)];
+        for (int cc = 0; cc < kD; ++cc) c1acc = fmaf(bf16_to_f32(wc[cc >> 3][cc & 7]), sC[cc], c1acc);
+        sC1[tid] = c1acc;
+    }
+    __syncthreads();
 
+
+    // Each wave takes 32 tokens at a time; the next block's V is loaded while
+    // this one is computed.  Tokens past t1 read token t0 (never stored).
+    auto load_v = [&](int64_t tb, bf16x8 (&B)[4]) {
+        const int64_t tok = tb + n;
+        const bf16* vr = V + ((tok < t1 ? tok : t0) * H + h) * kD + 8 * hh;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) B[ks] = load_bf16x8(vr + 16 * ks);
+    };
+    bf16x8 B[4], Bn[4];
+    load_v(t0 + 32 * wave, B);
     for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
         const int64_t tok = tb + n;
         const bool ok = tok < t1;
-        const bf16* vr = V + ((ok ? tok : t0) * H + h) * kD + 8 * hh;
-        bf16x8 B[4];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) B[ks] = load_bf16x8(vr + 16 * ks);
-        f32x16 A1[4];
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-            A1[mb] = zero_f32x16();
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 a =
-                    *reinterpret_cast<const bf16x8*>(&sW1[(32 * mb + n) * kW + 16 * ks + 8 * hh]);
-                A1[mb] = mfma_bf16(a, B[ks], A1[mb]);
-            }
-        }
-        bf16x8 Hop[2][4];   // [gamma|delta][k-step over hidden]
-#pragma unroll
-        for (int which = 0; which < 2; ++which)
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const int mb = 2 * which + (ks >> 1), r0 = 8 * (ks & 1);
-                float hv[8];
-#pragma unroll
-                for (int j = 0; j < 8; ++j) hv[j] = act_fn(A1[mb][r0 + j] + c1[mb][r0 + j], act);
-                Hop[which][ks] = pack_bf16x8(hv[0], hv[1], hv[2], hv[3], hv[4], hv[5], hv[6], hv[7]);
-            }
+        load_v(tb + 128 < t1 ? tb + 128 : tb, Bn);
+        // One MLP at a time (gamma: hidden blocks 0, 1 and W2_gamma; delta:
+        // blocks 2, 3 and W2_delta), so only one MLP's hidden layer is live.
+        // The weight fragments are read from LDS every iteration (an opaque
+        // offset keeps them from being hoisted into 128 loop-long registers,
+        // which would leave room for one wave per SIMD).
+        int wrow = n * kW + 8 * hh;
+        asm volatile("" : "+v"(wrow));
         f32x16 G[2], D[2];
 #pragma unroll
-        for (int db = 0; db < 2; ++db) {
-            G[db] = zero_f32x16();
-            D[db] = zero_f32x16();
+        for (int which = 0; which < 2; ++which) {
+            f32x16 A1[2];
+#pragma unroll
+            for (int m2 = 0; m2 < 2; ++m2) {
+                const int mb = 2 * which + m2;
+                A1[m2] = zero_f32x16();
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                        &sW1[32 * mb * kW + wrow + 16 * ks]);
+                    A1[m2] = mfma_bf16(a, B[ks], A1[m2]);
+                }
+            }
+            bf16x8 Hop[4];   // k-steps over this MLP's 64 hidden units
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 ag = *reinterpret_cast<const bf16x8*>(
-                    &sW2[0][(32 * db + n) * kW + 16 * ks + 8 * hh]);
-                const bf16x8 ad = *reinterpret_cast<const bf16x8*>(
-                    &sW2[1][(32 * db + n) * kW + 16 * ks + 8 * hh]);
-                G[db] = mfma_bf16(ag, Hop[0][ks], G[db]);
-                D[db] = mfma_bf16(ad, Hop[1][ks], D[db]);
+                // register r0 + j of block mb holds hidden unit 32 mb + 16 (ks % 2) + 8 hh + j
+                const int m2 = ks >> 1, mb = 2 * which + m2, r0 = 8 * (ks & 1);
+                const f32x4 ca = *reinterpret_cast<const f32x4*>(&sC1[32 * mb + 2 * r0 + 8 * hh]);
+                const f32x4 cb = *reinterpret_cast<const f32x4*>(&sC1[32 * mb + 2 * r0 + 8 * hh + 4]);
+                float hv[8];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    hv[j] = act_fn(A1[m2][r0 + j] + ca[j], ACT);
+                    hv[4 + j] = act_fn(A1[m2][r0 + 4 + j] + cb[j], ACT);
+                }
+                Hop[ks] = pack_bf16x8(hv[0], hv[1], hv[2], hv[3], hv[4], hv[5], hv[6], hv[7]);
+            }
+#pragma unroll
+            for (int db = 0; db < 2; ++db) {
+                f32x16 o = zero_f32x16();
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8 aw = *reinterpret_cast<const bf16x8*>(
+                        &sW2[which][32 * db * kW + wrow + 16 * ks]);
+                    o = mfma_bf16(aw, Hop[ks], o);
+                }
+                if (which == 0) G[db] = o; else D[db] = o;
             }
         }
         if (ok) {
@@ -161,6 +185,8 @@ __global__ __launch_bounds__(256) void k_surrogate_bf16(
                     }
                 }
         }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) B[ks] = Bn[ks];
     }
 }
 
@@ -516,10 +542,13 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
         const float* C = v == SURR_MEAN_CONTEXT ? a.vmean : a.ctx;
         const int add_v = v == SURR_ADD_IDENTITY;
         if (a.dtype == DT_BF16)
-            hipLaunchKernelGGL(k_surrogate_bf16, dim3(nbs, a.H), dim3(256), 0, st,
-                               (const bf16*)a.V, a.modes, C, (const bf16*)a.g_w1, a.g_b1,
-                               (const bf16*)a.g_w2, a.g_b2, (const bf16*)a.d_w1, a.d_b1,
-                               (const bf16*)a.d_w2, a.d_b2, a.act, add_v, a.N, a.H, a.Y, a.ydt);
+        {
+            auto* kern = a.act == 1 ? k_surrogate_bf16<1> : k_surrogate_bf16<0>;
+            hipLaunchKernelGGL(kern, dim3(nbs, a.H), dim3(256), 0, st, (const bf16*)a.V, a.modes, C,
+                               (const bf16*)a.g_w1, a.g_b1, (const bf16*)a.g_w2, a.g_b2,
+                               (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2, add_v,
+                               a.N, a.H, a.Y, a.ydt);
+        }
         else
             hipLaunchKernelGGL(k_surrogate_f32, dim3(nbs, a.H), dim3(256), 0, st,
                                (const float*)a.V, a.modes, C, (const float*)a.g_w1, a.g_b1,
