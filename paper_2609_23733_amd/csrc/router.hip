@@ -250,25 +250,29 @@ struct Combined {
     float M, L;
 };
 
-template <int NV>
+// NG groups of 64 threads (the workgroup is 64 NG threads); group g sums a
+// contiguous run of chunks, and the groups' sums are added in group order.
+template <int NV, int NG>
 __device__ Combined combine_chunks(const float* __restrict__ part, int nchunks, int stride,
                                    float (&acc)[NV]) {
     __shared__ float s_w[1024];
-    __shared__ float s_red[4][kD * NV];
-    __shared__ float s_ml[8];
+    __shared__ float s_red[NG][kD * NV];
+    __shared__ float s_ml[2 * NG];
     const int t = threadIdx.x, d = t & 63, g = t >> 6;
     float M = -INFINITY;
-    for (int c = t; c < nchunks; c += 256) M = fmaxf(M, part[(int64_t)c * stride]);
+    for (int c = t; c < nchunks; c += 64 * NG) M = fmaxf(M, part[(int64_t)c * stride]);
     M = wave_max(M);
-    if ((t & 63) == 0) s_ml[t >> 6] = M;
+    if ((t & 63) == 0) s_ml[g] = M;
     __syncthreads();
-    M = fmaxf(fmaxf(s_ml[0], s_ml[1]), fmaxf(s_ml[2], s_ml[3]));
-    for (int c = t; c < nchunks; c += 256) {
+    M = s_ml[0];
+#pragma unroll
+    for (int i = 1; i < NG; ++i) M = fmaxf(M, s_ml[i]);
+    for (int c = t; c < nchunks; c += 64 * NG) {
         const float mc = part[(int64_t)c * stride];
         s_w[c] = (mc == -INFINITY) ? 0.f : exp2f_fast(mc - M);
     }
     __syncthreads();
-    const int q = (nchunks + 3) >> 2;
+    const int q = (nchunks + NG - 1) / NG;
     const int c0 = g * q, c1 = (c0 + q < nchunks) ? c0 + q : nchunks;
     float a[NV], lsum = 0.f;
 #pragma unroll
@@ -283,15 +287,19 @@ __device__ Combined combine_chunks(const float* __restrict__ part, int nchunks, 
     }
 #pragma unroll
     for (int v = 0; v < NV; ++v) s_red[g][v * kD + d] = a[v];
-    if (d == 0) s_ml[4 + g] = lsum;
+    if (d == 0) s_ml[NG + g] = lsum;
     __syncthreads();
-#pragma unroll
-    for (int v = 0; v < NV; ++v)
-        acc[v] = ((s_red[0][v * kD + d] + s_red[1][v * kD + d]) + s_red[2][v * kD + d]) +
-                 s_red[3][v * kD + d];
     Combined r;
     r.M = M;
-    r.L = ((s_ml[4] + s_ml[5]) + s_ml[6]) + s_ml[7];
+    r.L = s_ml[NG];
+#pragma unroll
+    for (int i = 1; i < NG; ++i) r.L += s_ml[NG + i];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        acc[v] = s_red[0][v * kD + d];
+#pragma unroll
+        for (int i = 1; i < NG; ++i) acc[v] += s_red[i][v * kD + d];
+    }
     return r;
 }
 
@@ -301,7 +309,7 @@ __global__ __launch_bounds__(256) void k_pool_combine(const float* __restrict__ 
     const int h = blockIdx.x;
     float acc[1];
     const Combined r =
-        combine_chunks<1>(part + (int64_t)h * nchunks * (2 + kD), nchunks, 2 + kD, acc);
+        combine_chunks<1, 4>(part + (int64_t)h * nchunks * (2 + kD), nchunks, 2 + kD, acc);
     if (threadIdx.x < kD) q_pool[h * kD + threadIdx.x] = acc[0] / r.L;
 }
 
@@ -312,8 +320,9 @@ __global__ __launch_bounds__(256) void k_pool_combine(const float* __restrict__ 
 // Thread layout: 8 lanes per (token, head) row, each owning 8 of the 64
 // values; a workgroup streams whole token rows ([H, 64] contiguous).
 // ------------------------------------------------------------------------
+constexpr int kRouteThreads = 512;
 template <int DT>
-__global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ Kp,
+__global__ __launch_bounds__(kRouteThreads) void k_route_partial(const void* __restrict__ Kp,
                                                        const void* __restrict__ Vp,
                                                        const float* __restrict__ q_pool,
                                                        float scale, int64_t N, int H,
@@ -322,7 +331,7 @@ __global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ 
     const int64_t t0 = (int64_t)c * chunk;
     const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
     const int tpr = H * 8;
-    const int rpi = 256 / tpr;
+    const int rpi = kRouteThreads / tpr;
     const int t = threadIdx.x;
     const int rr = t / tpr, hs = t % tpr, h = hs >> 3, seg = hs & 7;
     const bool active = rr < rpi;
@@ -375,7 +384,8 @@ __global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ 
         }
     }
     // Combine the rpi row phases of each (head, segment) in order.
-    __shared__ float s_m[256], s_l[256], s_C[256][9], s_s[256][9];
+    __shared__ float s_m[kRouteThreads], s_l[kRouteThreads], s_C[kRouteThreads][9],
+        s_s[kRouteThreads][9];
     s_m[t] = m;
     s_l[t] = l;
 #pragma unroll
@@ -414,16 +424,18 @@ __global__ __launch_bounds__(256) void k_route_partial(const void* __restrict__ 
     }
 }
 
-// K9b: per head, combine the routing partials; write stats, score, ctx, vmean.
-__global__ __launch_bounds__(256) void k_route_combine(const float* __restrict__ part, int nchunks,
+// K9b: per head, combine the routing partials (up to 512 chunks, 16 groups of
+// 64 threads); write stats, score, ctx, vmean.
+constexpr int kRouteCombineGroups = 16;
+__global__ __launch_bounds__(64 * kRouteCombineGroups) void k_route_combine(const float* __restrict__ part, int nchunks,
                                                        int64_t N, float* __restrict__ stats,
                                                        float* __restrict__ score,
                                                        float* __restrict__ ctx,
                                                        float* __restrict__ vmean) {
     const int h = blockIdx.x, d = threadIdx.x;
     float acc[2];
-    const Combined r = combine_chunks<2>(part + (int64_t)h * nchunks * (2 + 2 * kD), nchunks,
-                                         2 + 2 * kD, acc);
+    const Combined r = combine_chunks<2, kRouteCombineGroups>(
+        part + (int64_t)h * nchunks * (2 + 2 * kD), nchunks, 2 + 2 * kD, acc);
     if (d < kD) {
         ctx[h * kD + d] = acc[0] / r.L;
         vmean[h * kD + d] = acc[1] / (float)N;
@@ -527,12 +539,12 @@ void launch_router(const RouterArgs& a, hipStream_t st) {
     hipLaunchKernelGGL(k_pool_combine, dim3(a.H), dim3(256), 0, st, a.part1, (int)a.n1,
                        a.q_pool);
     if (a.dtype == DT_BF16)
-        hipLaunchKernelGGL(k_route_partial<DT_BF16>, dim3((unsigned)a.n2), dim3(256), 0, st, a.K,
+        hipLaunchKernelGGL(k_route_partial<DT_BF16>, dim3((unsigned)a.n2), dim3(kRouteThreads), 0, st, a.K,
                            a.V, a.q_pool, a.scale, a.N, a.H, a.chunk2, a.part2);
     else
-        hipLaunchKernelGGL(k_route_partial<DT_F32>, dim3((unsigned)a.n2), dim3(256), 0, st, a.K,
+        hipLaunchKernelGGL(k_route_partial<DT_F32>, dim3((unsigned)a.n2), dim3(kRouteThreads), 0, st, a.K,
                            a.V, a.q_pool, a.scale, a.N, a.H, a.chunk2, a.part2);
-    hipLaunchKernelGGL(k_route_combine, dim3(a.H), dim3(256), 0, st, a.part2, (int)a.n2, a.N,
+    hipLaunchKernelGGL(k_route_combine, dim3(a.H), dim3(64 * kRouteCombineGroups), 0, st, a.part2, (int)a.n2, a.N,
                        a.stats, a.score, a.ctx, a.vmean);
 }
 
