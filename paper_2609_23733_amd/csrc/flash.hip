@@ -658,8 +658,11 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 
 // K6c: Y of the tail items that K6a split over workgroups: the parts' O and
 // l added in workgroup order (fixed, so results are deterministic), then
-// O 2^e_h / l.  One workgroup of 256 threads per tail item; items that K6a
-// finished whole or left to K6b exit at once.
+// O 2^e_h / l.  One workgroup of 256 threads per (tail item, 64-query
+// block): 4 threads per query, 16 consecutive values each, so a query's
+// 256-byte row of a part is read whole.  Items that K6a finished whole or
+// left to K6b exit at once.
+constexpr int kCombRows = 64;
 __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt,
                                                        const int32_t* __restrict__ wide_items,
@@ -670,7 +673,7 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
     const int full = active / G * G, R = active - full;
-    const int i = blockIdx.x;
+    const int i = blockIdx.x / (kBQf / kCombRows), rb = blockIdx.x % (kBQf / kCombRows);
     if (i >= R) return;
     const int64_t T = (int64_t)R * nkt;
     const int Gt = tail_groups(T, G);
@@ -686,39 +689,39 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
         const int k = i == (int)(tail_start(v, T, Gt) / nkt) ? 0 : 1;
         return part + (int64_t)(v * 2 + k) * kPartFloats;
     };
-#pragma unroll 1
-    for (int j = 0; j < kBQf / 256; ++j) {
-        const int qr = threadIdx.x + 256 * j;
-        const int64_t qi = (int64_t)qt * kBQf + qr;
-        if (qi >= N) continue;
-        float lt = 0.f;
-        for (int v = wf; v <= wl; ++v) lt += pslot(v)[kBQf * kD + qr];
-        if (off) off[(int64_t)h * N + qi] = __log2f(lt);
-        const float inv = vsc[2 * slot + 1] / lt;
-#pragma unroll 1
-        for (int d0 = 0; d0 < kD; d0 += 8) {
-            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            for (int v = wf; v <= wl; ++v) {
-                const float* src = pslot(v) + qr * kD + d0;
-                const float4 a = *reinterpret_cast<const float4*>(src);
-                const float4 b = *reinterpret_cast<const float4*>(src + 4);
-                acc[0] += a.x; acc[1] += a.y; acc[2] += a.z; acc[3] += a.w;
-                acc[4] += b.x; acc[5] += b.y; acc[6] += b.z; acc[7] += b.w;
-            }
-            const int64_t off = (qi * H + h) * kD + d0;
-            if (ydt == DT_BF16) {
-                bf16x8 o;
+    const int qr = rb * kCombRows + (threadIdx.x >> 2), d0 = (threadIdx.x & 3) * 16;
+    const int64_t qi = (int64_t)qt * kBQf + qr;
+    if (qi >= N) return;
+    float lt = 0.f;
+    for (int v = wf; v <= wl; ++v) lt += pslot(v)[kBQf * kD + qr];
+    if (off && d0 == 0) off[(int64_t)h * N + qi] = __log2f(lt);
+    const float inv = vsc[2 * slot + 1] / lt;
+    float acc[16];
 #pragma unroll
-                for (int k = 0; k < 8; ++k) o[k] = (bf16)(acc[k] * inv);
-                *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + off) = o;
-            } else {
-                float* yo = reinterpret_cast<float*>(Y) + off;
-                *reinterpret_cast<float4*>(yo) =
-                    make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
-                *reinterpret_cast<float4*>(yo + 4) =
-                    make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
-            }
+    for (int k = 0; k < 16; ++k) acc[k] = 0.f;
+    for (int v = wf; v <= wl; ++v) {
+        const float4* src = reinterpret_cast<const float4*>(pslot(v) + qr * kD + d0);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float4 a = src[k];
+            acc[4 * k] += a.x; acc[4 * k + 1] += a.y; acc[4 * k + 2] += a.z; acc[4 * k + 3] += a.w;
         }
+    }
+    const int64_t yo = (qi * H + h) * kD + d0;
+    if (ydt == DT_BF16) {
+#pragma unroll
+        for (int k8 = 0; k8 < 2; ++k8) {
+            bf16x8 o;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) o[k] = (bf16)(acc[8 * k8 + k] * inv);
+            *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + yo + 8 * k8) = o;
+        }
+    } else {
+        float* y = reinterpret_cast<float*>(Y) + yo;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            *reinterpret_cast<float4*>(y + 4 * k) = make_float4(
+                acc[4 * k] * inv, acc[4 * k + 1] * inv, acc[4 * k + 2] * inv, acc[4 * k + 3] * inv);
     }
 }
 
@@ -1127,7 +1130,8 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
                            0, st, (const bf16*)a.Q, (const f16*)a.kh, (const f16*)a.vt,
                            (const float*)a.kmax, (const float*)a.vsc, a.buckets, a.N, a.H, nqf,
                            nkt, c, a.qflag, a.part, G, a.Y, a.ydt, a.off);
-        hipLaunchKernelGGL(k_flash_combine, dim3(G), dim3(256), 0, st, a.buckets, a.N, a.H, nqf,
+        hipLaunchKernelGGL(k_flash_combine, dim3(G * (kBQf / kCombRows)), dim3(256), 0, st,
+                           a.buckets, a.N, a.H, nqf,
                            nkt, (const int32_t*)a.qflag, (const float*)a.part,
                            (const float*)a.vsc, G, a.Y, a.ydt, a.off);
         hipLaunchKernelGGL(a.off ? k_flash_bf16_wide<true> : k_flash_bf16_wide<false>,
