@@ -35,7 +35,7 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "2f5d8665582838e99e0c374d7c16df485a01c6b12332b34f7e19541f3404ac5e",
+    "source_sha256": "7d9c23b209df612007c32fc07626a6722ece575fb37687be577929f9224d108d",
     "S": 100, "n_full": 4,
     "fetch_kib": 1531131, "write_kib": 104952,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
