@@ -261,6 +261,41 @@ def test_permutation_equivariance_gpu():
         assert np.abs(Yb[:, h] - ref[:, h]).max() <= 1e-4 * rms(ref[:, h])
 
 
+# ------------------------------------------ seeded random configurations
+
+def _random_configurations(n, seed=4242):
+    """n seeded draws over the layer's small-shape space: views, tokens per
+    view (ragged around the 64-key and query tiles), head count, a mode per
+    head, operand dtype, Y dtype, activation and input sharpness."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        H = int(rng.integers(1, 17))
+        cases.append(dict(i=i, S=int(rng.integers(1, 4)), P=int(rng.integers(1, 600)), H=H,
+                          dtype=("f32", "bf16")[int(rng.integers(0, 2))],
+                          y_bf16=bool(rng.integers(0, 2)), act=int(rng.integers(0, 2)),
+                          sharp=bool(rng.integers(0, 2)),
+                          modes=rng.integers(0, 3, size=H).astype(np.uint8)))
+    return cases
+
+
+@pytest.mark.parametrize("c", _random_configurations(12), ids=lambda c: "r%d" % c["i"])
+def test_random_configurations(c):
+    """Router state, modes, buckets and every output row against the oracle
+    on a seeded random configuration."""
+    label = "random %d: S=%d P=%d H=%d %s y=%s act=%d sharp=%d modes=%s" % (
+        c["i"], c["S"], c["P"], c["H"], c["dtype"], "bf16" if c["y_bf16"] else "f32", c["act"],
+        c["sharp"], "".join(str(int(m)) for m in c["modes"]))
+    log(label)
+    x = synth.make_layer(c["S"], c["P"], dtype=c["dtype"], key=(40, c["i"]), sharp=c["sharp"],
+                         H=c["H"], modes=c["modes"], qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.bfloat16 if c["y_bf16"] else torch.float32, act=c["act"])
+    ref = oracle_layer(x, act=c["act"])
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], c["dtype"], c["y_bf16"],
+            label="random %d" % c["i"])
+
+
 # ------------------------------------------------- full-size workloads
 
 @pytest.mark.parametrize("wl,n_full", [("s32_bf16", 4), ("s32_bf16", 16), ("s100_bf16", 4),
