@@ -47,44 +47,54 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int n = lane & 31, hh = lane >> 5;
 
-    bf16x8 Wop[2][4], Uop[2][4];
-    float wv[2][16];
+    // W_h rows 0-63 then U_h rows 0-63 (bf16, 144-byte rows) and w_h, staged
+    // in LDS for the token loop; the same memory holds the wave partials
+    // afterwards.
+    __shared__ __attribute__((aligned(16))) float smem[4 * 64 * 33];
+    __shared__ float s_ml[4][2];
+    bf16* sWU = reinterpret_cast<bf16*>(smem);
+    float* sw = smem + 128 * 36;   // after the 128 rows of 72 bf16
     if (!mean_pool) {
         const bf16* Wh = W + (int64_t)h * kL * kD;
         const bf16* Uh = U + (int64_t)h * kL * kD;
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                Wop[mb][ks] = load_bf16x8(Wh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
-                Uop[mb][ks] = load_bf16x8(Uh + (32 * mb + n) * kD + 16 * ks + 8 * hh);
-            }
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                wv[mb][r] =
-                    bf16_to_f32(w[(int64_t)h * kL + 32 * mb + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+        for (int i = threadIdx.x; i < 128 * 8; i += 256) {
+            const int row = i >> 3, seg = (i & 7) * 8;
+            const bf16* src = (row < 64 ? Wh : Uh) + (row & 63) * kD + seg;
+            *reinterpret_cast<bf16x8*>(&sWU[row * 72 + seg]) = load_bf16x8(src);
+        }
+        if (threadIdx.x < kL) sw[threadIdx.x] = bf16_to_f32(w[(int64_t)h * kL + threadIdx.x]);
     }
+    __syncthreads();
 
     float m = -INFINITY, l = 0.f;
     float acc[32];
 #pragma unroll
     for (int i = 0; i < 32; ++i) acc[i] = 0.f;
 
+    // Each wave takes 32 tokens at a time; the next block's Q is loaded while
+    // this one is computed.  Tail lanes read a valid row (the chunk's first)
+    // and zero it afterwards.
+    auto load_q = [&](int64_t tb, bf16x8 (&B)[4]) {
+        const int64_t tok = tb + n;
+        const bf16* qrow = Q + ((tok < t1 ? tok : t0) * H + h) * kD;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) B[ks] = load_bf16x8(qrow + 16 * ks + 8 * hh);
+    };
+    bf16x8 Bc[4], Bn[4];
+    load_q(t0 + 32 * wave, Bc);
     for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
         const int64_t tok = tb + n;
         const bool valid = tok < t1;
+        load_q(tb + 128 < t1 ? tb + 128 : tb, Bn);
         bf16x8 B[4];
-        // Tail lanes read a valid row (the chunk's first) and zero it afterwards.
-        const bf16* qrow = Q + ((valid ? tok : t0) * H + h) * kD;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            B[ks] = load_bf16x8(qrow + 16 * ks + 8 * hh);
-            if (!valid) B[ks] = zero_bf16x8();
-        }
+        for (int ks = 0; ks < 4; ++ks) B[ks] = valid ? Bc[ks] : zero_bf16x8();
         float a = 0.f;
         if (!mean_pool) {
+            // An opaque offset keeps the fragment reads in the loop (hoisted,
+            // they would hold 96 registers for the whole loop).
+            int frow = n * 72 + 8 * hh;
+            asm volatile("" : "+v"(frow));
             f32x16 aW[2], aU[2];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
@@ -92,16 +102,25 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
                 aU[mb] = zero_f32x16();
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
-                    aW[mb] = mfma_bf16(Wop[mb][ks], B[ks], aW[mb]);
-                    aU[mb] = mfma_bf16(Uop[mb][ks], B[ks], aU[mb]);
+                    const bf16x8 wop = *reinterpret_cast<const bf16x8*>(
+                        &sWU[32 * mb * 72 + frow + 16 * ks]);
+                    const bf16x8 uop = *reinterpret_cast<const bf16x8*>(
+                        &sWU[(64 + 32 * mb) * 72 + frow + 16 * ks]);
+                    aW[mb] = mfma_bf16(wop, B[ks], aW[mb]);
+                    aU[mb] = mfma_bf16(uop, B[ks], aU[mb]);
                 }
             }
             float pa = 0.f;
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    pa += wv[mb][r] * tanh_times_sigmoid(aW[mb][r], aU[mb][r]);
+                for (int g = 0; g < 4; ++g) {
+                    // hidden units 32 mb + 8 g + 4 hh + i in registers 4 g + i
+                    const f32x4 wq = *reinterpret_cast<const f32x4*>(&sw[32 * mb + 8 * g + 4 * hh]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        pa += wq[i] * tanh_times_sigmoid(aW[mb][4 * g + i], aU[mb][4 * g + i]);
+                }
             a = (pa + __shfl_xor(pa, 32)) * kLog2e;
         }
         if (!valid) a = -INFINITY;
@@ -117,11 +136,14 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
 #pragma unroll
             for (int j = 0; j < 8; ++j) acc[8 * ks + j] = acc[8 * ks + j] * al + p * bf16_to_f32(B[ks][j]);
         m = mn;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) Bc[ks] = Bn[ks];
     }
+    __syncthreads();   // the staged weights are no longer read
 
     // Combine lanes (same hh share a d set) and waves through LDS.
-    __shared__ float s_acc[4][64][33];
-    __shared__ float s_ml[4][2];
+    float (*s_acc)[64][33] = reinterpret_cast<float (*)[64][33]>(smem);
+
     const float lw = wave_sum(l);
 #pragma unroll
     for (int i = 0; i < 32; ++i) s_acc[wave][lane][i] = acc[i];
