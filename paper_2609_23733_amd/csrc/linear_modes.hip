@@ -25,7 +25,7 @@ __device__ __forceinline__ float sigmoid_fast(float x) {
     return rcp_fast(1.f + exp2f_fast(-kLog2e * x));
 }
 
-constexpr int kSurrRows = 512;   // tokens per workgroup
+constexpr int kSurrRows = 384;   // tokens per workgroup
 constexpr int kW = 72;           // bf16 LDS row stride
 
 // ------------------------------------------------------------------------
