@@ -35,9 +35,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "7d9c23b209df612007c32fc07626a6722ece575fb37687be577929f9224d108d",
+    "source_sha256": "a3c727755cee073de6e653881026f3c6dd082ae212b386c1c1da0d3a5fcfe43e",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1531131, "write_kib": 104952,
+    "fetch_kib": 1531037, "write_kib": 104949,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 

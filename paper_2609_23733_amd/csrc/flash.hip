@@ -62,10 +62,18 @@ __global__ __launch_bounds__(256) void k_vmax_partial(const bf16* __restrict__ V
     const int64_t r1 = (r0 + kVmaxTiles * kBK < N) ? r0 + kVmaxTiles * kBK : N;
     const int seg = (threadIdx.x & 7) * 8;
     float m = 0.f;
-    for (int64_t row = r0 + (threadIdx.x >> 3); row < r1; row += 32) {
-        const bf16x8 v = load_bf16x8(V + (row * H + h) * kD + seg);
+    // Four rows per thread and iteration, their loads issued together.
+    for (int64_t row = r0 + (threadIdx.x >> 3); row < r1; row += 128) {
+        bf16x8 v[4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(bf16_to_f32(v[j])));
+        for (int u = 0; u < 4; ++u) {
+            const int64_t rr = row + 32 * u;
+            v[u] = rr < r1 ? load_bf16x8(V + (rr * H + h) * kD + seg) : zero_bf16x8();
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(bf16_to_f32(v[u][j])));
     }
     __shared__ float red[4];
     m = block_max256(m, red);
