@@ -74,9 +74,10 @@ __global__ __launch_bounds__(256) void k_layernorm(const bf16* __restrict__ X,
 // holds token l % 32 of a block and features 8 (r / 4) + 4 (l / 32) + r % 4 in
 // its register r: four consecutive features per store, and the rotary pair
 // (j, j + 16) of a 32-feature half in registers r and r + 8 of one lane.
-// Tiles are ordered in groups of four feature tiles per token tile, and
-// consecutive tiles share an XCD, so an XCD's L2 keeps a token tile for four
-// feature tiles and a group of weight tiles for all its token tiles.
+// Tiles are ordered in groups of feature tiles per token tile (four in B2b,
+// all of them in B2a), and consecutive tiles share an XCD, so an XCD's L2
+// keeps a token tile for its group of feature tiles and a group of weight
+// tiles for all its token tiles.
 // Every output sums its Kd products in the same order (stage by stage, 16 per
 // MFMA) in both kernels below, so they produce identical bits.
 // ------------------------------------------------------------------------
@@ -99,10 +100,11 @@ struct GemmArgs {
     float log2_base;      // QKV: log2 of the rotary base
 };
 
-// Tile (L) of the grouped order: features f0.., tokens t0...
-__device__ __forceinline__ void gemm_tile(int L, int ntt, int& f0, int64_t& t0) {
-    const int grp = L / (kGGroup * ntt), in = L - grp * kGGroup * ntt;
-    const int tt = in / kGGroup, ft = grp * kGGroup + in % kGGroup;
+// Tile (L) of the grouped order, `group` feature tiles per token tile:
+// features f0.., tokens t0...
+__device__ __forceinline__ void gemm_tile(int L, int ntt, int group, int& f0, int64_t& t0) {
+    const int grp = L / (group * ntt), in = L - grp * group * ntt;
+    const int tt = in / group, ft = grp * group + in % group;
     f0 = ft * kGM;
     t0 = (int64_t)tt * kGN;
 }
@@ -234,8 +236,11 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
     __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
     __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
 
+    // All of a token tile's feature tiles in one group (FFN 1: 16, so an XCD's
+    // 32 tiles are 2 token tiles x 16 feature tiles; 3 % faster than groups
+    // of 4 there).
     auto tile_of = [&](int i, int& f0, int64_t& t0, int64_t& tl) {
-        gemm_tile(i * G + slot, ntt, f0, t0);
+        gemm_tile(i * G + slot, ntt, nft, f0, t0);
         tl = t0 + kGN <= g.T ? t0 : g.T - kGN;
     };
 
@@ -367,7 +372,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_w8(GemmArgs g) {
     const int total = nft * ntt;
     int f0;
     int64_t t0;
-    gemm_tile(xcd_remap(blockIdx.x, total), ntt, f0, t0);
+    gemm_tile(xcd_remap(blockIdx.x, total), ntt, kGGroup, f0, t0);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int n = lane & 31, hh = lane >> 5;
     const int wm = wave >> 2, wn = wave & 3;
