@@ -74,14 +74,13 @@ __global__ __launch_bounds__(256) void k_layernorm(const bf16* __restrict__ X,
 // holds token l % 32 of a block and features 8 (r / 4) + 4 (l / 32) + r % 4 in
 // its register r: four consecutive features per store, and the rotary pair
 // (j, j + 16) of a 32-feature half in registers r and r + 8 of one lane.
-// Tiles are ordered in groups of feature tiles per token tile (four in B2b,
-// all of them in B2a), and consecutive tiles share an XCD, so an XCD's L2
-// keeps a token tile for its group of feature tiles and a group of weight
-// tiles for all its token tiles.
+// Tiles are ordered with all of a token tile's feature tiles together, and
+// consecutive tiles share an XCD, so an XCD's L2 keeps a token tile for all
+// its feature tiles while the weights stream by.
 // Every output sums its Kd products in the same order (stage by stage, 16 per
 // MFMA) in both kernels below, so they produce identical bits.
 // ------------------------------------------------------------------------
-constexpr int kGM = 256, kGN = 256, kGK = 64, kGRow = 72, kGGroup = 4;
+constexpr int kGM = 256, kGN = 256, kGK = 64, kGRow = 72;
 constexpr int kGemmWG = 256;   // persistent workgroups: one per CU
 
 enum { EPI_QKV = 0, EPI_GELU = 1, EPI_RESID = 2 };
@@ -238,7 +237,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
 
     // All of a token tile's feature tiles in one group (FFN 1: 16, so an XCD's
     // 32 tiles are 2 token tiles x 16 feature tiles; 3 % faster than groups
-    // of 4 there).
+    // of 4 there, and 2.6 % on QKV in B2b).
     auto tile_of = [&](int i, int& f0, int64_t& t0, int64_t& tl) {
         gemm_tile(i * G + slot, ntt, nft, f0, t0);
         tl = t0 + kGN <= g.T ? t0 : g.T - kGN;
@@ -372,7 +371,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_w8(GemmArgs g) {
     const int total = nft * ntt;
     int f0;
     int64_t t0;
-    gemm_tile(xcd_remap(blockIdx.x, total), ntt, kGGroup, f0, t0);
+    gemm_tile(xcd_remap(blockIdx.x, total), ntt, nft, f0, t0);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int n = lane & 31, hh = lane >> 5;
     const int wm = wave >> 2, wn = wave & 3;
@@ -450,8 +449,8 @@ static void gemm_launch(const GemmArgs& a, hipStream_t st) {
     hipLaunchKernelGGL(k_gemm_w8<EPI>, dim3(total), dim3(512), 0, st, a);
 }
 
-// F a multiple of 4 x 256 (whole groups of feature tiles), Kd of 128 (the
-// persistent kernel takes stages in pairs); the block's shapes are 1024 x
+// F a multiple of 256, Kd of 128 (the persistent kernel takes stages in
+// pairs); the block's shapes are 1024 x
 // {3, 1, 4} by 1024 and 1024 by 4096.
 static void gemm(int epi, const GemmArgs& a, hipStream_t st) {
     if (epi == EPI_QKV)
