@@ -70,44 +70,70 @@ def layer_flops(N, n_full, n_surr, n_mean):
     return flops_full(N, n_full) + router + 8 * D * L * N * n_surr + N * D * n_mean
 
 
+STAGES = ("router", "assign", "gather", "full", "linear")
+
+
 def measure(layer, steps, warmup):
+    """Average ms per layer pass over `steps` passes (HIP events around all of
+    them), and per-stage averages from events recorded between the stages."""
     import torch
     for _ in range(warmup):
         layer.step()
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(steps)]
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record()
     for k in range(steps):
-        layer.step(events=ev[k])
+        layer.step(stages=ev[k])
     t1.record()
     torch.cuda.synchronize()
     ms_step = t0.elapsed_time(t1) / steps
-    full = sorted(a.elapsed_time(b) for a, b in ev)
-    return ms_step, sum(full) / len(full), full[len(full) // 2]
+    stage = {name: sum(e[i].elapsed_time(e[i + 1]) for e in ev) / steps
+             for i, name in enumerate(STAGES)}
+    return ms_step, stage
 
 
-def run_workload(S, n_full, steps, warmup, seed_key):
+def stage_bytes(N, n_full, n_surr, n_mean, b_in, b_out):
+    """Algorithmic HBM bytes per stage: the router reads Q, K and V once; the
+    gather reads K and V of each FULL head and writes its fp16 K and V^T
+    tiles; SURR heads read V and write Y, MEAN heads write Y."""
+    return {"router": 3.0 * N * HEADS * D * b_in,
+            "gather": float(N) * D * n_full * (2 * b_in + 2 * 2) if b_in == 2 else 0.0,
+            "linear": float(N) * D * (n_surr * (b_in + b_out) + n_mean * b_out)}
+
+
+def run_workload(S, n_full, steps, warmup, seed_key, dtype="bf16", sharp=False):
     import torch
     from paper_2609_23733_amd import synth, vp
-    x = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=n_full, key=seed_key,
-                         qkv_device="cuda")
-    layer = vp.RoutedLayer(x, y_dtype=torch.bfloat16)
-    ms_step, full_avg, full_med = measure(layer, steps, warmup)
+    x = synth.make_layer(S, P_TOKENS, dtype=dtype, n_full=n_full, key=seed_key,
+                         qkv_device="cuda", sharp=sharp)
+    ydt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    layer = vp.RoutedLayer(x, y_dtype=ydt)
+    ms_step, stage = measure(layer, steps, warmup)
     modes = layer.modes.cpu().numpy()
     counts = [int((modes == m).sum()) for m in range(3)]
     assert counts[2] == n_full, "router did not produce the target FULL count"
     N = S * P_TOKENS
     fl = layer_flops(N, counts[2], counts[1], counts[0])
     ff = flops_full(N, counts[2])
-    rec = dict(S=S, N=N, n_full=counts[2], n_surr=counts[1], n_mean=counts[0],
+    peak = PEAK_BF16_TFLOPS if dtype == "bf16" else PEAK_FP32_TFLOPS
+    b_in = 2 if dtype == "bf16" else 4
+    b_out = 2 if ydt == torch.bfloat16 else 4
+    byt = stage_bytes(N, counts[2], counts[1], counts[0], b_in, b_out)
+    gbs = {k: round(v / stage[k] / 1e6, 1) for k, v in byt.items() if v and stage[k] > 0}
+    full_ms = stage["full"]
+    rec = dict(S=S, N=N, dtype=dtype, inputs="sharp N(0,1) Q/K" if sharp else "N(0,1/64)",
+               n_full=counts[2], n_surr=counts[1], n_mean=counts[0],
                ms=round(ms_step, 4), tflops=round(fl / ms_step / 1e9, 2),
-               frac_bf16_peak=round(fl / ms_step / 1e9 / PEAK_BF16_TFLOPS, 4),
-               full_kernel_ms=round(full_avg, 4),
-               full_kernel_tflops=round(ff / full_avg / 1e9, 2) if ff else None,
-               full_kernel_frac=round(ff / full_avg / 1e9 / PEAK_BF16_TFLOPS, 4) if ff else None)
+               frac_peak=round(fl / ms_step / 1e9 / peak, 4),
+               full_kernel_ms=round(full_ms, 4),
+               full_kernel_tflops=round(ff / full_ms / 1e9, 2) if ff else None,
+               full_kernel_frac=round(ff / full_ms / 1e9 / peak, 4) if ff else None,
+               peak_tflops=peak,
+               stage_ms={k: round(v, 4) for k, v in stage.items()},
+               hbm_gbs=gbs,
+               non_full_frac=round(1.0 - full_ms / ms_step, 4))
     return rec, layer, x
 
 
@@ -138,7 +164,8 @@ def run_variants(x, steps, warmup):
     out = []
     for name, rule, pool, sv in VARIANTS:
         layer = vp.RoutedLayer(x, rule=rule, y_dtype=torch.bfloat16, pool=pool, surr_variant=sv)
-        ms_step, full_avg, _ = measure(layer, steps, warmup)
+        ms_step, stage = measure(layer, steps, warmup)
+        full_avg = stage["full"]
         t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         xd = layer.x   # the layer's device copy of the inputs
         lin = lambda: vp.linear_heads(xd.V, layer.modes, layer.state, xd.surr, xd.S, xd.P,
@@ -265,27 +292,25 @@ def run_stack(S, layers, steps, warmup, tome_ratio=None):
 
 
 def run_layer_stack(S, layers, steps, warmup):
-    """A stack of routed layers at S views with independent router and
-    surrogate weights per layer and FULL-head counts drawn from {1, ..., 6}
-    per layer.  The layers read one seeded Q/K/V (the attention's cost does
-    not depend on the values) and share one workspace and output buffer.
+    """A stack of routed layers at S views, each with its own seeded Q/K/V
+    (drawn on the device before timing: 4.2 GB per layer at S = 500, all 24
+    resident in HBM), router and surrogate weights, and a FULL-head count
+    drawn from {1, ..., 6}; the layers share one workspace and output buffer.
     HIP events around each layer; MFMA work 4 N^2 d per FULL head."""
     import numpy as np
     import torch
     from paper_2609_23733_amd import synth, vp
     rng = np.random.Generator(np.random.PCG64(synth.derive_seed(S, 600)))
     n_full = rng.integers(1, 7, size=layers)
-    base = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=int(n_full[0]), key=(S, 600),
-                            qkv_device="cuda")
     N = S * P_TOKENS
     ws = vp.alloc_workspace(S, P_TOKENS, HEADS, torch.bfloat16)
     Y = torch.empty(N, HEADS, D, dtype=torch.bfloat16, device="cuda")
     lys = []
     for l in range(layers):
         x = synth.make_layer(S, P_TOKENS, dtype="bf16", n_full=int(n_full[l]), key=(S, 600 + l),
-                             with_qkv=False)
-        x = dataclasses.replace(x, Q=base.Q, K=base.K, V=base.V)
+                             qkv_device="cuda")
         lys.append(vp.RoutedLayer(x, y_dtype=torch.bfloat16, ws=ws, Y=Y))
+    torch.cuda.synchronize()
 
     def once(evs=None):
         for l, ly in enumerate(lys):
@@ -308,9 +333,10 @@ def run_layer_stack(S, layers, steps, warmup):
     got = [int((ly.modes == 2).sum()) for ly in lys]
     fl = sum(flops_full(N, n) for n in got)
     tot = float(per.sum())
-    del lys, ws, Y, base
+    del lys, ws, Y
     torch.cuda.empty_cache()
-    return dict(S=S, N=N, layers=layers, n_full=got, per_layer_ms=[round(float(v), 2) for v in per],
+    return dict(S=S, N=N, layers=layers, n_full=got, qkv="independent seeded Q/K/V per layer",
+                per_layer_ms=[round(float(v), 2) for v in per],
                 total_ms=round(tot, 1), tflops=round(fl / tot / 1e9, 1),
                 frac_bf16_peak=round(fl / tot / 1e9 / PEAK_BF16_TFLOPS, 4))
 
@@ -407,13 +433,48 @@ def run_tome(S, n_full, ratios, steps, warmup, unmerged_ms):
     return dict(S=S, N=N, n_full=n_full, unmerged_layer_ms=round(unmerged_ms, 4), by_ratio=out)
 
 
+def host_cpus():
+    """What the host offers the oracle: logical CPUs, the CPUs this process may
+    run on, the cgroup CPU quota (if any) and the CPU model string."""
+    info = {"nproc": os.cpu_count()}
+    try:
+        info["affinity"] = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        info["affinity"] = None
+    try:
+        q, per = open("/sys/fs/cgroup/cpu.max").read().split()[:2]
+        info["cgroup_quota_cpus"] = None if q == "max" else round(int(q) / int(per), 2)
+    except (OSError, ValueError):
+        info["cgroup_quota_cpus"] = None
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    info["model"] = model
+    return info
+
+
+# CPUs that one GPU's share of the box provides (the oracle's thread cap there).
+CPU_SHARE = 16
+
+
 def cpu_baseline(x, rows_per_head=800):
     """The fp64 oracle on a bounded sample of the same layer: the router over
     all N tokens, then `rows_per_head` query rows of every FULL and SURR head,
-    extrapolated linearly to all N rows (every row costs the same)."""
-    import numpy as np
+    extrapolated linearly to all N rows (every row costs the same).  It runs
+    on every CPU the process may use, up to the per-GPU share of the box."""
     import oracle
     from paper_2609_23733_amd import synth
+    host = host_cpus()
+    avail = [v for v in (host["nproc"], host["affinity"], CPU_SHARE) if v]
+    if host["cgroup_quota_cpus"]:
+        avail.append(max(1, int(host["cgroup_quota_cpus"])))
+    nt = max(1, min(avail))
+    os.environ["VP_ORACLE_THREADS"] = str(nt)
     Q, K, V = oracle.as_f32(x.Q), oracle.as_f32(x.K), oracle.as_f32(x.V)
     N = Q.shape[0]
     t0 = time.perf_counter()
@@ -433,7 +494,7 @@ def cpu_baseline(x, rows_per_head=800):
         t_rows += time.perf_counter() - t1
     total = t_router + t_rows * N / len(rows)
     return dict(value=round(total * 1e3, 1), unit="ms", cores=oracle.threads_used(),
-                kind="oracle",
+                kind="oracle", host=host,
                 sample="router over all %d tokens (%.1f s) + %d sampled query rows per FULL and "
                        "SURR head (%.1f s), extrapolated to %d rows; MEAN heads free"
                        % (N, t_router, len(rows), t_rows, N),
@@ -506,15 +567,23 @@ def main():
         for t in stack["tome"]:
             t["speedup_vs_unmerged_stack"] = round(stack["total_ms"] / t["total_ms"], 2)
     if not args.no_sweep:
-        for S, nf in ((8, 8), (32, 4), (32, 16), (100, 2), (100, 8), (100, 16), (500, 4)):
-            r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 0))
+        # S = 2 in fp32 (the fp32 FULL kernel against the fp32 matrix peak), the
+        # other view counts and FULL-head counts, and S = 100 with sharp FULL
+        # heads (logit bounds past the zero-reference window: the running-
+        # reference-point path carries the FULL stage).
+        sweep = ((2, 8, "f32", False), (8, 8, "bf16", False), (32, 4, "bf16", False),
+                 (32, 16, "bf16", False), (100, 2, "bf16", False), (100, 8, "bf16", False),
+                 (100, 16, "bf16", False), (500, 4, "bf16", False), (100, 4, "bf16", True))
+        for S, nf, dt, sharp in sweep:
+            r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 3 if sharp else 0),
+                                     dtype=dt, sharp=sharp)
             by.append(r)
             del lyr
-        torch.cuda.empty_cache()
+            torch.cuda.empty_cache()
         ref16 = [r for r in by if r["S"] == 100 and r["n_full"] == 16]
         if ref16:
             for r in by:
-                if r["S"] == 100:
+                if r["S"] == 100 and r["inputs"] == head["inputs"]:
                     r["speedup_vs_all_full"] = round(ref16[0]["ms"] / r["ms"], 3)
                     r["ideal_speedup"] = round(16.0 / max(r["n_full"], 1), 3)
 
@@ -540,13 +609,23 @@ def main():
                    "n_full": head["n_full"], "n_surr": head["n_surr"], "n_mean": head["n_mean"],
                    "layout": "Q/K/V [S*P, 16, 64] row-major"},
         "tflops": head["tflops"],
-        "frac_bf16_peak": head["frac_bf16_peak"],
+        "frac_bf16_peak": head["frac_peak"],
         "roofline": {"kernel": "k_flash_bf16", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": flash_traffic(100, head["n_full"]),
+                     "contraction": "fp16 MFMA 32x32x16 (bf16 Q, K converted to fp16; P and "
+                                    "the per-head power-of-two-scaled V in fp16), fp32 "
+                                    "accumulate; the fp16 and bf16 dense MFMA peaks are equal",
                      "algorithmic_flop_per_launch": ff,
                      "avg_launch_ms": round(head["full_kernel_ms"], 4)},
+        "hbm": {"router_gbs": head["hbm_gbs"].get("router"),
+                "gather_gbs": head["hbm_gbs"].get("gather"),
+                "linear_heads_gbs": head["hbm_gbs"].get("linear"),
+                "peak_gbs": PEAK_HBM_GBS,
+                "note": "algorithmic bytes / HIP-event stage time: router = vp_router_score "
+                        "(Q, K, V read once), gather = vp_gather_full_heads (K, V read, fp16 K "
+                        "and V^T written per FULL head), linear = vp_linear_heads"},
         "by_workload": by,
     }
     if variants is not None:

@@ -151,13 +151,19 @@ vp_status vp_router_score(const vp_shape *shape, const void *Q, const void *K, c
                           size_t ws_bytes, void *stream);
 
 /* Linear-logit mode router of the synthetic workloads (not a construct of the
- * paper): logits[r] = sum_c W_r[r, c] * u[c] + b_r[r] for r = h * 3 + m,
- * m in (MEAN, SURR, FULL).  u: fp32 [Din]; W_r: [H * 3, Din] in w_dtype;
- * b_r: fp32 [H * 3]; logits: fp32 [H, 3].  1 <= Din <= 65536. */
+ * paper): logits[r] = sum_c W_r[r, c] * u[c] + b_r[r] for r = h * M + m,
+ * m in (MEAN, SURR, FULL).  u: fp32 [Din]; W_r: [H * M, Din] in w_dtype;
+ * b_r: fp32 [H * M]; logits: fp32 [H, M].  1 <= Din <= 65536.  M is the number
+ * of modes, which Eq.4 fixes at VP_NUM_MODES = 3; any other M returns
+ * VP_ERR_UNSUPPORTED. */
 vp_status vp_router_logits(const float *u, const void *W_r, const float *b_r, int32_t H,
-                           int32_t Din, vp_dtype w_dtype, float *logits, void *stream);
+                           int32_t Din, int32_t M, vp_dtype w_dtype, float *logits,
+                           void *stream);
 
-/* Mode assignment (Eq.4).  THRESHOLD: scores = s_h [H]; FULL if s >= tau_high,
+/* Mode assignment (Eq.4).  `scores` holds M values per head: M = 1 for the
+ * threshold rules (s_h), M = VP_NUM_MODES = 3 for the argmax rules (logits);
+ * any other M for the rule returns VP_ERR_UNSUPPORTED.
+ * THRESHOLD: scores = s_h [H]; FULL if s >= tau_high,
  * MEAN if s <= tau_low, SURR otherwise (0 <= tau_low <= tau_high).  ARGMAX:
  * scores = logits [H, 3]; the first maximal mode.  THRESHOLD_BINARY: FULL if
  * s >= tau_high, else MEAN (tau_low is checked but unused).  ARGMAX_BINARY:
@@ -168,8 +174,9 @@ vp_status vp_router_logits(const float *u, const void *W_r, const float *b_r, in
  *   buckets[3..3+H) head ids grouped by mode (MEAN, then SURR, then FULL),
  *                   ascending within a group;
  *   buckets[3+16]   flags (bit 0: a NaN score was seen). */
-vp_status vp_assign_heads(const float *scores, int32_t H, vp_assign_rule rule, float tau_low,
-                          float tau_high, uint8_t *modes, int32_t *buckets, void *stream);
+vp_status vp_assign_heads(const float *scores, int32_t H, int32_t M, vp_assign_rule rule,
+                          float tau_low, float tau_high, uint8_t *modes, int32_t *buckets,
+                          void *stream);
 
 /* Routed global attention (Algorithm 1 step 2, Eq.5-7): writes Y [N, H, d] in
  * y_dtype, every head in the mode vp_assign_heads gave it.  `modes` [H] and

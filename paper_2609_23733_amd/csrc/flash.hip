@@ -166,42 +166,46 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 }
 
 // ------------------------------------------------------------------------
-// K6 (bf16): FULL-head attention, one workgroup = 4 waves x 64 queries of one
-// FULL head.  Per 64-key tile and wave:  S^T = K Q^T  (keys x queries, 2 x 2
-// blocks of 32x32, 16 MFMAs), softmax weights in registers, O^T += V^T P^T
-// (d x queries, 16 MFMAs).  Each lane owns one query column of every block,
-// so softmax row statistics stay in the lane plus one exchange with lane ^ 32.
-// K rows sit in LDS with index bits 2 and 3 swapped so that the S^T registers
-// hold eight consecutive keys per lane-half: they become the B operand of the
-// PV MFMA without any data movement.
+// K6 (bf16): FULL-head attention.  Per 64-key tile and wave of 64 queries:
+// S^T = K Q^T (keys x queries, 2 x 2 blocks of 32x32, 16 MFMAs), softmax
+// weights in registers, O^T += V^T P^T (d x queries, 16 MFMAs).  Each lane
+// owns one query column of every block, so softmax row statistics stay in
+// the lane plus one exchange with lane ^ 32.  K rows sit in LDS with index
+// bits 2 and 3 swapped so that the S^T registers hold eight consecutive keys
+// per lane-half: they become the B operand of the PV MFMA without any data
+// movement.  Operands are fp16: K as packed by the gather (bf16 values in
+// fp16's range convert exactly), V^T scaled by 2^-e_h, P rounded to nearest
+// (relative error at most 2^-11).
 //
 // Softmax is invariant to the reference point subtracted from the logits
-// before exponentiation.  K6a uses zero: when Cauchy-Schwarz bounds every
-// logit of a workgroup's queries by kFastBound in log2 units
-// (|q . k| c <= |c q| max_j |k_j|), p = 2^x stays within [2^-14, 2^14], fp16's
-// normal range, and a score costs one exp2, half an fp16 pack and one add
-// (row sums).  The scale c = log2(e) / sqrt(d) is folded into Q, rounded to
-// fp16 (relative error 2^-11; K converts exactly), so S comes out of an fp16
-// MFMA in log2 units; P and the scaled V are fp16 too (P rounded to nearest:
-// relative error at most 2^-11).  Work items outside that bound (or outside
-// fp16's safe range for Q and K) are flagged and left to K6b, which keeps
-// bf16 Q and K exact, scales in fp32 and carries a running reference point m:
-// a tile whose logits provably stay below m + kSlack is exponentiated against
-// m directly (p <= 2^8, fp16 again); only otherwise is the tile maximum
-// computed, and m moves (rescaling O and l) only when the tile exceeds
-// m + kSlack.
+// before exponentiation.  A work item (512 queries of one head) runs in one
+// of two modes, chosen from Cauchy-Schwarz bounds (|q . k| <= |q| max_j |k_j|)
+// before its first tile:
+//  - FAST: every logit of the item lies within +-kFastBound in log2 units.
+//    The scale c = log2(e) / sqrt(d) is folded into Q (rounded to fp16,
+//    relative error 2^-11), S comes out of the MFMA in log2 units and the
+//    reference point is 0: p = 2^S lies in [2^-10, 2^10], fp16's normal range,
+//    and a score costs one exp2 and half a pack.
+//  - WIDE: Q keeps its bf16 value (exact in fp16), logits are scaled in fp32
+//    and a running reference point m moves with the logits: a tile whose
+//    logits provably stay below m + kSlack (the tile's largest key norm bounds
+//    them) is exponentiated against m directly; only otherwise is the tile
+//    maximum taken, and m moves (rescaling O and l) only when the tile
+//    exceeds m + kSlack.  A score costs one FMA more than in FAST mode.
+// Row sums: the packed fp16 weights of a lane's 32 keys per tile are added
+// as a tree of packed fp16 adds (at most 32 weights of at most 2^10: no
+// overflow; relative error at most 5 * 2^-11), then into l in fp32.  The
+// numerator uses the same rounded weights.  Teacher instances (which also
+// write each query's log2 sum_k 2^x) run every item in WIDE mode, whose
+// logits are exact, and add the unrounded fp32 weights with a compensated
+// sum instead.  Items whose Q or K values exceed fp16's range are flagged
+// and left to K6b, which keeps bf16 operands.
 // ------------------------------------------------------------------------
 constexpr int kBQ16 = 256;
-constexpr float kSlack = 8.f;        // log2 headroom above a running reference point
-constexpr float kFastBound = 14.f;   // |logit| bound (log2 units) for reference point 0
-constexpr float kF16Safe = 4096.f;   // |c q|, |k| limit for the fp16 logit path
-// Teacher instances (row offsets o_q = log2 sum_k 2^x_qk wanted exactly) add
-// the fp16 residual of c q as a second MFMA operand: per component the
-// logit then errs by at most 2^-22 |c q_i| + 2^-25 (the residual's fp16
-// subnormal spacing), i.e. by 2^-22 * 14 + 2^-25 * 8 max|k| over a work item,
-// which stays below 2^-15.9 when max|k| <= kTeachKmax; items past it go to
-// the exact bf16 kernel.
-constexpr float kTeachKmax = 64.f;
+constexpr float kFastBound = 10.f;   // |logit| bound (log2 units) of FAST mode
+constexpr float kSlack = 10.f;       // WIDE: log2 headroom above the running reference
+constexpr float kF16Safe = 4096.f;   // FAST: |c q|, |k| limit for the fp16 operands
+constexpr float kF16Max = 65504.f;   // WIDE: largest finite fp16
 
 // Kahan step: adds x to the sum s with compensation e (the sum is s - e).
 __device__ __forceinline__ void kahan_add(float& s, float& e, float x) {
@@ -215,6 +219,24 @@ __device__ __forceinline__ float dot2_ones(uint32_t pair, float acc) {
     const f16x2 v = __builtin_bit_cast(f16x2, pair);
     const f16x2 one = {(f16)1.0f, (f16)1.0f};
     return __builtin_amdgcn_fdot2(v, one, acc, false);
+}
+
+// Sum of the 32 packed fp16 weights of one query block (16 registers of two
+// weights) as a tree of packed fp16 adds, added to acc in fp32.
+__device__ __forceinline__ float tree_sum(const f16x8 (&P)[2][2], float acc) {
+    f16x2 t[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        t[2 * i] = f16x2{P[0][0][2 * i], P[0][0][2 * i + 1]} +
+                   f16x2{P[0][1][2 * i], P[0][1][2 * i + 1]};
+        t[2 * i + 1] = f16x2{P[1][0][2 * i], P[1][0][2 * i + 1]} +
+                       f16x2{P[1][1][2 * i], P[1][1][2 * i + 1]};
+    }
+#pragma unroll
+    for (int w = 4; w >= 1; w >>= 1)
+#pragma unroll
+        for (int i = 0; i < w; ++i) t[i] = t[i] + t[i + w];
+    return dot2_ones(__builtin_bit_cast(uint32_t, t[0]), acc);
 }
 
 // Y[q, h, d] = O up / l for the wave's two 32-query blocks (up = 2^e_h, the
@@ -261,17 +283,14 @@ __device__ __forceinline__ void store_offsets(const float (&l)[2], const float (
     }
 }
 
-// K6a: reference point 0, fp16 logits.  One workgroup = 8 waves x 64 queries
-// of one FULL head, two waves per SIMD (waves w and w + 4).  Ping-pong:
-// waves 0-3 (group A) and 4-7 (group B) run the same sequence of phases,
-// matrix(0), vector(0), matrix(1), ..., group B one phase behind, with one
-// workgroup barrier per phase, so that in every phase one wave of each SIMD
-// issues MFMAs while the other issues the softmax's exp2 / pack / sums:
-//   matrix(t): O += V(t-1) P(t-1)  then  S(t) = K(t) (c Q)^T   (32 MFMAs)
-//   vector(t): P(t) = fp16(2^S(t)) (round to nearest, one pack per pair),
-//              l += row sums of the fp32 2^S(t) (the packing error has zero
-//              mean, so l needs no rounded copy: five vector instructions per
-//              pair of scores, the fewest found)
+// K6a: one workgroup = 8 waves x 64 queries of one FULL head, two waves per
+// SIMD (waves w and w + 4).  Ping-pong: waves 0-3 (group A) and 4-7 (group
+// B) run the same sequence of phases, matrix(0), vector(0), matrix(1), ...,
+// group B one phase behind, with one workgroup barrier per phase, so that in
+// every phase one wave of each SIMD issues MFMAs while the other issues the
+// softmax's vector instructions:
+//   matrix(t): O += V(t-1) P(t-1)  then  S(t) = K(t) Q^T   (32 MFMAs)
+//   vector(t): P(t) = fp16 weights of S(t), l += their row sums
 // LDS slot t % 2 holds K(t) and V(t-1).
 //
 // Balanced tail: the work is n_full x q-tiles items of nkt key tiles.  A
@@ -280,16 +299,16 @@ __device__ __forceinline__ void store_offsets(const float (&l)[2], const float (
 // stream the same key tiles of one head through its L2.  The R < G items of
 // the last, partial round are cut into one flat sequence of R nkt item-tile
 // steps, split evenly over the workgroups (at least kMinPartTiles steps
-// each), so the tail takes R / G of a round instead of a whole one.  With
-// reference point 0, results over key ranges simply add: a workgroup that
-// covers only part of an item writes its unnormalized O and l to one of its
-// two partial slots (0 for the first item of its range, 1 for the last), and
-// K6c adds the parts of each split item in workgroup order.  The part
-// holding tile 0 writes wide_items[L] (1 = left to K6b), so flags never
+// each), so the tail takes R / G of a round instead of a whole one.  Results
+// over key ranges combine exactly: a workgroup that covers only part of an
+// item writes its unnormalized O, l and reference point m to one of its two
+// partial slots (0 for the first item of its range, 1 for the last), and K6c
+// combines the parts of each split item in workgroup order.  The part
+// holding tile 0 writes exact_items[L] (1 = left to K6b), so flags never
 // carry over.
 constexpr int kBQf = 512;
 constexpr int kStreamWG = 256;      // grid: one workgroup per CU
-constexpr int kPartFloats = kBQf * kD + kBQf;   // one partial slot: O[512][64], l[512]
+constexpr int kPartFloats = kBQf * kD + 2 * kBQf;   // partial slot: O[512][64], l[512], m[512]
 
 constexpr int kMinPartTiles = 8;    // fewest key tiles per workgroup in the tail
 
@@ -306,6 +325,8 @@ __device__ __forceinline__ int tail_owner(int64_t x, int64_t T, int G) {
     return (int)(((x + 1) * G + T - 1) / T) - 1;
 }
 
+enum { ITEM_FAST = 0, ITEM_WIDE = 1, ITEM_EXACT = 2 };
+
 template <bool kTeach>
 __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ Q,
                                                        const f16* __restrict__ Kh,
@@ -314,7 +335,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                                                        const float* __restrict__ vsc,
                                                        const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt, float c,
-                                                       int32_t* __restrict__ wide_items,
+                                                       int32_t* __restrict__ exact_items,
                                                        float* __restrict__ part, int G,
                                                        void* __restrict__ Y, int ydt,
                                                        float* __restrict__ off) {
@@ -331,12 +352,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 
     __shared__ __attribute__((aligned(16))) f16 sK[2][kBK * kLdsRow];
     __shared__ __attribute__((aligned(16))) f16 sV[2][kD * kLdsRow];
-    __shared__ float sKmax[8];
-    __shared__ int sWide[8];
-    // Teacher instances: each wave's fp16 residual operands of c Q, in lane
-    // order ([wave][qb][ks][lane]), read back in every matrix phase (registers
-    // are full).
-    __shared__ __attribute__((aligned(16))) f16x8 sQlo[kTeach ? 8 * 2 * 4 * 64 : 1];
+    __shared__ float sKmax[8], sQmax[8];
 
     // One segment: key tiles [t0, t1) of item L; written to partial slot
     // pslot of this workgroup if the segment is not the whole item.
@@ -354,9 +370,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
             if (lane == 0) sKmax[wave] = km;
         }
 
-        // (c Q)^T operands of this wave's two 32-query blocks, fp16, kept in
-        // registers, and |c q| per query.
-        f16x8 Qop[2][4];
+        // This wave's two 32-query blocks (bf16) and |q| per query.
+        bf16x8 qraw[2][4];
         int64_t qidx[2];
         float qn[2];
 #pragma unroll
@@ -368,38 +383,48 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
             float n2 = 0.f;
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
-                const bf16x8 raw = load_bf16x8(qp + 16 * ks);
+                qraw[qb][ks] = ok ? load_bf16x8(qp + 16 * ks) : zero_bf16x8();
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const float x = ok ? bf16_to_f32(raw[j]) * c : 0.f;
-                    const f16 hi = (f16)x;
-                    Qop[qb][ks][j] = hi;
-                    if (kTeach)   // x - hi is exact
-                        sQlo[((wave * 2 + qb) * 4 + ks) * 64 + lane][j] = (f16)(x - (float)hi);
+                    const float x = bf16_to_f32(qraw[qb][ks][j]);
                     n2 = fmaf(x, x, n2);
                 }
             }
             n2 += __shfl_xor(n2, 32);
             qn[qb] = sqrtf(n2);
         }
-        __syncthreads();
         {
-            float km = sKmax[0];
-#pragma unroll
-            for (int v = 1; v < 8; ++v) km = fmaxf(km, sKmax[v]);
-            const float qm = fmaxf(qn[0], qn[1]);
-            // Written as "not within" so that a NaN norm also goes to K6b.
-            const bool out = !(qm * km <= kFastBound && qm <= kF16Safe &&
-                               km <= (kTeach ? kTeachKmax : kF16Safe));
-            const bool wave_out = __builtin_amdgcn_ballot_w64(out) != 0;
-            if (lane == 0) sWide[wave] = wave_out;
+            const float qm = wave_max(fmaxf(qn[0], qn[1]));
+            if (lane == 0) sQmax[wave] = qm;
         }
         __syncthreads();
-        int wide = 0;
+        int mode;
+        {
+            float km = sKmax[0], qm = sQmax[0];
 #pragma unroll
-        for (int v = 0; v < 8; ++v) wide |= sWide[v];
-        if (t0 == 0 && threadIdx.x == 0) wide_items[L] = wide;
-        if (wide) return;
+            for (int v = 1; v < 8; ++v) {
+                km = fmaxf(km, sKmax[v]);
+                qm = fmaxf(qm, sQmax[v]);
+            }
+            // Conditions written as "within" so that a NaN norm goes to K6b.
+            const bool fast = !kTeach && qm * c * km <= kFastBound && qm * c <= kF16Safe &&
+                              km <= kF16Safe;
+            const bool wide = qm <= kF16Max && km <= kF16Max;
+            mode = fast ? ITEM_FAST : (wide ? ITEM_WIDE : ITEM_EXACT);
+        }
+        if (t0 == 0 && threadIdx.x == 0) exact_items[L] = mode == ITEM_EXACT;
+        if (mode == ITEM_EXACT) return;   // uniform over the workgroup
+
+        // Q^T operands, kept in registers: fp16 c q (FAST) or fp16 q (WIDE).
+        f16x8 Qop[2][4];
+        const float qs = mode == ITEM_FAST ? c : 1.f;
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    Qop[qb][ks][j] = (f16)(bf16_to_f32(qraw[qb][ks][j]) * qs);
 
         // Tile copies: group A (threads 0-255) copies K tiles, group B V^T
         // tiles, each a contiguous 8 KB block: 64 rows x 4 segments of 16
@@ -426,39 +451,30 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 
         f32x16 O[2][2], S[2][2];
         f16x8 P[2][2][2];
-        float l[2], le[2];   // le: Kahan compensation of l (teacher instances)
+        float l[2], le[2], m[2];   // le: Kahan compensation of l (teacher instances)
+        const float qnc[2] = {qn[0] * c, qn[1] * c};
         const f16x8 zp = {};
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
             O[qb][0] = O[qb][1] = zero_f32x16();
             l[qb] = le[qb] = 0.f;
+            m[qb] = mode == ITEM_FAST ? 0.f : -INFINITY;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) P[qb][kb][0] = P[qb][kb][1] = zp;
         }
 
-        // Matrix phase of tile r: O += V(r-1) P(r-1) from sV[r%2], then S(r)
-        // from sK[r%2].  (PV first: P(r-1) is dead before S(r) is written, so
-        // the two can share registers.  r = 0: P and V slot 0 are zero, so the
-        // PV adds exactly nothing.)
-        auto pv = [&](int sl) {
+        // Matrix phase of tile r: O += V(r-1) P(r-1), then S(r) = K(r) Q^T
+        // from sK[r%2].  The V operands were read into registers at the end of
+        // the wave's previous vector phase, so the 16 PV MFMAs start at once
+        // and hide the latency of the K reads.  (PV first: P(r-1) is dead
+        // before S(r) is written, so the two can share registers.  r = 0: P
+        // and the V operands are zero, so the PV adds exactly nothing.)
+        f16x8 va[2][2][2];
 #pragma unroll
-            for (int db = 0; db < 2; ++db)
+        for (int db = 0; db < 2; ++db)
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int b = 0; b < 2; ++b) {
-                        const f16x8 a = *reinterpret_cast<const f16x8*>(
-                            &sV[sl][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
-                        O[0][db] = mfma_f16(a, P[0][kb][b], O[0][db]);
-                        O[1][db] = mfma_f16(a, P[1][kb][b], O[1][db]);
-                    }
-        };
-        auto mma_phase = [&](int r) {
-            const int sl = r & 1;
-            // All 16 LDS operands of the phase are requested first, so LDS
-            // latency is paid once per phase rather than once per two reads.
-            f16x8 va[2][2][2];
-            f16x8 ka[2][4];
+            for (int kb = 0; kb < 2; ++kb) va[db][kb][0] = va[db][kb][1] = zp;
+        auto prefetch_v = [&](int sl) {   // V operands of the next PV product
 #pragma unroll
             for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -467,12 +483,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     for (int b = 0; b < 2; ++b)
                         va[db][kb][b] = *reinterpret_cast<const f16x8*>(
                             &sV[sl][(db * 32 + n) * kLdsRow + kb * 32 + 16 * b + 8 * hh]);
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks)
-                    ka[kb][ks] = *reinterpret_cast<const f16x8*>(
-                        &sK[sl][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
+        };
+        auto pv = [&] {
 #pragma unroll
             for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -482,6 +494,17 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         O[0][db] = mfma_f16(va[db][kb][b], P[0][kb][b], O[0][db]);
                         O[1][db] = mfma_f16(va[db][kb][b], P[1][kb][b], O[1][db]);
                     }
+        };
+        auto mma_phase = [&](int r) {
+            const int sl = r & 1;
+            f16x8 ka[2][4];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    ka[kb][ks] = *reinterpret_cast<const f16x8*>(
+                        &sK[sl][(kb * 32 + n) * kLdsRow + 16 * ks + 8 * hh]);
+            pv();
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -490,32 +513,15 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     S[0][kb] = mfma_f16(ka[kb][ks], Qop[0][ks], S[0][kb]);
                     S[1][kb] = mfma_f16(ka[kb][ks], Qop[1][ks], S[1][kb]);
                 }
-            if (kTeach) {
-                const f16x8* ql = &sQlo[wave * 2 * 4 * 64 + lane];
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const f16x8 q0 = ql[ks * 64], q1 = ql[(4 + ks) * 64];
-#pragma unroll
-                    for (int kb = 0; kb < 2; ++kb) {
-                        S[0][kb] = mfma_f16(ka[kb][ks], q0, S[0][kb]);
-                        S[1][kb] = mfma_f16(ka[kb][ks], q1, S[1][kb]);
-                    }
-                }
-                // V and K operands, the PV products, the residual operands
-                // (V's registers are free by then), the S products.
-                __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
-            } else {
-                __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
-                __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
-            }
+            // K operands first, then the PV and S products.
+            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
         };
         // Vector phase of tile r: S(r) -> P(r), l += row sums.  The segment's
         // last tile masks keys >= N to weight 0 (a separate instance, so that
         // no other tile pays for the test).
-        auto valu_phase = [&](int r, auto last_tag) {
+        auto valu_phase = [&](int r, auto last_tag, auto mode_tag) {
+            constexpr bool kWide = decltype(mode_tag)::value == ITEM_WIDE;
             if (decltype(last_tag)::value) {
                 const int64_t k0 = (int64_t)(t0 + r) * kBK;
 #pragma unroll
@@ -526,8 +532,32 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         if (key >= N) S[0][kb][i] = S[1][kb][i] = -INFINITY;
                     }
             }
+            const float kbt = kWide ? kmx[t0 + r] : 0.f;
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
+                if (kWide) {
+                    // Keep m unless the bound cannot rule out a logit above
+                    // m + kSlack for some query of this block.
+                    if (__builtin_amdgcn_ballot_w64(qnc[qb] * kbt > m[qb] + kSlack) != 0) {
+                        float mx = -INFINITY;
+#pragma unroll
+                        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][kb][i]);
+                        mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+                        const bool move = mx > m[qb] + kSlack;
+                        const float mn = move ? mx : m[qb];
+                        const float al = move ? exp2f_fast(m[qb] - mn) : 1.f;
+                        m[qb] = mn;
+                        l[qb] *= al;
+                        le[qb] *= al;
+#pragma unroll
+                        for (int db = 0; db < 2; ++db)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
+                    }
+                }
+                const float nm = -m[qb];
                 float ls0 = 0.f, ls1 = 0.f;
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
@@ -537,19 +567,26 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
                             f32x2 e;
-                            e[0] = exp2f_fast(S[qb][kb][8 * b + 2 * j]);
-                            e[1] = exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]);
+                            if (kWide) {
+                                e[0] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j], c, nm));
+                                e[1] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j + 1], c, nm));
+                            } else {
+                                e[0] = exp2f_fast(S[qb][kb][8 * b + 2 * j]);
+                                e[1] = exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]);
+                            }
                             pk[j] = __builtin_bit_cast(uint32_t,
                                                        __builtin_convertvector(e, f16x2));
-                            ls0 += e[0];
-                            ls1 += e[1];
+                            if (kTeach) {
+                                ls0 += e[0];
+                                ls1 += e[1];
+                            }
                         }
                         P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                     }
                 if (kTeach)
                     kahan_add(l[qb], le[qb], ls0 + ls1);
                 else
-                    l[qb] += ls0 + ls1;
+                    l[qb] = tree_sum(P[qb], l[qb]);
             }
         };
         const std::false_type body{};
@@ -563,55 +600,71 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
             __builtin_amdgcn_sched_barrier(0);
         };
 
-        // Prologue: K(t0) into slot 0; V of slot 0 (tile t0 - 1) is zero.
-        if (groupB) {
-            const u32x4 z = {0u, 0u, 0u, 0u};
-            g0 = g1 = z;
-        } else {
-            fetch(0);
-        }
-        stash(0);
-        phase_end();
-
-        // Phases, one workgroup barrier each (2 ns + 1 in both groups):
+        // Phases, one workgroup barrier each (2 ns + 2 in both groups, counting
+        // the prologue's):
         //   group A:  M(0) V(0) M(1) V(1) ... M(ns-1) V(ns-1) -
         //   group B:  -    M(0) V(0) M(1) ... V(ns-2) M(ns-1) V(ns-1)
-        // Group A loads K(r+1) during M(r) and stores it to slot (r+1) % 2
-        // after V(r); group B loads V(r) during V(r-1) and stores it to slot
-        // (r+1) % 2 after M(r).  A slot is rewritten only after both groups'
+        // A wave issues its 32 MFMAs in a few dozen cycles and then waits for
+        // the other wave's vector phase, so the tile copies live in the
+        // matrix phases: a group loads a tile from global memory during its
+        // vector phase and stores it to LDS after issuing the MFMAs of its
+        // next matrix phase.  Group A stores K(r+1) to sK[(r+1) % 2] during
+        // M(r); group B stores V(r+1) to sV[r % 2] during M(r) (V(0) to sV[1]
+        // in the first phase), two phases before group A reads those V
+        // operands at the end of its V(r+1) for M(r+2), and group B at the end
+        // of its own V(r+1).  A slot is rewritten only after both groups'
         // last reads.
-        if (!groupB) {
-            for (int r = 0; r < ns - 1; ++r) {
-                fetch(r + 1);
-                mma_phase(r);
+        auto mma_then = [&](int r, int store_slot) {
+            mma_phase(r);
+            __builtin_amdgcn_sched_barrier(0);
+            if (store_slot >= 0) stash(store_slot);
+        };
+        auto run = [&](auto mode_tag) {
+            if (!groupB) {
+                fetch(0);
+                stash(0);
+                fetch(1);
                 phase_end();
-                valu_phase(r, body);
-                stash((r + 1) & 1);
+                for (int r = 0; r < ns - 1; ++r) {
+                    mma_then(r, (r + 1) & 1);
+                    phase_end();
+                    valu_phase(r, body, mode_tag);
+                    fetch(r + 2);
+                    prefetch_v((r + 1) & 1);
+                    phase_end();
+                }
+                mma_then(ns - 1, -1);
+                phase_end();
+                valu_phase(ns - 1, tail, mode_tag);
+                prefetch_v(ns & 1);
+                phase_end();
+                phase_end();
+            } else {
+                fetch(0);
+                phase_end();
+                stash(1);
+                fetch(1);
+                phase_end();
+                for (int r = 0; r < ns - 1; ++r) {
+                    mma_then(r, r & 1);
+                    phase_end();
+                    valu_phase(r, body, mode_tag);
+                    fetch(r + 2);
+                    prefetch_v((r + 1) & 1);
+                    phase_end();
+                }
+                mma_then(ns - 1, -1);
+                phase_end();
+                valu_phase(ns - 1, tail, mode_tag);
+                prefetch_v(ns & 1);
                 phase_end();
             }
-            mma_phase(ns - 1);
-            phase_end();
-            valu_phase(ns - 1, tail);
-            phase_end();
-            phase_end();
-        } else {
-            fetch(0);
-            phase_end();
-            for (int r = 0; r < ns - 1; ++r) {
-                mma_phase(r);
-                stash((r + 1) & 1);
-                phase_end();
-                fetch(r + 1);
-                valu_phase(r, body);
-                phase_end();
-            }
-            mma_phase(ns - 1);
-            stash(ns & 1);
-            phase_end();
-            valu_phase(ns - 1, tail);
-            phase_end();
-        }
-        pv(ns & 1);   // O += V(ns-1) P(ns-1)
+            pv();   // O += V(ns-1) P(ns-1)
+        };
+        if (kTeach || mode == ITEM_WIDE)
+            run(std::integral_constant<int, ITEM_WIDE>{});
+        else
+            run(std::integral_constant<int, ITEM_FAST>{});
 
         if (kTeach) {
 #pragma unroll
@@ -619,12 +672,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         }
         if (t0 == 0 && t1 == nkt) {
             store_rows(O, l, qidx, N, H, h, hh, vsc[2 * slot + 1], Y, ydt);
-            if (kTeach) {
-                const float zero[2] = {0.f, 0.f};
-                store_offsets(l, zero, qidx, N, h, hh, off);
-            }
+            if (kTeach) store_offsets(l, m, qidx, N, h, hh, off);
         } else {
-            // Partial slot: O[q][d] unnormalized, then l[q], q = row in item.
+            // Partial slot: O[q][d] unnormalized, then l[q], then m[q]
+            // (q = row in item).
             float* ps = part + (int64_t)(w * 2 + pslot) * kPartFloats;
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
@@ -637,7 +688,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                             make_float4(O[qb][db][4 * g], O[qb][db][4 * g + 1],
                                         O[qb][db][4 * g + 2], O[qb][db][4 * g + 3]);
                 const float lt = l[qb] + __shfl_xor(l[qb], 32);
-                if (hh == 0) ps[kBQf * kD + qr] = lt;
+                if (hh == 0) {
+                    ps[kBQf * kD + qr] = lt;
+                    ps[kBQf * kD + kBQf + qr] = m[qb];
+                }
             }
         }
     };
@@ -665,7 +719,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 }
 
 // K6c: Y of the tail items that K6a split over workgroups: the parts' O and
-// l added in workgroup order (fixed, so results are deterministic), then
+// l, each relative to its part's reference point m, scaled to the largest m
+// and added in workgroup order (fixed, so results are deterministic), then
 // O 2^e_h / l.  One workgroup of 256 threads per (tail item, 64-query
 // block): 4 threads per query, 16 consecutive values each, so a query's
 // 256-byte row of a part is read whole.  Items that K6a finished whole or
@@ -673,7 +728,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 constexpr int kCombRows = 64;
 __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict__ buckets,
                                                        int64_t N, int H, int nqt, int nkt,
-                                                       const int32_t* __restrict__ wide_items,
+                                                       const int32_t* __restrict__ exact_items,
                                                        const float* __restrict__ part,
                                                        const float* __restrict__ vsc, int G,
                                                        void* __restrict__ Y, int ydt,
@@ -688,7 +743,7 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
     const int wf = tail_owner((int64_t)i * nkt, T, Gt);
     const int wl = tail_owner((int64_t)(i + 1) * nkt - 1, T, Gt);
     const int L = full + i;
-    if (wf == wl || wide_items[L]) return;
+    if (wf == wl || exact_items[L]) return;
     const int slot = L / nqt, qt = L - slot * nqt;
     const int h = full_head(buckets, H, slot);
     if (h < 0) return;
@@ -700,21 +755,30 @@ __global__ __launch_bounds__(256) void k_flash_combine(const int32_t* __restrict
     const int qr = rb * kCombRows + (threadIdx.x >> 2), d0 = (threadIdx.x & 3) * 16;
     const int64_t qi = (int64_t)qt * kBQf + qr;
     if (qi >= N) return;
+    float mt = -INFINITY;
+    for (int v = wf; v <= wl; ++v) mt = fmaxf(mt, pslot(v)[kBQf * kD + kBQf + qr]);
     float lt = 0.f;
-    for (int v = wf; v <= wl; ++v) lt += pslot(v)[kBQf * kD + qr];
-    if (off && d0 == 0) off[(int64_t)h * N + qi] = __log2f(lt);
-    const float inv = vsc[2 * slot + 1] / lt;
     float acc[16];
 #pragma unroll
     for (int k = 0; k < 16; ++k) acc[k] = 0.f;
     for (int v = wf; v <= wl; ++v) {
-        const float4* src = reinterpret_cast<const float4*>(pslot(v) + qr * kD + d0);
+        const float* ps = pslot(v);
+        // 2^(m_v - max m): exactly 1 for parts at the largest reference point
+        // (every part of a FAST item has m = 0).
+        const float sc = exp2f_fast(ps[kBQf * kD + kBQf + qr] - mt);
+        lt = fmaf(ps[kBQf * kD + qr], sc, lt);
+        const float4* src = reinterpret_cast<const float4*>(ps + qr * kD + d0);
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const float4 a = src[k];
-            acc[4 * k] += a.x; acc[4 * k + 1] += a.y; acc[4 * k + 2] += a.z; acc[4 * k + 3] += a.w;
+            acc[4 * k] = fmaf(a.x, sc, acc[4 * k]);
+            acc[4 * k + 1] = fmaf(a.y, sc, acc[4 * k + 1]);
+            acc[4 * k + 2] = fmaf(a.z, sc, acc[4 * k + 2]);
+            acc[4 * k + 3] = fmaf(a.w, sc, acc[4 * k + 3]);
         }
     }
+    if (off && d0 == 0) off[(int64_t)h * N + qi] = mt + __log2f(lt);
+    const float inv = vsc[2 * slot + 1] / lt;
     const int64_t yo = (qi * H + h) * kD + d0;
     if (ydt == DT_BF16) {
 #pragma unroll

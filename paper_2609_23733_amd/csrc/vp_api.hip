@@ -168,10 +168,11 @@ vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, c
 }
 
 vp_status vp_router_logits(const float* u, const void* W_r, const float* b_r, int32_t H,
-                           int32_t Din, vp_dtype w_dtype, float* logits, void* stream) {
+                           int32_t Din, int32_t M, vp_dtype w_dtype, float* logits,
+                           void* stream) {
     if (!u || !W_r || !b_r || !logits) return VP_ERR_INVALID_ARG;
-    if (H < 1 || Din < 1 || Din > 65536) return VP_ERR_INVALID_ARG;
-    if (H > VP_MAX_HEADS) return VP_ERR_UNSUPPORTED;
+    if (H < 1 || Din < 1 || Din > 65536 || M < 1) return VP_ERR_INVALID_ARG;
+    if (H > VP_MAX_HEADS || M != VP_NUM_MODES) return VP_ERR_UNSUPPORTED;
     if (w_dtype != VP_F32 && w_dtype != VP_BF16) return VP_ERR_INVALID_ARG;
     if (((uintptr_t)u & 3u) || ((uintptr_t)b_r & 3u) || ((uintptr_t)logits & 3u) ||
         ((uintptr_t)W_r & (w_dtype == VP_BF16 ? 1u : 3u)))
@@ -182,14 +183,17 @@ vp_status vp_router_logits(const float* u, const void* W_r, const float* b_r, in
     return hip_status("vp_router_logits");
 }
 
-vp_status vp_assign_heads(const float* scores, int32_t H, vp_assign_rule rule, float tau_low,
-                          float tau_high, uint8_t* modes, int32_t* buckets, void* stream) {
+vp_status vp_assign_heads(const float* scores, int32_t H, int32_t M, vp_assign_rule rule,
+                          float tau_low, float tau_high, uint8_t* modes, int32_t* buckets,
+                          void* stream) {
     if (!scores || !modes || !buckets) return VP_ERR_INVALID_ARG;
-    if (H < 1) return VP_ERR_INVALID_ARG;
+    if (H < 1 || M < 1) return VP_ERR_INVALID_ARG;
     if (H > VP_MAX_HEADS) return VP_ERR_UNSUPPORTED;
     if (rule != VP_ASSIGN_THRESHOLD && rule != VP_ASSIGN_ARGMAX &&
         rule != VP_ASSIGN_THRESHOLD_BINARY && rule != VP_ASSIGN_ARGMAX_BINARY)
         return VP_ERR_INVALID_ARG;
+    const bool by_logits = rule == VP_ASSIGN_ARGMAX || rule == VP_ASSIGN_ARGMAX_BINARY;
+    if (M != (by_logits ? VP_NUM_MODES : 1)) return VP_ERR_UNSUPPORTED;
     if ((rule == VP_ASSIGN_THRESHOLD || rule == VP_ASSIGN_THRESHOLD_BINARY) &&
         (!isfinite(tau_low) || !isfinite(tau_high) || tau_low < 0.f || tau_low > tau_high))
         return VP_ERR_INVALID_ARG;

@@ -91,8 +91,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vp_router_score.argtypes = [ctypes.POINTER(vp_shape), P, P, P,
                                     ctypes.POINTER(vp_router_weights),
                                     ctypes.POINTER(vp_router_state), P, ctypes.c_size_t, P]
-    lib.vp_router_logits.argtypes = [P, P, P, i32, i32, ctypes.c_int, P, P]
-    lib.vp_assign_heads.argtypes = [P, i32, ctypes.c_int, f32, f32, P, P, P]
+    lib.vp_router_logits.argtypes = [P, P, P, i32, i32, i32, ctypes.c_int, P, P]
+    lib.vp_assign_heads.argtypes = [P, i32, i32, ctypes.c_int, f32, f32, P, P, P]
     lib.vp_routed_global_attention.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P,
                                                ctypes.POINTER(vp_router_state),
                                                ctypes.POINTER(vp_surrogate_weights), P,
@@ -259,7 +259,7 @@ def router_logits(u, Wr, br, out: Optional[torch.Tensor] = None) -> torch.Tensor
     if out is None:
         out = torch.empty(H, 3, dtype=torch.float32, device=u.device)
     _need(out, "logits", (H, 3), torch.float32)
-    _check(load_library().vp_router_logits(_ptr(u), _ptr(Wr), _ptr(br), H, Din, _dt(Wr),
+    _check(load_library().vp_router_logits(_ptr(u), _ptr(Wr), _ptr(br), H, Din, 3, _dt(Wr),
                                            _ptr(out), _stream()), "vp_router_logits")
     return out
 
@@ -275,7 +275,8 @@ def assign_heads(scores, rule: int, tau_low: float = TAU_LOW, tau_high: float = 
         buckets = torch.empty(BUCKETS_LEN, dtype=torch.int32, device=scores.device)
     _need(modes, "modes", (H,), torch.uint8)
     _need(buckets, "buckets", (BUCKETS_LEN,), torch.int32)
-    _check(load_library().vp_assign_heads(_ptr(scores), H, int(rule), float(tau_low),
+    M = 3 if rule in (RULE_ARGMAX, RULE_ARGMAX_BINARY) else 1
+    _check(load_library().vp_assign_heads(_ptr(scores), H, M, int(rule), float(tau_low),
                                           float(tau_high), _ptr(modes), _ptr(buckets),
                                           _stream()), "vp_assign_heads")
     return modes, buckets
@@ -402,33 +403,45 @@ class RoutedLayer:
         self.Y = Y if Y is not None else torch.empty(x.N, x.H, HEAD_DIM, dtype=self.y_dtype,
                                                      device=device)
 
-    def step(self, Q=None, K=None, V=None, events=None) -> torch.Tensor:
-        """One pass of the layer; ``events`` = (start, end) torch.cuda.Events
-        recorded around the FULL-head attention kernel on the current stream."""
+    def step(self, Q=None, K=None, V=None, events=None, stages=None) -> torch.Tensor:
+        """One pass of the layer.  ``events`` = (start, end) torch.cuda.Events
+        recorded around the FULL-head attention stage on the current stream;
+        ``stages`` = six events recorded before the router, after the router,
+        after the mode assignment, after the bucket gather, after the FULL
+        heads and after the SURR/MEAN heads."""
         x = self.x
         Q = x.Q if Q is None else Q
         K = x.K if K is None else K
         V = x.V if V is None else V
+        rec = (lambda i: stages[i].record()) if stages is not None else (lambda i: None)
+        rec(0)
         router_score(Q, K, V, x.W, x.U, x.w, self.S, self.P, self.ws, out=self.state,
                      pool=self.pool)
+        rec(1)
         if self.rule in (RULE_ARGMAX, RULE_ARGMAX_BINARY):
             router_logits(x.u, x.Wr, x.br, out=self.logits)
             scores = self.logits
         else:
             scores = self.state.score
         assign_heads(scores, self.rule, self.tau_low, self.tau_high, self.modes, self.buckets)
-        if events is None:
+        rec(2)
+        if events is None and stages is None:
             routed_global_attention(Q, K, V, self.modes, self.buckets, self.state, x.surr,
                                     self.S, self.P, self.ws, self.y_dtype, self.act, self.Y,
                                     self.surr_variant)
         else:
-            # the same three stages, with events bracketing the FULL-head kernel
+            # the same three stages, with events between them
             gather_full_heads(K, V, self.buckets, self.S, self.P, self.ws)
-            events[0].record()
+            rec(3)
+            if events is not None:
+                events[0].record()
             full_head_attention(Q, K, V, self.buckets, self.S, self.P, self.ws, self.Y)
-            events[1].record()
+            if events is not None:
+                events[1].record()
+            rec(4)
             linear_heads(V, self.modes, self.state, x.surr, self.S, self.P, self.Y, self.act,
                          self.surr_variant, Q, K, self.ws)
+            rec(5)
         return self.Y
 
 

@@ -103,34 +103,48 @@ def test_router_score_validation(lib):
 
 def test_router_logits_validation(lib):
     f = lib.vp_router_logits
-    assert f(None, FAKE, FAKE, 16, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, None, FAKE, 16, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, FAKE, FAKE, 0, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, FAKE, FAKE, 17, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_UNSUPPORTED
-    assert f(FAKE, FAKE, FAKE, 16, 0, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, FAKE, FAKE, 16, 1 << 20, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, FAKE, FAKE, 16, 1024, 9, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE + 1, FAKE, FAKE, 16, 1024, vp.VP_BF16, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    B = vp.VP_BF16
+    assert f(None, FAKE, FAKE, 16, 1024, 3, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, None, FAKE, 16, 1024, 3, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 0, 1024, 3, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 17, 1024, 3, B, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, 16, 0, 3, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 16, 1 << 20, 3, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 16, 1024, 3, 9, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE + 1, FAKE, FAKE, 16, 1024, 3, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    # M: the number of modes, which Eq.4 fixes at 3
+    assert f(FAKE, FAKE, FAKE, 16, 1024, 0, B, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, FAKE, 16, 1024, 2, B, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, FAKE, FAKE, 16, 1024, 4, B, FAKE, None) == vp.VP_ERR_UNSUPPORTED
 
 
 def test_assign_validation(lib):
     f = lib.vp_assign_heads
-    assert f(None, 16, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, 0, 0.01, 0.2, None, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, 0, 0.01, 0.2, FAKE, None, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 0, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 17, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_UNSUPPORTED
-    assert f(FAKE, 16, 4, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, -1, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, 0, 0.3, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    T, A = vp.RULE_THRESHOLD, vp.RULE_ARGMAX
+    assert f(None, 16, 1, T, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 1, T, 0.01, 0.2, None, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 1, T, 0.01, 0.2, FAKE, None, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 0, 1, T, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 17, 1, T, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, 16, 1, 4, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 1, -1, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 1, T, 0.3, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
     # the binary threshold rule checks its thresholds like Eq.4 does
-    assert f(FAKE, 16, vp.RULE_THRESHOLD_BINARY, 0.3, 0.2, FAKE, FAKE, None) == \
+    assert f(FAKE, 16, 1, vp.RULE_THRESHOLD_BINARY, 0.3, 0.2, FAKE, FAKE, None) == \
         vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, vp.RULE_THRESHOLD_BINARY, 0.01, float("inf"), FAKE, FAKE, None) == \
+    assert f(FAKE, 16, 1, vp.RULE_THRESHOLD_BINARY, 0.01, float("inf"), FAKE, FAKE, None) == \
         vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, 0, -0.1, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE, 16, 0, float("nan"), 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
-    assert f(FAKE + 2, 16, 0, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 1, T, -0.1, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 1, T, float("nan"), 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE + 2, 16, 1, T, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    # M: one score per head for the threshold rules, three logits for argmax
+    assert f(FAKE, 16, 0, T, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_INVALID_ARG
+    assert f(FAKE, 16, 3, T, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, 16, 3, vp.RULE_THRESHOLD_BINARY, 0.01, 0.2, FAKE, FAKE, None) == \
+        vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, 16, 1, A, 0.01, 0.2, FAKE, FAKE, None) == vp.VP_ERR_UNSUPPORTED
+    assert f(FAKE, 16, 2, vp.RULE_ARGMAX_BINARY, 0.01, 0.2, FAKE, FAKE, None) == \
+        vp.VP_ERR_UNSUPPORTED
 
 
 def sw(L=64, act=0, g_w1=FAKE, variant=vp.SURR_EQ7):

@@ -319,9 +319,58 @@ def test_full_size_sampled(wl, n_full):
     check_y(Yg, ref["Y"], "bf16", True, label="%s/%d" % (wl, n_full))
 
 
+@pytest.mark.parametrize("wl,n_full", [("s32_bf16", 4), ("s32_bf16", 16), ("s100_bf16", 4),
+                                       ("s500_bf16", 6)])
+def test_full_size_sampled_f32_output(wl, n_full):
+    """The benchmark workloads at full size with fp32 Y, so that the
+    comparison is the bf16-operand bar alone: max |err| <= 2e-2 * min(head
+    RMS, layer RMS) with no output rounding term.  At these sizes most FULL
+    work items run whole (one workgroup over all key tiles) and the rest in
+    the split tail; the sampled rows include the last one."""
+    cfg = synth.WORKLOADS[wl]
+    log("full size fp32 Y %s n_full=%d" % (wl, n_full))
+    x = synth.make_layer(cfg["S"], dtype="bf16", n_full=n_full, key=(cfg["S"], 0),
+                         qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.float32)
+    rows = synth.sample_rows(x.N, 128, synth.derive_seed(cfg["S"], 1, 20))
+    ref = oracle_layer(x, rows=rows, full_rows_sel=rows)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    Yg = layer.Y[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    for h in range(16):
+        if ref["modes"][h] == 2:
+            ref["Y"][:, h, :] = ref["Y_full_rows"][h]
+    check_y(Yg, ref["Y"], "bf16", False, label="%s/%d fp32 Y" % (wl, n_full))
+
+
+@pytest.mark.parametrize("S,y_bf16", [(32, False), (100, True)])
+def test_full_size_sharp(S, y_bf16):
+    """Full-size layers whose FULL heads attend sharply (Q, K ~ N(0, 1): logit
+    spread of several log2 units, as heads routed FULL by Eq.4 have), so every
+    work item's Cauchy-Schwarz bound exceeds the zero-reference window and
+    the running-reference-point path carries the whole FULL stage."""
+    log("full size sharp S=%d y=%s" % (S, "bf16" if y_bf16 else "f32"))
+    x = synth.make_layer(S, dtype="bf16", n_full=4, key=(S, 3), sharp=True, qkv_device="cuda")
+    full = [h for h in range(16) if x.modes[h] == 2]
+    qn = torch.linalg.vector_norm(x.Q[:, full].float(), dim=2) * C_LOG2      # [N, 4]
+    kn = torch.linalg.vector_norm(x.K[:, full].float(), dim=2).amax(dim=0)   # [4]
+    nq = -(-x.N // 512)
+    qmax = torch.stack([qn[t * 512:(t + 1) * 512].amax(dim=0) for t in range(nq)])
+    assert (qmax * kn > FAST_BOUND).all()
+    layer = run_gpu(x, y_dtype=torch.bfloat16 if y_bf16 else torch.float32)
+    rows = synth.sample_rows(x.N, 128, synth.derive_seed(S, 3, 20))
+    ref = oracle_layer(x, rows=rows, full_rows_sel=rows)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    Yg = layer.Y[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    for h in full:
+        ref["Y"][:, h, :] = ref["Y_full_rows"][h]
+    check_y(Yg, ref["Y"], "bf16", y_bf16, label="sharp S=%d" % S)
+
+
 # ------------------------------------ softmax reference point (FULL, bf16)
 
 C_LOG2 = 1.4426950408889634 / 8.0
+# |logit| window (log2 units) of the zero-reference-point FULL path
+FAST_BOUND = 14.0
 
 
 def tile_bounds(x, bq=256):
