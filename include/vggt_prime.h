@@ -150,6 +150,21 @@ vp_status vp_router_score(const vp_shape *shape, const void *Q, const void *K, c
                           const vp_router_weights *rw, vp_router_state *out, void *ws,
                           size_t ws_bytes, void *stream);
 
+/* vp_router_score for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same kernels and results, with the router's partial sums kept in a
+ * static device array of the library (4.5 MiB, one per device, held until
+ * the process ends) instead of a caller workspace.  It calls no allocating
+ * routine.  Every shape the library accepts fits; a shape needing more than
+ * the array returns VP_ERR_WORKSPACE (message in vp_last_error).  All calls
+ * on one device share that device's array: calls that overlap on one device
+ * (different streams, or host threads) race and must be serialised by the
+ * caller.  The array's address is looked up once per device, on the first
+ * call made with that device current. */
+vp_status vp_router_score_noalloc(const vp_shape *shape, const void *Q, const void *K,
+                                  const void *V, const vp_router_weights *rw,
+                                  vp_router_state *out, void *stream);
+
 /* Linear-logit mode router of the synthetic workloads (not a construct of the
  * paper): logits[r] = sum_c W_r[r, c] * u[c] + b_r[r] for r = h * M + m,
  * m in (MEAN, SURR, FULL).  u: fp32 [Din]; W_r: [H * M, Din] in w_dtype;

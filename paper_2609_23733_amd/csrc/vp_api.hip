@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/vggt_prime.h"
 #include "vp_internal.hpp"
 
@@ -127,9 +129,13 @@ size_t vp_workspace_bytes(const vp_shape* shape) {
     return make_layout(shape, &L) ? L.total : 0;
 }
 
-vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, const void* V,
-                          const vp_router_weights* rw, vp_router_state* out, void* ws,
-                          size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Host-side checks of vp_router_score's arguments other than the workspace.
+vp_status check_router(const vp_shape* shape, const void* Q, const void* K, const void* V,
+                       const vp_router_weights* rw, const vp_router_state* out) {
     vp_status st = shape_status(shape);
     if (st != VP_OK) return st;
     if (!Q || !K || !V || !rw || !out) return VP_ERR_INVALID_ARG;
@@ -145,9 +151,13 @@ vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, c
         return VP_ERR_INVALID_ARG;
     if (!aligned16(out->q_pool) || !aligned16(out->ctx) || !aligned16(out->vmean))
         return VP_ERR_INVALID_ARG;
-    Layout L;
-    if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+    return VP_OK;
+}
 
+// Enqueues the router with its partial sums at ws + L.off_part1 / L.off_part2.
+vp_status launch_router_at(const vp_shape* shape, const Layout& L, const void* Q, const void* K,
+                           const void* V, const vp_router_weights* rw, vp_router_state* out,
+                           void* ws, void* stream, const char* where) {
     (void)hipGetLastError();
     vp::RouterArgs a;
     a.dtype = shape->dtype == VP_BF16 ? 1 : 0;
@@ -164,7 +174,87 @@ vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, c
     a.q_pool = out->q_pool; a.stats = out->stats; a.score = out->score;
     a.ctx = out->ctx; a.vmean = out->vmean;
     vp::launch_router(a, (hipStream_t)stream);
-    return hip_status("vp_router_score");
+    return hip_status(where);
+}
+
+// Bytes of the workspace that the router uses (its partial sums, from offset 0).
+size_t router_scratch_bytes(const vp_shape* shape, const Layout& L) {
+    return align_up(L.off_part2 + (size_t)L.n2 * shape->H * (2 + 2 * VP_HEAD_DIM) * sizeof(float));
+}
+
+// Scratch of vp_router_score_noalloc: the router's partial sums (at most 64
+// pooling chunks and 512 routing chunks of 16 heads, 4.32 MiB, for every
+// shape the library accepts).  Each device holds its own copy for the life
+// of the process; host code uses it only through the address that
+// hipGetSymbolAddress returns on that device.
+constexpr size_t kNoAllocScratchBytes = (size_t)9 << 19;   // 4.5 MiB
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device, looked up on the first
+// call made with that device current.
+vp_status scratch_address(void** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        snprintf(g_err, sizeof(g_err), "vp_router_score_noalloc: hipGetDevice: %s",
+                 hipGetErrorString(e));
+        return VP_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        snprintf(g_err, sizeof(g_err), "vp_router_score_noalloc: device %d beyond %d", dev,
+                 kMaxDevices);
+        return VP_ERR_UNSUPPORTED;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            snprintf(g_err, sizeof(g_err), "vp_router_score_noalloc: hipGetSymbolAddress: %s",
+                     hipGetErrorString(e));
+            return VP_ERR_HIP;
+        }
+        g_scratch[dev] = p;
+    }
+    *ptr = g_scratch[dev];
+    return VP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vp_status vp_router_score(const vp_shape* shape, const void* Q, const void* K, const void* V,
+                          const vp_router_weights* rw, vp_router_state* out, void* ws,
+                          size_t ws_bytes, void* stream) {
+    vp_status st = check_router(shape, Q, K, V, rw, out);
+    if (st != VP_OK) return st;
+    Layout L;
+    if ((st = check_ws(shape, ws, ws_bytes, &L)) != VP_OK) return st;
+    return launch_router_at(shape, L, Q, K, V, rw, out, ws, stream, "vp_router_score");
+}
+
+vp_status vp_router_score_noalloc(const vp_shape* shape, const void* Q, const void* K,
+                                  const void* V, const vp_router_weights* rw,
+                                  vp_router_state* out, void* stream) {
+    vp_status st = check_router(shape, Q, K, V, rw, out);
+    if (st != VP_OK) return st;
+    Layout L;
+    if (!make_layout(shape, &L)) return VP_ERR_INVALID_ARG;
+    const size_t need = router_scratch_bytes(shape, L);
+    if (need > kNoAllocScratchBytes) {
+        snprintf(g_err, sizeof(g_err),
+                 "vp_router_score_noalloc: %zu bytes of scratch needed, %zu available", need,
+                 kNoAllocScratchBytes);
+        return VP_ERR_WORKSPACE;
+    }
+    void* ws = nullptr;
+    if ((st = scratch_address(&ws)) != VP_OK) return st;
+    return launch_router_at(shape, L, Q, K, V, rw, out, ws, stream, "vp_router_score_noalloc");
 }
 
 vp_status vp_router_logits(const float* u, const void* W_r, const float* b_r, int32_t H,

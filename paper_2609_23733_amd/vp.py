@@ -28,7 +28,8 @@ MAX_HEADS, HEAD_DIM, HIDDEN = 16, 64, 64
 BUCKETS_LEN = 3 + MAX_HEADS + 1
 TAU_LOW, TAU_HIGH = 0.01, 0.20
 
-EXPORTS = ("vp_workspace_bytes", "vp_router_score", "vp_router_logits", "vp_assign_heads",
+EXPORTS = ("vp_workspace_bytes", "vp_router_score", "vp_router_score_noalloc",
+           "vp_router_logits", "vp_assign_heads",
            "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
            "vp_linear_heads", "vp_status_string", "vp_last_error", "vp_block_workspace_bytes",
            "vp_block_qkv", "vp_block_out", "vp_teacher_workspace_bytes", "vp_loss_workspace_bytes",
@@ -91,6 +92,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vp_router_score.argtypes = [ctypes.POINTER(vp_shape), P, P, P,
                                     ctypes.POINTER(vp_router_weights),
                                     ctypes.POINTER(vp_router_state), P, ctypes.c_size_t, P]
+    lib.vp_router_score_noalloc.argtypes = [ctypes.POINTER(vp_shape), P, P, P,
+                                            ctypes.POINTER(vp_router_weights),
+                                            ctypes.POINTER(vp_router_state), P]
     lib.vp_router_logits.argtypes = [P, P, P, i32, i32, i32, ctypes.c_int, P, P]
     lib.vp_assign_heads.argtypes = [P, i32, i32, ctypes.c_int, f32, f32, P, P, P]
     lib.vp_routed_global_attention.argtypes = [ctypes.POINTER(vp_shape), P, P, P, P, P,
@@ -132,7 +136,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     for f in ("vp_tome_split", "vp_tome_plan", "vp_tome_merge", "vp_tome_merge_qkv",
               "vp_tome_unmerge"):
         getattr(lib, f).restype = ctypes.c_int
-    for f in ("vp_router_score", "vp_router_logits", "vp_assign_heads",
+    for f in ("vp_router_score", "vp_router_score_noalloc", "vp_router_logits", "vp_assign_heads",
               "vp_routed_global_attention", "vp_gather_full_heads", "vp_full_head_attention",
               "vp_linear_heads", "vp_block_qkv", "vp_block_out", "vp_teacher_targets",
               "vp_router_loss", "vp_latent_loss"):
@@ -246,6 +250,31 @@ def router_score(Q, K, V, W, U, w, S: int, P: int, ws: torch.Tensor, scale: floa
                                           ctypes.byref(rw), ctypes.byref(st), _ptr(ws),
                                           ws.numel() * ws.element_size(), _stream()),
            "vp_router_score")
+    return out
+
+
+def router_score_noalloc(Q, K, V, W, U, w, S: int, P: int, scale: float = 0.0,
+                         out: Optional[RouterState] = None,
+                         pool: int = POOL_GATED) -> RouterState:
+    """router_score without a workspace: the library keeps the partial sums in
+    its own static device array (see vp_router_score_noalloc)."""
+    N, H = S * P, Q.shape[1]
+    for t, nm in ((Q, "Q"), (K, "K"), (V, "V")):
+        _need(t, nm, (N, H, HEAD_DIM), Q.dtype)
+    if pool == POOL_GATED:
+        _need(W, "W", (H, HIDDEN, HEAD_DIM), Q.dtype)
+        _need(U, "U", (H, HIDDEN, HEAD_DIM), Q.dtype)
+        _need(w, "w", (H, HIDDEN), Q.dtype)
+    if out is None:
+        out = RouterState.empty(H, Q.device)
+    ptr = lambda t: None if t is None else t.data_ptr()
+    rw = vp_router_weights(ptr(W), ptr(U), ptr(w), HIDDEN, float(scale), int(pool))
+    shp = make_shape(S, P, H, Q.dtype)
+    st = out.c()
+    _check(load_library().vp_router_score_noalloc(ctypes.byref(shp), _ptr(Q), _ptr(K), _ptr(V),
+                                                  ctypes.byref(rw), ctypes.byref(st),
+                                                  _stream()),
+           "vp_router_score_noalloc")
     return out
 
 

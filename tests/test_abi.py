@@ -101,6 +101,26 @@ def test_router_score_validation(lib):
         vp.VP_ERR_INVALID_ARG
 
 
+def test_router_score_noalloc_validation(lib):
+    """The allocation-free router rejects the same arguments as vp_router_score
+    on the host, before it looks up its scratch or enqueues anything."""
+    f = lambda shp=None, Q=FAKE, w=None, st=None: lib.vp_router_score_noalloc(
+        ctypes.byref(shp or shape()), Q, FAKE, FAKE, ctypes.byref(w or rw()),
+        ctypes.byref(st or rs()), None)
+    assert f(shp=shape(S=0)) == vp.VP_ERR_INVALID_ARG
+    assert f(shp=shape(H=17)) == vp.VP_ERR_UNSUPPORTED
+    assert f(shp=shape(d=128)) == vp.VP_ERR_UNSUPPORTED
+    assert f(shp=shape(S=1 << 20, P=1 << 10)) == vp.VP_ERR_UNSUPPORTED
+    assert f(Q=None) == vp.VP_ERR_INVALID_ARG
+    assert f(Q=FAKE_ODD) == vp.VP_ERR_INVALID_ARG
+    assert f(w=rw(W=None)) == vp.VP_ERR_INVALID_ARG
+    assert f(w=rw(L=32)) == vp.VP_ERR_UNSUPPORTED
+    assert f(w=rw(pool=2)) == vp.VP_ERR_INVALID_ARG
+    assert f(st=rs(q=None)) == vp.VP_ERR_INVALID_ARG
+    assert lib.vp_router_score_noalloc(None, FAKE, FAKE, FAKE, None, None, None) == \
+        vp.VP_ERR_INVALID_ARG
+
+
 def test_router_logits_validation(lib):
     f = lib.vp_router_logits
     B = vp.VP_BF16

@@ -1,0 +1,53 @@
+"""The allocation-free router (vp_router_score_noalloc) against the router
+with a caller workspace (vp_router_score): the same kernels on the same
+inputs, so every output must be bitwise equal.  Two calls in a row, the
+second on a smaller input, then the first shape again (the static scratch
+keeps the last call's contents, which must not leak into a result)."""
+import sys
+
+import pytest
+import torch
+
+from paper_2609_23733_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    sys.stdout.write("[gpu-case] %s\n" % msg)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_23733_amd import vp
+    vp.load_library()
+
+
+def _compare(S, P, dtype, key, pool):
+    from paper_2609_23733_amd import vp
+    log("noalloc router S=%d P=%d %s pool=%d" % (S, P, dtype, pool))
+    x = synth.make_layer(S, P, dtype=dtype, key=key, sharp=True, qkv_device="cuda").to("cuda")
+    ws = vp.alloc_workspace(S, P, x.H, x.Q.dtype)
+    ref = vp.router_score(x.Q, x.K, x.V, x.W, x.U, x.w, S, P, ws, pool=pool)
+    got = vp.router_score_noalloc(x.Q, x.K, x.V, x.W, x.U, x.w, S, P, pool=pool)
+    torch.cuda.synchronize()
+    for name in ("q_pool", "stats", "score", "ctx", "vmean"):
+        a, b = getattr(ref, name), getattr(got, name)
+        assert torch.isfinite(a).all(), name
+        assert torch.equal(a, b), (name, (a - b).abs().max().item())
+
+
+def test_noalloc_router_matches_workspace_router():
+    _compare(8, 1374, "bf16", (70, 0), 0)    # N = 10,992: many routing chunks
+    _compare(2, 300, "bf16", (70, 1), 0)     # smaller input on the same scratch
+    _compare(3, 777, "f32", (70, 2), 0)      # fp32 operands
+    _compare(2, 300, "bf16", (70, 1), 1)     # mean-query pooling
+    _compare(8, 1374, "bf16", (70, 0), 0)    # the first shape again
+
+
+def test_noalloc_router_full_size():
+    """S = 100 (N = 137,400): the largest chunk counts the scratch must hold."""
+    _compare(100, 1374, "bf16", (70, 3), 0)
