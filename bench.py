@@ -35,9 +35,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "a3c727755cee073de6e653881026f3c6dd082ae212b386c1c1da0d3a5fcfe43e",
+    "source_sha256": "82462dd9186039acf974f77fb447de5c2580225f0c1a76895fa6509c2b207cac",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1531037, "write_kib": 104949,
+    "fetch_kib": 1534694, "write_kib": 109645,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 
@@ -517,6 +517,8 @@ def main():
                     help="skip the 24-layer routed stack at S=500")
     ap.add_argument("--stack", type=int, default=0, metavar="S",
                     help="also time a 24-block stack at S views (e.g. 500)")
+    ap.add_argument("--workload", default=None, metavar="S,NFULL[,sharp|f32]",
+                    help="time only this workload and print its record (for profiling runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the "
                          "reference for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -538,6 +540,14 @@ def main():
         return
     from paper_2609_23733_amd import vp
     vp.load_library()
+    if args.workload:
+        f = args.workload.split(",")
+        S, nf = int(f[0]), int(f[1])
+        sharp, dt = "sharp" in f[2:], ("f32" if "f32" in f[2:] else "bf16")
+        rec, _, _ = run_workload(S, nf, args.steps, args.warmup, (S, 3 if sharp else 0),
+                                 dtype=dt, sharp=sharp)
+        print(json.dumps(rec))
+        return
 
     head, layer, x = run_workload(100, args.n_full, args.steps, args.warmup, (100, 0))
     by = [head]
