@@ -191,37 +191,52 @@ __global__ __launch_bounds__(256, 4) void k_surrogate_bf16(
 }
 
 // ------------------------------------------------------------------------
-// K7 (fp32): one token per thread, weights in LDS, plain FMAs in fp32.
+// K7 (fp32): the same two-layer MLP on fp32 32x32x2 MFMAs; a wave takes 32
+// tokens (lane l: token l % 32, half hh = l / 32), a workgroup 128.
+//   layer 1: H1^T = W1_v V^T + (W1_C C_h + b1)   (128 hidden x 32 tokens,
+//            4 blocks x 32 steps); step s reduces over value features s
+//            (lanes hh = 0) and 32 + s (hh = 1), so a lane holds one
+//            contiguous half of its token's value row;
+//   layer 2: G^T = W2_gamma act(H1_gamma)^T, D^T = W2_delta act(H1_delta)^T
+//            (64 x 32 each); step s of hidden block ub reduces over the two
+//            hidden units that layer 1's output register s holds in the two
+//            lane halves (8 (s / 4) + 4 hh + s % 4), so those registers are
+//            the B operand as they are.
+// W1's value half sits in LDS row-major with stride 65 floats, W2 transposed
+// ([hidden][d]) with stride 72: both MFMA A-operand reads are bank-conflict
+// free.
 // ------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_surrogate_f32(
+constexpr int kSurr32Rows = 128;   // tokens per workgroup (4 waves x 32)
+constexpr int kW1s = 65, kW2s = 72;
+
+template <int ACT>
+__global__ __launch_bounds__(256, 2) void k_surrogate_f32(
     const float* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
     const float* __restrict__ gw1, const float* __restrict__ gb1, const float* __restrict__ gw2,
     const float* __restrict__ gb2, const float* __restrict__ dw1, const float* __restrict__ db1,
-    const float* __restrict__ dw2, const float* __restrict__ db2, int act, int add_v, int64_t N,
-    int H, void* __restrict__ Y, int ydt) {
+    const float* __restrict__ dw2, const float* __restrict__ db2, int add_v, int64_t N, int H,
+    void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
-    const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
-    const int64_t t1 = (t0 + kSurrRows < N) ? t0 + kSurrRows : N;
-    const int tid = threadIdx.x;
-    __shared__ float sW1v[2][kL][kD + 1];   // value half of layer 1, [gamma|delta][u][c]
-    __shared__ float sW2t[2][kL][kD];       // layer 2 transposed: [which][u][d]
-    __shared__ float sC1[2][kL], sC[kD], sB2[2][kD];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, n = lane & 31, hh = lane >> 5;
+    __shared__ float sW1[2 * kL * kW1s];        // [gamma units | delta units][value feature]
+    __shared__ float sW2t[2][kL * kW2s];        // [which][hidden][d]
+    __shared__ float sC1[2 * kL], sC[kD], sB2[2][kD];
     const float* C = ctx + h * kD;
     for (int i = tid; i < 2 * kL * kD; i += 256) {
-        const int which = i / (kL * kD), u = (i / kD) % kL, cc = i % kD;
-        const float* w1 = (which == 0 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD;
-        sW1v[which][u][cc] = w1[cc];
+        const int u = i / kD, c = i % kD;        // unit u of [gamma | delta], feature c
+        const float* w1 = (u < kL ? gw1 : dw1) + ((int64_t)h * kL + (u & (kL - 1))) * 2 * kD;
+        sW1[u * kW1s + c] = w1[c];
+        const int which = u / kL, uu = u % kL;   // here (uu, c) = (d, hidden) of W2
         const float* w2 = (which == 0 ? gw2 : dw2) + (int64_t)h * kD * kL;
-        // sW2t[which][u][d] = W2[d][u]; here (u, cc) runs over (hidden, d)
-        sW2t[which][u][cc] = w2[(int64_t)cc * kL + u];
+        sW2t[which][c * kW2s + uu] = w2[uu * kL + c];
     }
-    if (tid < 128) {
-        const int which = tid >> 6, u = tid & 63;
+    if (tid < 2 * kL) {
+        const int which = tid / kL, u = tid % kL;
         const float* w1 = (which == 0 ? gw1 : dw1) + ((int64_t)h * kL + u) * 2 * kD;
         float acc = (which == 0 ? gb1 : db1)[h * kL + u];
-        for (int cc = 0; cc < kD; ++cc) acc = fmaf(w1[kD + cc], C[cc], acc);
-        sC1[which][u] = acc;
+        for (int c = 0; c < kD; ++c) acc = fmaf(w1[kD + c], C[c], acc);
+        sC1[tid] = acc;
     }
     if (tid < kD) {
         sC[tid] = C[tid];
@@ -229,39 +244,79 @@ __global__ __launch_bounds__(256) void k_surrogate_f32(
         sB2[1][tid] = db2[h * kD + tid];
     }
     __syncthreads();
-    for (int64_t tok = t0 + tid; tok < t1; tok += 256) {
-        float v[kD], og[kD], od[kD];
-        const float* vr = V + (tok * H + h) * kD;
+
+    const int64_t tok = (int64_t)blockIdx.x * kSurr32Rows + wave * 32 + n;
+    const bool ok = tok < N;
+    float v[32];
+    {
+        const float4* vr = reinterpret_cast<const float4*>(V + ((ok ? tok : 0) * H + h) * kD + 32 * hh);
 #pragma unroll
-        for (int k = 0; k < kD; ++k) {
-            v[k] = vr[k];
-            og[k] = sB2[0][k];
-            od[k] = sB2[1][k];
-        }
-        for (int u = 0; u < kL; ++u) {
-            float ag = sC1[0][u], ad = sC1[1][u];
-#pragma unroll
-            for (int k = 0; k < kD; ++k) {
-                ag = fmaf(sW1v[0][u][k], v[k], ag);
-                ad = fmaf(sW1v[1][u][k], v[k], ad);
-            }
-            const float hg = act_fn(ag, act), hd = act_fn(ad, act);
-#pragma unroll
-            for (int k = 0; k < kD; ++k) {
-                og[k] = fmaf(sW2t[0][u][k], hg, og[k]);
-                od[k] = fmaf(sW2t[1][u][k], hd, od[k]);
-            }
-        }
-        const int64_t off = (tok * H + h) * kD;
-#pragma unroll
-        for (int k = 0; k < kD; ++k) {
-            const float y = sC[k] + sigmoid_fast(og[k]) * od[k] + (add_v ? v[k] : 0.f);
-            if (ydt == DT_BF16)
-                reinterpret_cast<bf16*>(Y)[off + k] = (bf16)y;
-            else
-                reinterpret_cast<float*>(Y)[off + k] = y;
+        for (int q = 0; q < 8; ++q) {
+            const float4 x = ok ? vr[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+            v[4 * q] = x.x; v[4 * q + 1] = x.y; v[4 * q + 2] = x.z; v[4 * q + 3] = x.w;
         }
     }
+    // Layer 1: block ub holds hidden units 32 ub + 8 (r / 4) + 4 hh + r % 4 in
+    // register r; the accumulators start at the per-head constant W1_C C_h + b1.
+    f32x16 acc[4];
+#pragma unroll
+    for (int ub = 0; ub < 4; ++ub)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[ub][r] = sC1[32 * ub + 8 * (r >> 2) + 4 * hh + (r & 3)];
+#pragma unroll
+    for (int st = 0; st < 32; ++st)
+#pragma unroll
+        for (int ub = 0; ub < 4; ++ub)
+            acc[ub] = mfma_f32(sW1[(32 * ub + n) * kW1s + 32 * hh + st], v[st], acc[ub]);
+#pragma unroll
+    for (int ub = 0; ub < 4; ++ub)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            acc[ub][r] = ACT == 1 ? fmaxf(acc[ub][r], 0.f) : gelu_erf(acc[ub][r]);
+    // Layer 2: output block db holds d = 32 db + 8 (r / 4) + 4 hh + r % 4.
+    f32x16 og[2], od[2];
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int d = 32 * db + 8 * (r >> 2) + 4 * hh + (r & 3);
+            og[db][r] = sB2[0][d];
+            od[db][r] = sB2[1][d];
+        }
+#pragma unroll
+    for (int ub = 0; ub < 2; ++ub)
+#pragma unroll
+        for (int st = 0; st < 16; ++st) {
+            const int u = 32 * ub + 8 * (st >> 2) + 4 * hh + (st & 3);
+#pragma unroll
+            for (int db = 0; db < 2; ++db) {
+                og[db] = mfma_f32(sW2t[0][u * kW2s + 32 * db + n], acc[ub][st], og[db]);
+                od[db] = mfma_f32(sW2t[1][u * kW2s + 32 * db + n], acc[2 + ub][st], od[db]);
+            }
+        }
+    if (!ok) return;
+    const int64_t row = (tok * H + h) * kD;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int d0 = 32 * db + 8 * q + 4 * hh;
+            float y[4];
+            float4 vv = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (add_v) vv = *reinterpret_cast<const float4*>(V + row + d0);
+            const float va[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                y[j] = sC[d0 + j] + sigmoid_fast(og[db][4 * q + j]) * od[db][4 * q + j] + va[j];
+            if (ydt == DT_BF16) {
+                bf16x4 o;
+                o[0] = (bf16)y[0]; o[1] = (bf16)y[1]; o[2] = (bf16)y[2]; o[3] = (bf16)y[3];
+                *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(Y) + row + d0) = o;
+            } else {
+                *reinterpret_cast<float4*>(reinterpret_cast<float*>(Y) + row + d0) =
+                    make_float4(y[0], y[1], y[2], y[3]);
+            }
+        }
 }
 
 // ------------------------------------------------------------------------
@@ -549,11 +604,14 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
                                (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2, add_v,
                                a.N, a.H, a.Y, a.ydt);
         }
-        else
-            hipLaunchKernelGGL(k_surrogate_f32, dim3(nbs, a.H), dim3(256), 0, st,
-                               (const float*)a.V, a.modes, C, (const float*)a.g_w1, a.g_b1,
-                               (const float*)a.g_w2, a.g_b2, (const float*)a.d_w1, a.d_b1,
-                               (const float*)a.d_w2, a.d_b2, a.act, add_v, a.N, a.H, a.Y, a.ydt);
+        else {
+            const unsigned nb32 = (unsigned)((a.N + kSurr32Rows - 1) / kSurr32Rows);
+            auto* kern = a.act == 1 ? k_surrogate_f32<1> : k_surrogate_f32<0>;
+            hipLaunchKernelGGL(kern, dim3(nb32, a.H), dim3(256), 0, st, (const float*)a.V,
+                               a.modes, C, (const float*)a.g_w1, a.g_b1, (const float*)a.g_w2,
+                               a.g_b2, (const float*)a.d_w1, a.d_b1, (const float*)a.d_w2,
+                               a.d_b2, add_v, a.N, a.H, a.Y, a.ydt);
+        }
     } else if (v == SURR_NO_RESIDUAL) {
         const unsigned nb = (unsigned)((a.N + kMeanRows - 1) / kMeanRows);
         hipLaunchKernelGGL(k_broadcast_heads, dim3(nb, a.H), dim3(256), 0, st, a.modes,

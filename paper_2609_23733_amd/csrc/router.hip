@@ -175,7 +175,13 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
     }
 }
 
-// fp32: one token per thread, weights in LDS, plain FMAs.
+// fp32: the same structure on fp32 32x32x2 MFMAs.  Step s of a 32-token block
+// reduces over query features s (lanes hh = 0) and 32 + s (hh = 1), so a lane
+// holds one contiguous half of its token's query row (the B operand, and the
+// values the pooled sum weights); W and U sit in LDS row-major with stride 65
+// floats (the A-operand reads are bank-conflict free).
+constexpr int kPoolS = 65;
+
 __global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restrict__ Q,
                                                           const float* __restrict__ W,
                                                           const float* __restrict__ U,
@@ -186,76 +192,106 @@ __global__ __launch_bounds__(256) void k_pool_partial_f32(const float* __restric
     const int h = blockIdx.y, c = blockIdx.x;
     const int64_t t0 = (int64_t)c * chunk;
     const int64_t t1 = (t0 + chunk < N) ? t0 + chunk : N;
-    __shared__ float sW[kL * kD], sU[kL * kD], sw[kL];
-    __shared__ float s_red[4][2 + kD];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int n = lane & 31, hh = lane >> 5;
+
+    // W_h rows then U_h rows (stride 65) and w_h for the token loop; the same
+    // memory holds the wave partials afterwards.
+    __shared__ float smem[4 * 64 * 33];
+    __shared__ float sw[kL], s_ml[4][2];
+    float* sWU = smem;
     if (!mean_pool) {
-        for (int i = threadIdx.x; i < kL * kD; i += 256) {
-            sW[i] = W[(int64_t)h * kL * kD + i];
-            sU[i] = U[(int64_t)h * kL * kD + i];
+        const float* Wh = W + (int64_t)h * kL * kD;
+        const float* Uh = U + (int64_t)h * kL * kD;
+        for (int i = threadIdx.x; i < 2 * kL * kD; i += 256) {
+            const int row = i / kD, col = i % kD;
+            sWU[row * kPoolS + col] = (row < kL ? Wh : Uh)[(row & (kL - 1)) * kD + col];
         }
         if (threadIdx.x < kL) sw[threadIdx.x] = w[(int64_t)h * kL + threadIdx.x];
     }
     __syncthreads();
 
     float m = -INFINITY, l = 0.f;
-    float acc[kD];
+    float acc[32];
 #pragma unroll
-    for (int k = 0; k < kD; ++k) acc[k] = 0.f;
-    for (int64_t tok = t0 + threadIdx.x; tok < t1; tok += 256) {
-        float q[kD];
-        const float4* qr = reinterpret_cast<const float4*>(Q + (tok * H + h) * kD);
+    for (int i = 0; i < 32; ++i) acc[i] = 0.f;
+    for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
+        const int64_t tok = tb + n;
+        const bool valid = tok < t1;
+        float q[32];
+        {
+            const float4* qr =
+                reinterpret_cast<const float4*>(Q + ((valid ? tok : t0) * H + h) * kD + 32 * hh);
 #pragma unroll
-        for (int k = 0; k < kD / 4; ++k) {
-            float4 v = qr[k];
-            q[4 * k] = v.x; q[4 * k + 1] = v.y; q[4 * k + 2] = v.z; q[4 * k + 3] = v.w;
+            for (int k = 0; k < 8; ++k) {
+                const float4 v = valid ? qr[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+                q[4 * k] = v.x; q[4 * k + 1] = v.y; q[4 * k + 2] = v.z; q[4 * k + 3] = v.w;
+            }
         }
         float a = 0.f;
-        for (int li = 0; li < (mean_pool ? 0 : kL); ++li) {
-            float x = 0.f, y = 0.f;
+        if (!mean_pool) {
+            f32x16 aW[2], aU[2];
 #pragma unroll
-            for (int k = 0; k < kD; ++k) {
-                x = fmaf(sW[li * kD + k], q[k], x);
-                y = fmaf(sU[li * kD + k], q[k], y);
-            }
-            a = fmaf(sw[li], tanh_times_sigmoid(x, y), a);
+            for (int mb = 0; mb < 2; ++mb) aW[mb] = aU[mb] = zero_f32x16();
+#pragma unroll
+            for (int st = 0; st < 32; ++st)
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb) {
+                    const int r = (32 * mb + n) * kPoolS + 32 * hh + st;
+                    aW[mb] = mfma_f32(sWU[r], q[st], aW[mb]);
+                    aU[mb] = mfma_f32(sWU[kL * kPoolS + r], q[st], aU[mb]);
+                }
+            float pa = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)   // hidden unit 32 mb + 8 g + 4 hh + i
+                        pa += sw[32 * mb + 8 * g + 4 * hh + i] *
+                              tanh_times_sigmoid(aW[mb][4 * g + i], aU[mb][4 * g + i]);
+            a = (pa + __shfl_xor(pa, 32)) * kLog2e;
         }
-        a *= kLog2e;
-        const float mn = fmaxf(m, a);
-        const float al = exp2f_fast(m - mn);
-        const float p = exp2f_fast(a - mn);
-        l = l * al + p;
+        if (!valid) a = -INFINITY;
+        float bm = a;
 #pragma unroll
-        for (int k = 0; k < kD; ++k) acc[k] = acc[k] * al + p * q[k];
+        for (int o = 16; o >= 1; o >>= 1) bm = fmaxf(bm, __shfl_xor(bm, o));
+        const float mn = fmaxf(m, bm);
+        const float al = exp2f_fast(m - mn);
+        const float p = valid ? exp2f_fast(a - mn) : 0.f;
+        l = l * al + (hh == 0 ? p : 0.f);
+#pragma unroll
+        for (int j = 0; j < 32; ++j) acc[j] = acc[j] * al + p * q[j];
         m = mn;
     }
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const float M = wave_max(m);
-    const float sc = (m == -INFINITY) ? 0.f : exp2f_fast(m - M);
-    const float lw = wave_sum(l * sc);
+    __syncthreads();   // the staged weights are no longer read
+
+    // Combine lanes (lanes of one half hold the same 32 features) and waves.
+    float (*s_acc)[64][33] = reinterpret_cast<float (*)[64][33]>(smem);
+    const float lw = wave_sum(l);
 #pragma unroll
-    for (int k = 0; k < kD; ++k) {
-        const float v = wave_sum(acc[k] * sc);
-        if (lane == 0) s_red[wave][2 + k] = v;
-    }
+    for (int j = 0; j < 32; ++j) s_acc[wave][lane][j] = acc[j];
     if (lane == 0) {
-        s_red[wave][0] = M;
-        s_red[wave][1] = lw;
+        s_ml[wave][0] = m;
+        s_ml[wave][1] = lw;
     }
     __syncthreads();
     if (threadIdx.x < kD) {
-        const int d = threadIdx.x;
-        float MM = -INFINITY;
-        for (int wv = 0; wv < 4; ++wv) MM = fmaxf(MM, s_red[wv][0]);
+        const int d = threadIdx.x, dh = d >> 5, j = d & 31;
+        float M = -INFINITY;
+        for (int wv = 0; wv < 4; ++wv) M = fmaxf(M, s_ml[wv][0]);
         float L = 0.f, A = 0.f;
         for (int wv = 0; wv < 4; ++wv) {
-            const float mw = s_red[wv][0];
-            const float s2 = (mw == -INFINITY) ? 0.f : exp2f_fast(mw - MM);
-            L += s_red[wv][1] * s2;
-            A += s_red[wv][2 + d] * s2;
+            const float mw = s_ml[wv][0];
+            const float sc = (mw == -INFINITY) ? 0.f : exp2f_fast(mw - M);
+            L += s_ml[wv][1] * sc;
+            float sa = 0.f;
+            for (int nn = 0; nn < 32; ++nn) sa += s_acc[wv][32 * dh + nn][j];
+            A += sa * sc;
         }
         float* o = part + ((int64_t)h * gridDim.x + c) * (2 + kD);
         if (d == 0) {
-            o[0] = MM;
+            o[0] = M;
             o[1] = L;
         }
         o[2 + d] = A;
