@@ -94,6 +94,26 @@ def measure(layer, steps, warmup):
     return ms_step, stage
 
 
+def measure_graph(layer, steps, warmup):
+    """Average ms per replay of the layer captured as a HIP graph (the same
+    launches without per-call host work), HIP events around `steps` replays."""
+    import torch
+    from paper_2609_23733_amd import vp
+    g = vp.LayerGraph(layer)
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        g.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    del g
+    return ms
+
+
 def stage_bytes(N, n_full, n_surr, n_mean, b_in, b_out):
     """Algorithmic HBM bytes per stage: the router reads Q, K and V once; the
     gather reads K and V of each FULL head and writes its fp16 K and V^T
@@ -114,6 +134,7 @@ def run_workload(S, n_full, steps, warmup, seed_key, dtype="bf16", sharp=False):
     modes = layer.modes.cpu().numpy()
     counts = [int((modes == m).sum()) for m in range(3)]
     assert counts[2] == n_full, "router did not produce the target FULL count"
+    ms_graph = measure_graph(layer, steps, warmup)
     N = S * P_TOKENS
     fl = layer_flops(N, counts[2], counts[1], counts[0])
     ff = flops_full(N, counts[2])
@@ -133,7 +154,8 @@ def run_workload(S, n_full, steps, warmup, seed_key, dtype="bf16", sharp=False):
                peak_tflops=peak,
                stage_ms={k: round(v, 4) for k, v in stage.items()},
                hbm_gbs=gbs,
-               non_full_frac=round(1.0 - full_ms / ms_step, 4))
+               non_full_frac=round(1.0 - full_ms / ms_step, 4),
+               ms_graph_replay=round(ms_graph, 4))
     return rec, layer, x
 
 

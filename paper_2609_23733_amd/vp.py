@@ -474,6 +474,28 @@ class RoutedLayer:
         return self.Y
 
 
+class LayerGraph:
+    """One pass of a RoutedLayer captured as a HIP graph (torch.cuda.CUDAGraph):
+    the same library launches on the same buffers, replayed without per-call
+    host work.  The layer's buffers (weights, workspace, router state, modes,
+    Y) stay owned by the layer; replay() overwrites Y."""
+
+    def __init__(self, layer: "RoutedLayer"):
+        self.layer = layer
+        side = torch.cuda.Stream()   # default priority
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            layer.step()             # one eager pass before capture
+        torch.cuda.current_stream().wait_stream(side)
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(self.graph):
+            layer.step()
+
+    def replay(self) -> torch.Tensor:
+        self.graph.replay()
+        return self.layer.Y
+
+
 # ------------------------------------------- dense block around the layer
 
 def block_workspace_bytes(S: int, P: int) -> int:
