@@ -25,7 +25,10 @@ __device__ __forceinline__ float sigmoid_fast(float x) {
     return rcp_fast(1.f + exp2f_fast(-kLog2e * x));
 }
 
-constexpr int kSurrRows = 384;   // tokens per workgroup
+// Tokens per workgroup: 384 (fewer weight copies per token), down to 128
+// when that would leave fewer than kSurrMinGroups workgroups over all heads.
+constexpr int kSurrRows = 384;
+constexpr int kSurrMinGroups = 2048;
 constexpr int kW = 72;           // bf16 LDS row stride
 
 // ------------------------------------------------------------------------
@@ -42,11 +45,11 @@ __global__ __launch_bounds__(256, 4) void k_surrogate_bf16(
     const bf16* __restrict__ gw1, const float* __restrict__ gb1, const bf16* __restrict__ gw2,
     const float* __restrict__ gb2, const bf16* __restrict__ dw1, const float* __restrict__ db1,
     const bf16* __restrict__ dw2, const float* __restrict__ db2, int add_v, int64_t N, int H,
-    void* __restrict__ Y, int ydt) {
+    int rows, void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
-    const int64_t t0 = (int64_t)blockIdx.x * kSurrRows;
-    const int64_t t1 = (t0 + kSurrRows < N) ? t0 + kSurrRows : N;
+    const int64_t t0 = (int64_t)blockIdx.x * rows;
+    const int64_t t1 = (t0 + rows < N) ? t0 + rows : N;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int n = lane & 31, hh = lane >> 5;
 
@@ -591,7 +594,9 @@ __global__ __launch_bounds__(256) void k_linattn_apply(const void* __restrict__ 
 // ------------------------------------------------------------------ launchers
 
 void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
-    const unsigned nbs = (unsigned)((a.N + kSurrRows - 1) / kSurrRows);
+    int rows = kSurrRows;
+    while (rows > 128 && (a.N + rows - 1) / rows * a.H < kSurrMinGroups) rows -= 128;
+    const unsigned nbs = (unsigned)((a.N + rows - 1) / rows);
     const int v = a.variant;
     if (v == SURR_EQ7 || v == SURR_MEAN_CONTEXT || v == SURR_ADD_IDENTITY) {
         const float* C = v == SURR_MEAN_CONTEXT ? a.vmean : a.ctx;
@@ -602,7 +607,7 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
             hipLaunchKernelGGL(kern, dim3(nbs, a.H), dim3(256), 0, st, (const bf16*)a.V, a.modes, C,
                                (const bf16*)a.g_w1, a.g_b1, (const bf16*)a.g_w2, a.g_b2,
                                (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2, add_v,
-                               a.N, a.H, a.Y, a.ydt);
+                               a.N, a.H, rows, a.Y, a.ydt);
         }
         else {
             const unsigned nb32 = (unsigned)((a.N + kSurr32Rows - 1) / kSurr32Rows);

@@ -49,5 +49,12 @@ def test_noalloc_router_matches_workspace_router():
 
 
 def test_noalloc_router_full_size():
-    """S = 100 (N = 137,400): the largest chunk counts the scratch must hold."""
+    """S = 100 (N = 137,400): the largest routing chunks."""
     _compare(100, 1374, "bf16", (70, 3), 0)
+
+
+def test_noalloc_router_largest_scratch():
+    """N = 32,705 with 16 heads: 64 pooling and 512 routing chunks, the
+    largest scratch any accepted shape needs (4.32 MiB of the 4.5 MiB
+    array)."""
+    _compare(31, 1055, "bf16", (70, 4), 0)
