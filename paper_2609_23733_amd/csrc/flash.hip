@@ -187,11 +187,16 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 //    reference point is 0: p = 2^S lies in [2^-10, 2^10], fp16's normal range,
 //    and a score costs one exp2 and half a pack.
 //  - WIDE: Q keeps its bf16 value (exact in fp16), logits are scaled in fp32
-//    and a running reference point m moves with the logits: a tile whose
-//    logits provably stay below m + kSlack (the tile's largest key norm bounds
-//    them) is exponentiated against m directly; only otherwise is the tile
-//    maximum taken, and m moves (rescaling O and l) only when the tile
-//    exceeds m + kSlack.  A score costs one FMA more than in FAST mode.
+//    and a running reference point m moves with the logits.  The segment's
+//    first tile sets m to its maximum; every later tile is exponentiated
+//    against m as it comes, and only if a weight or a lane's fp16 row sum
+//    overflows (some logit more than ~15 above m) is the tile maximum taken,
+//    m moved to it (O and l rescaled) and the tile's weights taken again.
+//    A score costs one FMA more than in FAST mode.  (Teacher instances keep
+//    the earlier test before the weights: a tile whose logits provably stay
+//    below m + kSlack, by its largest key norm, is exponentiated against m
+//    directly; otherwise the tile maximum is taken and m moves when the tile
+//    exceeds m + kSlack.)
 // Row sums: the packed fp16 weights of a lane's 32 keys per tile are added
 // as a tree of packed fp16 adds (at most 32 weights of at most 2^10: no
 // overflow; relative error at most 5 * 2^-11), then into l in fp32.  The
@@ -532,10 +537,59 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         if (key >= N) S[0][kb][i] = S[1][kb][i] = -INFINITY;
                     }
             }
-            const float kbt = kWide ? kmx[t0 + r] : 0.f;
+            const float kbt = (kWide && kTeach) ? kmx[t0 + r] : 0.f;
+            if (!kWide && !kTeach) {
+                // FAST: all exponentials first (in place), then the packs and
+                // row sums.
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) S[qb][kb][i] = exp2f_fast(S[qb][kb][i]);
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) {
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int b = 0; b < 2; ++b) {
+                            u32x4 pk;
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) {
+                                const f32x2 e = {S[qb][kb][8 * b + 2 * j],
+                                                 S[qb][kb][8 * b + 2 * j + 1]};
+                                pk[j] = __builtin_bit_cast(uint32_t,
+                                                           __builtin_convertvector(e, f16x2));
+                            }
+                            P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
+                        }
+                    l[qb] = tree_sum(P[qb], l[qb]);
+                }
+                return;
+            }
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
-                if (kWide) {
+                // WIDE (not teacher): the segment's first tile sets m to its
+                // maximum before the weights; later tiles are taken against m
+                // and redone only on fp16 overflow (below).
+                auto reset_m = [&] {
+                    float mx = -INFINITY;
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][kb][i]);
+                    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+                    const float mn = fmaxf(m[qb], mx);
+                    const float al = exp2f_fast(m[qb] - mn);
+                    m[qb] = mn;
+                    l[qb] *= al;
+#pragma unroll
+                    for (int db = 0; db < 2; ++db)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
+                };
+                if (kWide && !kTeach && r == 0) reset_m();
+                if (kWide && kTeach) {
                     // Keep m unless the bound cannot rule out a logit above
                     // m + kSlack for some query of this block.
                     if (__builtin_amdgcn_ballot_w64(qnc[qb] * kbt > m[qb] + kSlack) != 0) {
@@ -583,10 +637,35 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         }
                         P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                     }
-                if (kTeach)
+                if (kTeach) {
                     kahan_add(l[qb], le[qb], ls0 + ls1);
-                else
+                } else if (kWide) {
+                    const float ln = tree_sum(P[qb], l[qb]);
+                    if (__builtin_amdgcn_ballot_w64(!(ln < INFINITY)) != 0) {
+                        reset_m();
+                        const float nm2 = -m[qb];
+#pragma unroll
+                        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                            for (int b = 0; b < 2; ++b) {
+                                u32x4 pk;
+#pragma unroll
+                                for (int j = 0; j < 4; ++j) {
+                                    f32x2 e;
+                                    e[0] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j], c, nm2));
+                                    e[1] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j + 1], c, nm2));
+                                    pk[j] = __builtin_bit_cast(uint32_t,
+                                                               __builtin_convertvector(e, f16x2));
+                                }
+                                P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
+                            }
+                        l[qb] = tree_sum(P[qb], l[qb]);
+                    } else {
+                        l[qb] = ln;
+                    }
+                } else {
                     l[qb] = tree_sum(P[qb], l[qb]);
+                }
             }
         };
         const std::false_type body{};
@@ -628,8 +707,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int r = 0; r < ns - 1; ++r) {
                     mma_then(r, (r + 1) & 1);
                     phase_end();
-                    valu_phase(r, body, mode_tag);
                     fetch(r + 2);
+                    valu_phase(r, body, mode_tag);
                     prefetch_v((r + 1) & 1);
                     phase_end();
                 }
@@ -648,8 +727,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int r = 0; r < ns - 1; ++r) {
                     mma_then(r, r & 1);
                     phase_end();
-                    valu_phase(r, body, mode_tag);
                     fetch(r + 2);
+                    valu_phase(r, body, mode_tag);
                     prefetch_v((r + 1) & 1);
                     phase_end();
                 }

@@ -406,19 +406,25 @@ def test_reference_point_mixed_launch():
     check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="mixed")
 
 
-@pytest.mark.parametrize("P", [1500, 4097])
-def test_reference_point_moves(P):
-    """Key norms grow along the sequence (x1 to x8) and queries are scaled by
-    4, so logits exceed every earlier reference point several times: the
-    running reference point moves and O, l are rescaled; ragged last tile."""
-    log("reference point: growing logits P=%d" % P)
+@pytest.mark.parametrize("P,grow_to,qs", [(1500, 8.0, 4.0), (4097, 8.0, 4.0),
+                                          (1500, 2.2, 1.0), (4097, 2.2, 1.0)])
+def test_reference_point_moves(P, grow_to, qs):
+    """Key norms grow along the sequence (x1 to x`grow_to`) and queries are
+    scaled by `qs`, so logits exceed every earlier reference point several
+    times: the running reference point moves and O, l are rescaled; ragged
+    last tile.  (8, 4): logit bounds above 380, weights overflow fp16 at
+    once; (2.2, 1): bounds between 24 and 44, the row maxima creep up tile
+    by tile."""
+    log("reference point: growing logits P=%d grow=%g q*%g" % (P, grow_to, qs))
     x = synth.make_layer(1, P, dtype="bf16", key=(10, P), sharp=True, modes=FULL8,
                          qkv_device="cuda")
-    grow = torch.linspace(1.0, 8.0, x.N, device=x.K.device)[:, None, None]
+    grow = torch.linspace(1.0, grow_to, x.N, device=x.K.device)[:, None, None]
     x.K = (x.K.float() * grow).to(torch.bfloat16)
-    x.Q *= 4
-    assert (tile_bounds(x) > 64).all()
+    x.Q *= qs
+    b = tile_bounds(x, bq=512)[:, x.modes == 2]
+    assert (b > (64 if grow_to > 4 else FAST_BOUND)).all(), b
     layer = run_gpu(x, y_dtype=torch.float32)
     ref = oracle_layer(x)
     check_router(layer, ref, oracle.RULE_ARGMAX)
-    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="grow P=%d" % P)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False,
+            label="grow P=%d x%g q*%g" % (P, grow_to, qs))
