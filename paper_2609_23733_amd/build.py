@@ -23,6 +23,10 @@ ARCH = "gfx950"
 CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # Loop heads on 64-byte boundaries: the FULL-head kernel's inner loops
+    # otherwise land at addresses that cost it a few percent, differently
+    # from one build to the next.
+    "-falign-loops=64",
 ]
 # MFMA results in arch VGPRs: the softmax reads S directly instead of copying
 # it out of accumulation registers every tile.  Not for the block GEMM, whose

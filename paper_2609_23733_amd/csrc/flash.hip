@@ -186,6 +186,14 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 //    relative error 2^-11), S comes out of the MFMA in log2 units and the
 //    reference point is 0: p = 2^S lies in [2^-10, 2^10], fp16's normal range,
 //    and a score costs one exp2 and half a pack.
+//  - EXT: every logit lies within +-kExtBound.  Q and S as in FAST mode, and
+//    the reference point m of a query stays 0 unless the segment's first
+//    tile's maximum lies below kExtLow (then m is that maximum) or a weight
+//    or a lane's fp16 row sum overflows (then m moves to the tile maximum,
+//    O and l are rescaled and the tile's weights taken again).  While m = 0
+//    for every query of a wave's 32-query block, its scores cost what they
+//    cost in FAST mode; otherwise one subtraction more.  The fp16 rounding
+//    of c q moves a logit by at most 2^-11 kExtBound.
 //  - WIDE: Q keeps its bf16 value (exact in fp16), logits are scaled in fp32
 //    and a running reference point m moves with the logits.  The segment's
 //    first tile sets m to its maximum; every later tile is exponentiated
@@ -211,6 +219,8 @@ constexpr float kFastBound = 10.f;   // |logit| bound (log2 units) of FAST mode
 constexpr float kSlack = 10.f;       // WIDE: log2 headroom above the running reference
 constexpr float kF16Safe = 4096.f;   // FAST: |c q|, |k| limit for the fp16 operands
 constexpr float kF16Max = 65504.f;   // WIDE: largest finite fp16
+constexpr float kExtBound = 24.f;    // EXT: |logit| bound (log2 units)
+constexpr float kExtLow = -4.f;      // EXT: lowest first-tile maximum kept at reference 0
 
 // Kahan step: adds x to the sum s with compensation e (the sum is s - e).
 __device__ __forceinline__ void kahan_add(float& s, float& e, float x) {
@@ -330,7 +340,7 @@ __device__ __forceinline__ int tail_owner(int64_t x, int64_t T, int G) {
     return (int)(((x + 1) * G + T - 1) / T) - 1;
 }
 
-enum { ITEM_FAST = 0, ITEM_WIDE = 1, ITEM_EXACT = 2 };
+enum { ITEM_FAST = 0, ITEM_WIDE = 1, ITEM_EXACT = 2, ITEM_EXT = 3 };
 
 template <bool kTeach>
 __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ Q,
@@ -412,17 +422,19 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 qm = fmaxf(qm, sQmax[v]);
             }
             // Conditions written as "within" so that a NaN norm goes to K6b.
-            const bool fast = !kTeach && qm * c * km <= kFastBound && qm * c <= kF16Safe &&
-                              km <= kF16Safe;
+            const bool safe = !kTeach && qm * c <= kF16Safe && km <= kF16Safe;
+            const bool fast = safe && qm * c * km <= kFastBound;
+            const bool ext = safe && qm * c * km <= kExtBound;
             const bool wide = qm <= kF16Max && km <= kF16Max;
-            mode = fast ? ITEM_FAST : (wide ? ITEM_WIDE : ITEM_EXACT);
+            mode = fast ? ITEM_FAST : (ext ? ITEM_EXT : (wide ? ITEM_WIDE : ITEM_EXACT));
         }
         if (t0 == 0 && threadIdx.x == 0) exact_items[L] = mode == ITEM_EXACT;
         if (mode == ITEM_EXACT) return;   // uniform over the workgroup
 
-        // Q^T operands, kept in registers: fp16 c q (FAST) or fp16 q (WIDE).
+        // Q^T operands, kept in registers: fp16 c q (FAST, EXT) or fp16 q
+        // (WIDE).
         f16x8 Qop[2][4];
-        const float qs = mode == ITEM_FAST ? c : 1.f;
+        const float qs = mode == ITEM_WIDE ? 1.f : c;
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
@@ -463,7 +475,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         for (int qb = 0; qb < 2; ++qb) {
             O[qb][0] = O[qb][1] = zero_f32x16();
             l[qb] = le[qb] = 0.f;
-            m[qb] = mode == ITEM_FAST ? 0.f : -INFINITY;
+            m[qb] = mode == ITEM_WIDE ? -INFINITY : 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) P[qb][kb][0] = P[qb][kb][1] = zp;
         }
@@ -525,8 +537,17 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         // Vector phase of tile r: S(r) -> P(r), l += row sums.  The segment's
         // last tile masks keys >= N to weight 0 (a separate instance, so that
         // no other tile pays for the test).
+        auto tile_max = [&](int qb) {   // largest S of the tile, per query
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][kb][i]);
+            return fmaxf(mx, __shfl_xor(mx, 32));
+        };
         auto valu_phase = [&](int r, auto last_tag, auto mode_tag) {
             constexpr bool kWide = decltype(mode_tag)::value == ITEM_WIDE;
+            constexpr bool kExt = decltype(mode_tag)::value == ITEM_EXT;
             if (decltype(last_tag)::value) {
                 const int64_t k0 = (int64_t)(t0 + r) * kBK;
 #pragma unroll
@@ -538,6 +559,73 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     }
             }
             const float kbt = (kWide && kTeach) ? kmx[t0 + r] : 0.f;
+            if (kExt) {
+                // Exponentials in place (S <= kExtBound - m: finite in fp32),
+                // then fp16 packs and row sums; a query block whose weights
+                // or row sums overflow fp16 moves its reference point to the
+                // tile maximum, log2 of its largest exponential.
+                bool sh[2];
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) {
+                    if (r == 0) {
+                        const float mx = tile_max(qb);
+                        m[qb] = mx < kExtLow ? mx : 0.f;   // O, l are still 0
+                    }
+                    sh[qb] = __builtin_amdgcn_ballot_w64(m[qb] != 0.f) != 0;
+                }
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) {
+                    const float nm = -m[qb];
+                    if (sh[qb]) {
+#pragma unroll
+                        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i)
+                                S[qb][kb][i] = exp2f_fast(S[qb][kb][i] + nm);
+                    } else {
+#pragma unroll
+                        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) S[qb][kb][i] = exp2f_fast(S[qb][kb][i]);
+                    }
+                }
+                auto pack = [&](int qb, float sc) {   // P = fp16 (sc * e)
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int b = 0; b < 2; ++b) {
+                            u32x4 pk;
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) {
+                                f32x2 e = {S[qb][kb][8 * b + 2 * j], S[qb][kb][8 * b + 2 * j + 1]};
+                                if (sc != 1.f) e = e * sc;
+                                pk[j] = __builtin_bit_cast(uint32_t,
+                                                           __builtin_convertvector(e, f16x2));
+                            }
+                            P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
+                        }
+                };
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) {
+                    pack(qb, 1.f);
+                    const float ln = tree_sum(P[qb], l[qb]);
+                    if (__builtin_amdgcn_ballot_w64(!(ln < INFINITY)) != 0) {
+                        const float mn = fmaxf(m[qb], m[qb] + __log2f(tile_max(qb)));
+                        const float al = exp2f_fast(m[qb] - mn);
+                        m[qb] = mn;
+                        l[qb] *= al;
+#pragma unroll
+                        for (int db = 0; db < 2; ++db)
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
+                        pack(qb, al);
+                        l[qb] = tree_sum(P[qb], l[qb]);
+                    } else {
+                        l[qb] = ln;
+                    }
+                }
+                return;
+            }
             if (!kWide && !kTeach) {
                 // FAST: all exponentials first (in place), then the packs and
                 // row sums.
@@ -742,6 +830,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         };
         if (kTeach || mode == ITEM_WIDE)
             run(std::integral_constant<int, ITEM_WIDE>{});
+        else if (!kTeach && mode == ITEM_EXT)
+            run(std::integral_constant<int, ITEM_EXT>{});
         else
             run(std::integral_constant<int, ITEM_FAST>{});
 

@@ -385,6 +385,62 @@ def tile_bounds(x, bq=256):
 FULL8 = np.array([2, 2, 1, 0, 2, 2, 1, 0, 2, 2, 1, 0, 2, 2, 1, 0], np.uint8)
 
 
+# Logit bound (log2 units) up to which a work item keeps the zero reference
+# point until a weight overflows fp16.
+EXT_BOUND = 24.0
+
+
+def item_bounds(x):
+    """Per 512-query work item and FULL head: the Cauchy-Schwarz logit bound."""
+    return tile_bounds(x, bq=512)[:, x.modes == 2]
+
+
+def test_zero_reference_overflow_moves():
+    """Logit bounds between 14 and 24 (zero reference point kept while the
+    weights fit fp16), with one key per FULL head planted in tile 5 along
+    that head's largest query, 20 log2 units above 0: that query's weights
+    overflow fp16 mid-sequence and its reference point moves there."""
+    log("zero reference point: planted overflow")
+    x = synth.make_layer(1, 1500, dtype="bf16", key=(11, 0), sharp=True, modes=FULL8,
+                         qkv_device="cuda")
+    x.K = (x.K.float() * 0.8).to(torch.bfloat16)
+    for h in np.nonzero(x.modes == 2)[0]:
+        q = x.Q[:, h].float()
+        i0 = int(torch.linalg.vector_norm(q, dim=1).argmax())
+        qn = float(torch.linalg.vector_norm(q[i0]))
+        x.K[5 * 64 + 7, h] = (q[i0] / qn * (20.0 / (C_LOG2 * qn))).to(torch.bfloat16)
+        logit = float((x.Q[i0, h].float() @ x.K[5 * 64 + 7, h].float())) * C_LOG2
+        assert 19.5 < logit < 20.5, logit
+    b = item_bounds(x)
+    assert ((b > FAST_BOUND) & (b <= EXT_BOUND)).all(), b
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="planted overflow")
+
+
+def test_zero_reference_low_first_tile():
+    """Queries with positive components and first-tile keys pointing against
+    them (k = -(7/8) (1, ..., 1) plus small noise): every query's first-tile
+    maximum lies below -4 log2 units, so its reference point starts there;
+    later keys (random signs) raise the row maxima by about ten log2 units,
+    and queries whose weights then overflow fp16 move their reference point."""
+    log("zero reference point: low first tile")
+    x = synth.make_layer(1, 1500, dtype="bf16", key=(12, 0), sharp=True, modes=FULL8,
+                         qkv_device="cuda")
+    x.Q = (x.Q.float().abs() * 0.9).to(torch.bfloat16)
+    x.K[:64] = (-7.0 / 8.0 + 0.05 * x.K[:64].float()).to(torch.bfloat16)
+    q, k = x.Q.float().cpu(), x.K[:64].float().cpu()
+    first = torch.stack([q[:, h] @ k[:, h].T for h in range(16)]).amax(dim=2) * C_LOG2
+    assert (first[torch.from_numpy(x.modes == 2)] < -4).all(), first.max()
+    b = item_bounds(x)
+    assert ((b > FAST_BOUND) & (b <= EXT_BOUND)).all(), b
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", False, label="low first tile")
+
+
 def test_reference_point_mixed_launch():
     """Query tiles whose logits are provably small (reference point 0: bound
     at most 14 in log2 units) and tiles that need the running reference point,
