@@ -35,9 +35,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "82462dd9186039acf974f77fb447de5c2580225f0c1a76895fa6509c2b207cac",
+    "source_sha256": "b80b52bbfd4a47928a3699f2859651a929b7922339b433fef73e8dcceec1c069",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1534694, "write_kib": 109645,
+    "fetch_kib": 1496433, "write_kib": 133170,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 
