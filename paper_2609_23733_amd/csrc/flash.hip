@@ -451,8 +451,16 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         const f16* Khh = Kh + ((int64_t)slot * nkt + t0) * kBK * kD;
         const f16* Vth = Vt + ((int64_t)slot * nkt + t0) * kD * kBK;
         u32x4 g0, g1;
+        // The segment's tiles are taken in a rotated order, starting at a
+        // different tile in each of the 32 workgroups of an XCD, so that
+        // they do not all read the same tile at the same time.
+        const int rot = (int)(((int64_t)(w & 31) * ns) >> 5);
+        auto tile_of = [&](int r) {   // r < ns
+            const int t = r + rot;
+            return t >= ns ? t - ns : t;
+        };
         auto fetch = [&](int r) {   // tile r (clamped to the last one) into registers
-            r = r < ns ? r : ns - 1;
+            r = tile_of(r < ns ? r : ns - 1);
             const u32x4* src = groupB
                 ? reinterpret_cast<const u32x4*>(Vth + ((int64_t)r * kD + lr) * kBK + lc)
                 : reinterpret_cast<const u32x4*>(Khh + ((int64_t)r * kBK + lr) * kD + lc);
@@ -548,8 +556,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         auto valu_phase = [&](int r, auto last_tag, auto mode_tag) {
             constexpr bool kWide = decltype(mode_tag)::value == ITEM_WIDE;
             constexpr bool kExt = decltype(mode_tag)::value == ITEM_EXT;
-            if (decltype(last_tag)::value) {
-                const int64_t k0 = (int64_t)(t0 + r) * kBK;
+            (void)last_tag;
+            const int tr = t0 + tile_of(r);
+            if ((N & (kBK - 1)) && tr == nkt - 1) {
+                const int64_t k0 = (int64_t)tr * kBK;
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -558,7 +568,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         if (key >= N) S[0][kb][i] = S[1][kb][i] = -INFINITY;
                     }
             }
-            const float kbt = (kWide && kTeach) ? kmx[t0 + r] : 0.f;
+            const float kbt = (kWide && kTeach) ? kmx[tr] : 0.f;
             if (kExt) {
                 // Exponentials in place (S <= kExtBound - m: finite in fp32),
                 // then fp16 packs and row sums; a query block whose weights
