@@ -59,38 +59,39 @@ __global__ __launch_bounds__(64 * kCmWaves) void k_colmax(const bf16* __restrict
     const float ninv = -1.f / c;
     bf16x8 gq[kSegs];
     float go = 0.f;
-    auto gload = [&](int64_t t) {
+    // (Token indices fit int32: N is at most 2^28.)
+    const int Ni = (int)N;
+    const int64_t qstride = (int64_t)H * kD;
+    const bf16* qh = Q + (int64_t)h * kD;
+    auto gload = [&](int t) {
 #pragma unroll
         for (int i = 0; i < kSegs; ++i) {
             const int sg = threadIdx.x + i * kThreads;
-            const int64_t q = t * kCmQ + (sg >> 3);
-            gq[i] = load_bf16x8(Q + ((q < N ? q : 0) * H + h) * kD + (sg & 7) * 8);
+            const int q = min(t * kCmQ + (sg >> 3), Ni - 1);
+            gq[i] = load_bf16x8(qh + (int64_t)q * qstride + (sg & 7) * 8);
         }
         // (scaled at the store, so that nothing waits for the load here)
-        if (threadIdx.x < kCmQ) {
-            const int64_t qq = t * kCmQ + threadIdx.x;
-            go = oh[qq < N ? qq : N - 1];
-        }
+        if (threadIdx.x < kCmQ) go = oh[min(t * kCmQ + (int)threadIdx.x, Ni - 1)];
     };
-    auto lstore = [&](int64_t t, int b) {
+    auto lstore = [&](int t, int b) {
 #pragma unroll
         for (int i = 0; i < kSegs; ++i) {
             const int sg = threadIdx.x + i * kThreads;
             *reinterpret_cast<bf16x8*>(&sQ[b][(sg >> 3) * kDL + (sg & 7) * 8]) = gq[i];
         }
         if (threadIdx.x < kCmQ)
-            sO[b][threadIdx.x] = t * kCmQ + threadIdx.x < N ? go * ninv : -INFINITY;
+            sO[b][threadIdx.x] = t * kCmQ + (int)threadIdx.x < Ni ? go * ninv : -INFINITY;
     };
     float acc[kCmKB][16];
 #pragma unroll
     for (int kb = 0; kb < kCmKB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[kb][r] = -INFINITY;
-    const int64_t nt = (N + kCmQ - 1) / kCmQ;
+    const int nt = (Ni + kCmQ - 1) / kCmQ;
     gload(0);
     lstore(0, 0);
     __syncthreads();
-    for (int64_t t = 0; t < nt; ++t) {
+    for (int t = 0; t < nt; ++t) {
         const int b = (int)(t & 1);
         if (t + 1 < nt) gload(t + 1);
 #pragma unroll
@@ -104,9 +105,16 @@ __global__ __launch_bounds__(64 * kCmWaves) void k_colmax(const bf16* __restrict
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks)
                     qv[u][ks] = *reinterpret_cast<const bf16x8*>(&sQ[b][row * kDL + 16 * ks + 8 * hh]);
+                // ci = 16 copies of o: one copy into a register pair, then
+                // 64-bit moves (8 instructions instead of 16).
                 const float o = sO[b][row];
+                const uint32_t ob = __builtin_bit_cast(uint32_t, o);
+                const uint64_t pr = ((uint64_t)ob << 32) | ob;
+                uint64_t c8[8];
+                c8[0] = pr;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) ci[u][r] = o;
+                for (int r = 1; r < 8; ++r) asm volatile("v_mov_b64 %0, %1" : "=v"(c8[r]) : "v"(pr));
+                ci[u] = __builtin_bit_cast(f32x16, c8);
             }
 #pragma unroll
             for (int kb = 0; kb < kCmKB; ++kb) {

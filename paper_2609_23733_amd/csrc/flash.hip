@@ -326,6 +326,7 @@ constexpr int kStreamWG = 256;      // grid: one workgroup per CU
 constexpr int kPartFloats = kBQf * kD + 2 * kBQf;   // partial slot: O[512][64], l[512], m[512]
 
 constexpr int kMinPartTiles = 8;    // fewest key tiles per workgroup in the tail
+constexpr int64_t kRotateTiles = 4096;   // 64 MB of K and V^T tiles (16 KB each)
 
 // Workgroups used for T tail steps (at most G, at least kMinPartTiles steps
 // each), the first step of workgroup w, and the workgroup holding step x.
@@ -451,10 +452,14 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
         const f16* Khh = Kh + ((int64_t)slot * nkt + t0) * kBK * kD;
         const f16* Vth = Vt + ((int64_t)slot * nkt + t0) * kD * kBK;
         u32x4 g0, g1;
-        // The segment's tiles are taken in a rotated order, starting at a
-        // different tile in each of the 32 workgroups of an XCD, so that
-        // they do not all read the same tile at the same time.
-        const int rot = (int)(((int64_t)(w & 31) * ns) >> 5);
+        // While all FULL heads' tiles fit in 64 MB (a quarter of the
+        // last-level cache), the segment's tiles are taken in a rotated
+        // order, starting at a different tile in each of the 32 workgroups of
+        // an XCD, so that they do not all read the same tile at the same time
+        // (larger sets are read in step, so that the workgroups of an XCD
+        // share what its L2 holds).
+        const int rot = (int64_t)nfull * nkt <= kRotateTiles
+                            ? (int)(((int64_t)(w & 31) * ns) >> 5) : 0;
         auto tile_of = [&](int r) {   // r < ns
             const int t = r + rot;
             return t >= ns ? t - ns : t;
