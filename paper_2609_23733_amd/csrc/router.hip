@@ -6,6 +6,8 @@
 // Every reduction over tokens is split into fixed token chunks whose partial
 // results are combined in chunk order by a second kernel: no float atomics,
 // so results are bitwise reproducible run to run.
+#include <type_traits>
+
 #include "vp_device.hpp"
 #include "vp_internal.hpp"
 
@@ -21,6 +23,17 @@ __device__ __forceinline__ float tanh_times_sigmoid(float x, float y) {
     return (1.f - e1) * rcp_fast((1.f + e1) * (1.f + e2));
 }
 
+// acc + w tanh(x) sigmoid(y), as w (1 - e1) / ((1 + e1) (1 + e2)): the same
+// clamp (a median of three, which also passes NaN through without the
+// canonicalising move of fminf/fmaxf) and exponentials as above, the
+// numerator and the denominator's product each by one FMA.
+__device__ __forceinline__ float add_w_tanh_times_sigmoid(float acc, float w, float x, float y) {
+    x = __builtin_amdgcn_fmed3f(x, -15.f, 15.f);
+    const float e1 = exp2f_fast(-2.f * kLog2e * x);
+    const float e2p1 = exp2f_fast(-kLog2e * y) + 1.f;
+    return fmaf(fmaf(-e1, w, w), rcp_fast(fmaf(e1, e2p1, e2p1)), acc);
+}
+
 // ------------------------------------------------------------------------
 // K1: gated attention pooling, partial sums per (token chunk, head).
 // part1[c][h] = (m, l, acc[64]) with m = max_i a_i (log2 units: a * log2 e),
@@ -34,7 +47,7 @@ __device__ __forceinline__ float tanh_times_sigmoid(float x, float y) {
 // The four 32-row blocks of A are W rows 0-31, W rows 32-63, U rows 0-31,
 // U rows 32-63, so W and U results for one hidden unit l land in the same
 // lane and register.
-__global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restrict__ Q,
+__global__ __launch_bounds__(256, 3) void k_pool_partial_bf16(const bf16* __restrict__ Q,
                                                            const bf16* __restrict__ W,
                                                            const bf16* __restrict__ U,
                                                            const bf16* __restrict__ w,
@@ -80,15 +93,11 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) B[ks] = load_bf16x8(qrow + 16 * ks + 8 * hh);
     };
-    bf16x8 Bc[4], Bn[4];
-    load_q(t0 + 32 * wave, Bc);
-    for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
+    // One 32-token block: B holds its tokens' rows (tail lanes hold the
+    // chunk's first row, a finite value that p = 0 removes from the sums).
+    auto block = [&](int64_t tb, const bf16x8 (&B)[4], auto fixed_tag) {
         const int64_t tok = tb + n;
         const bool valid = tok < t1;
-        load_q(tb + 128 < t1 ? tb + 128 : tb, Bn);
-        bf16x8 B[4];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) B[ks] = valid ? Bc[ks] : zero_bf16x8();
         float a = 0.f;
         if (!mean_pool) {
             // An opaque offset keeps the fragment reads in the loop (hoisted,
@@ -119,25 +128,70 @@ __global__ __launch_bounds__(256) void k_pool_partial_bf16(const bf16* __restric
                     const f32x4 wq = *reinterpret_cast<const f32x4*>(&sw[32 * mb + 8 * g + 4 * hh]);
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        pa += wq[i] * tanh_times_sigmoid(aW[mb][4 * g + i], aU[mb][4 * g + i]);
+                        pa = add_w_tanh_times_sigmoid(pa, wq[i], aW[mb][4 * g + i],
+                                                      aU[mb][4 * g + i]);
                 }
             a = (pa + __shfl_xor(pa, 32)) * kLog2e;
+        }
+        if (decltype(fixed_tag)::value) {
+            // Reference point 0: p = 2^a, |a| <= ||w_h||_1 log2 e.
+            const float p = valid ? exp2f_fast(a) : 0.f;
+            l += hh == 0 ? p : 0.f;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    acc[8 * ks + j] = fmaf(p, bf16_to_f32(B[ks][j]), acc[8 * ks + j]);
+            return;
         }
         if (!valid) a = -INFINITY;
         float bm = a;
 #pragma unroll
         for (int o = 16; o >= 1; o >>= 1) bm = fmaxf(bm, __shfl_xor(bm, o));
         const float mn = fmaxf(m, bm);
-        const float al = exp2f_fast(m - mn);
         const float p = valid ? exp2f_fast(a - mn) : 0.f;
-        l = l * al + (hh == 0 ? p : 0.f);
+        // (m and mn are the same in every lane: the rescale is skipped, as
+        // a whole wave, whenever the block leaves the maximum unchanged.)
+        if (__builtin_amdgcn_readfirstlane(mn != m ? 1 : 0)) {
+            const float al = exp2f_fast(m - mn);
+            l = l * al + (hh == 0 ? p : 0.f);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+            for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc[8 * ks + j] = acc[8 * ks + j] * al + p * bf16_to_f32(B[ks][j]);
+                for (int j = 0; j < 8; ++j)
+                    acc[8 * ks + j] = acc[8 * ks + j] * al + p * bf16_to_f32(B[ks][j]);
+        } else {
+            l += hh == 0 ? p : 0.f;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    acc[8 * ks + j] = fmaf(p, bf16_to_f32(B[ks][j]), acc[8 * ks + j]);
+        }
         m = mn;
+    };
+    auto loop = [&](auto fixed_tag) {
+        bf16x8 Bc[4], Bn[4];
+        load_q(t0 + 32 * wave, Bc);
+        for (int64_t tb = t0 + 32 * wave; tb < t1; tb += 128) {
+            load_q(tb + 128 < t1 ? tb + 128 : tb, Bn);
+            block(tb, Bc, fixed_tag);
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) Bc[ks] = Bn[ks];
+            for (int ks = 0; ks < 4; ++ks) Bc[ks] = Bn[ks];
+        }
+    };
+    // While ||w_h||_1 log2 e <= 60 every 2^a lies in [2^-60, 2^60], and the
+    // sums need no reference point (m = 0); otherwise a running maximum.
+    float wl1 = 0.f;
+    if (!mean_pool) {
+        wl1 = wave_sum(lane < kL ? fabsf(sw[lane]) : 0.f) * kLog2e;
+        wl1 = __builtin_amdgcn_readfirstlane(wl1);
+    }
+    if (mean_pool || wl1 <= 60.f) {
+        m = 0.f;
+        loop(std::true_type{});
+    } else {
+        loop(std::false_type{});
     }
     __syncthreads();   // the staged weights are no longer read
 

@@ -159,6 +159,26 @@ def test_bf16_output_and_relu():
         check_y(layer.Y.double().cpu().numpy(), ref["Y"], "bf16", True, label="act=%d" % act)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("wscale", [1.0, 20.0])
+def test_pooling_weight_scale(dtype, wscale):
+    """Gated pooling (Eq.1-2) with the pooling vector w as drawn (|w|_1 log2 e
+    near 6: every exponential of the pooling logits fits fp32 without a
+    reference point) and scaled by 20 (near 115: the pooling sums keep a
+    running maximum)."""
+    log("pooling weights x%g %s" % (wscale, dtype))
+    x = synth.make_layer(2, 700, dtype=dtype, key=(13, 0), sharp=True, n_full=6,
+                         qkv_device="cuda")
+    x.w = (x.w.float() * wscale).to(x.w.dtype)
+    l1 = x.w.float().abs().sum(dim=1) * 1.4426950408889634
+    assert ((l1 < 60) if wscale == 1.0 else (l1 > 60)).all(), l1
+    layer = run_gpu(x, y_dtype=torch.float32)
+    ref = oracle_layer(x)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    check_y(layer.Y.double().cpu().numpy(), ref["Y"], dtype, False,
+            label="pool w x%g %s" % (wscale, dtype))
+
+
 def test_single_token():
     """N = 1: FULL returns v, MEAN returns v, s = 1 (every head FULL under Eq.4)."""
     log("N=1")
