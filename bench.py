@@ -35,9 +35,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "b80b52bbfd4a47928a3699f2859651a929b7922339b433fef73e8dcceec1c069",
+    "source_sha256": "b96dc36c053f0c5914ab3e6bb3208a511575dd086bee1ddac738bfce90d6abde",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1496433, "write_kib": 133170,
+    "fetch_kib": 1538197, "write_kib": 117837,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 
