@@ -372,7 +372,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 
     // One segment: key tiles [t0, t1) of item L; written to partial slot
     // pslot of this workgroup if the segment is not the whole item.
-    auto segment = [&](int L, int t0, int t1, int pslot) {
+    auto segment = [&](int L, int t0, int t1, int pslot) __attribute__((always_inline)) {
         const int slot = L / nqt, qt = L - slot * nqt;
         const int h = full_head(buckets, H, slot);
         if (h < 0) return;
@@ -558,7 +558,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][kb][i]);
             return fmaxf(mx, __shfl_xor(mx, 32));
         };
-        auto valu_phase = [&](int r, auto last_tag, auto mode_tag) {
+        auto valu_phase = [&](int r, auto last_tag, auto mode_tag, auto mid) {
             constexpr bool kWide = decltype(mode_tag)::value == ITEM_WIDE;
             constexpr bool kExt = decltype(mode_tag)::value == ITEM_EXT;
             (void)last_tag;
@@ -638,6 +638,9 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     } else {
                         l[qb] = ln;
                     }
+                    // (the first block's S is dead: the next V operands' LDS
+                    // reads go here, under the second block's work)
+                    if (qb == 0) mid();
                 }
                 return;
             }
@@ -666,8 +669,12 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                             }
                             P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                         }
-                    l[qb] = tree_sum(P[qb], l[qb]);
                 }
+                // (S is dead: the next V operands' LDS reads go here, so that
+                // they complete under the row sums rather than at the barrier.)
+                mid();
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) l[qb] = tree_sum(P[qb], l[qb]);
                 return;
             }
 #pragma unroll
@@ -770,6 +777,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     l[qb] = tree_sum(P[qb], l[qb]);
                 }
             }
+            mid();
         };
         const std::false_type body{};
         const std::true_type tail{};
@@ -811,14 +819,12 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     mma_then(r, (r + 1) & 1);
                     phase_end();
                     fetch(r + 2);
-                    valu_phase(r, body, mode_tag);
-                    prefetch_v((r + 1) & 1);
+                    valu_phase(r, body, mode_tag, [&] { prefetch_v((r + 1) & 1); });
                     phase_end();
                 }
                 mma_then(ns - 1, -1);
                 phase_end();
-                valu_phase(ns - 1, tail, mode_tag);
-                prefetch_v(ns & 1);
+                valu_phase(ns - 1, tail, mode_tag, [&] { prefetch_v(ns & 1); });
                 phase_end();
                 phase_end();
             } else {
@@ -831,14 +837,12 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     mma_then(r, r & 1);
                     phase_end();
                     fetch(r + 2);
-                    valu_phase(r, body, mode_tag);
-                    prefetch_v((r + 1) & 1);
+                    valu_phase(r, body, mode_tag, [&] { prefetch_v((r + 1) & 1); });
                     phase_end();
                 }
                 mma_then(ns - 1, -1);
                 phase_end();
-                valu_phase(ns - 1, tail, mode_tag);
-                prefetch_v(ns & 1);
+                valu_phase(ns - 1, tail, mode_tag, [&] { prefetch_v(ns & 1); });
                 phase_end();
             }
             pv();   // O += V(ns-1) P(ns-1)
