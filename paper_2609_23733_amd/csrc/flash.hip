@@ -776,8 +776,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 } else {
                     l[qb] = tree_sum(P[qb], l[qb]);
                 }
+                if (qb == 0) mid();   // (after the first block, as in EXT mode)
             }
-            mid();
         };
         const std::false_type body{};
         const std::true_type tail{};
