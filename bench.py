@@ -35,9 +35,9 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "b96dc36c053f0c5914ab3e6bb3208a511575dd086bee1ddac738bfce90d6abde",
+    "source_sha256": "9c61a8dd16be87dd796d98d177bdf8e70882932a07d05977e93ca2332fcbaa21",
     "S": 100, "n_full": 4,
-    "fetch_kib": 1538197, "write_kib": 117837,
+    "fetch_kib": 1368856, "write_kib": 120916,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,
 }
 
