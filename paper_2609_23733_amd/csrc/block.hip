@@ -167,7 +167,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
                 dst = g.out + t * g.F + fbase;
                 if (EPI == EPI_GELU) {
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) v[r] = gelu_erf(v[r]);
+                    for (int r = 0; r < 16; ++r) v[r] = gelu(v[r]);
                 } else {   // ls (acc + bias) + res + res2, summed in fp32
 #pragma unroll
                     for (int gq = 0; gq < 4; ++gq) {

@@ -18,7 +18,7 @@ namespace vp {
 
 __device__ __forceinline__ float act_fn(float x, int act) {
     if (act == 1) return fmaxf(x, 0.f);
-    return gelu_erf(x);
+    return gelu(x);
 }
 
 __device__ __forceinline__ float sigmoid_fast(float x) {
