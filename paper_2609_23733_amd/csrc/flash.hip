@@ -620,28 +620,35 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                             P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
                         }
                 };
+                // Both blocks packed and summed, then one overflow test for
+                // the two (a branch per block would keep the second block's
+                // work from overlapping the first one's dependent sums).
+                float ln[2];
 #pragma unroll
-                for (int qb = 0; qb < 2; ++qb) {
-                    pack(qb, 1.f);
-                    const float ln = tree_sum(P[qb], l[qb]);
-                    if (__builtin_amdgcn_ballot_w64(!(ln < INFINITY)) != 0) {
-                        const float mn = fmaxf(m[qb], m[qb] + __log2f(tile_max(qb)));
-                        const float al = exp2f_fast(m[qb] - mn);
-                        m[qb] = mn;
-                        l[qb] *= al;
+                for (int qb = 0; qb < 2; ++qb) pack(qb, 1.f);
 #pragma unroll
-                        for (int db = 0; db < 2; ++db)
+                for (int qb = 0; qb < 2; ++qb) ln[qb] = tree_sum(P[qb], l[qb]);
+                if (__builtin_amdgcn_ballot_w64(!(ln[0] < INFINITY) || !(ln[1] < INFINITY)) != 0) {
 #pragma unroll
-                            for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
-                        pack(qb, al);
-                        l[qb] = tree_sum(P[qb], l[qb]);
-                    } else {
-                        l[qb] = ln;
+                    for (int qb = 0; qb < 2; ++qb) {
+                        if (__builtin_amdgcn_ballot_w64(!(ln[qb] < INFINITY)) != 0) {
+                            const float mn = fmaxf(m[qb], m[qb] + __log2f(tile_max(qb)));
+                            const float al = exp2f_fast(m[qb] - mn);
+                            m[qb] = mn;
+                            l[qb] *= al;
+#pragma unroll
+                            for (int db = 0; db < 2; ++db)
+#pragma unroll
+                                for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
+                            pack(qb, al);
+                            ln[qb] = tree_sum(P[qb], l[qb]);
+                        }
                     }
-                    // (the first block's S is dead: the next V operands' LDS
-                    // reads go here, under the second block's work)
-                    if (qb == 0) mid();
                 }
+                l[0] = ln[0];
+                l[1] = ln[1];
+                // (S is dead: the next V operands' LDS reads)
+                mid();
                 return;
             }
             if (!kWide && !kTeach) {
