@@ -684,28 +684,31 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int qb = 0; qb < 2; ++qb) l[qb] = tree_sum(P[qb], l[qb]);
                 return;
             }
+            // WIDE (not teacher): the segment's first tile sets m to its
+            // maximum before the weights; later tiles are taken against m and
+            // redone only on fp16 overflow (below).
+            auto reset_m = [&](int qb) {
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][kb][i]);
+                mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
+                const float mn = fmaxf(m[qb], mx);
+                const float al = exp2f_fast(m[qb] - mn);
+                m[qb] = mn;
+                l[qb] *= al;
+#pragma unroll
+                for (int db = 0; db < 2; ++db)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
+            };
+            if (kWide && !kTeach && r == 0) {
+                reset_m(0);
+                reset_m(1);
+            }
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
-                // WIDE (not teacher): the segment's first tile sets m to its
-                // maximum before the weights; later tiles are taken against m
-                // and redone only on fp16 overflow (below).
-                auto reset_m = [&] {
-                    float mx = -INFINITY;
-#pragma unroll
-                    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, S[qb][kb][i]);
-                    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c;
-                    const float mn = fmaxf(m[qb], mx);
-                    const float al = exp2f_fast(m[qb] - mn);
-                    m[qb] = mn;
-                    l[qb] *= al;
-#pragma unroll
-                    for (int db = 0; db < 2; ++db)
-#pragma unroll
-                        for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
-                };
-                if (kWide && !kTeach && r == 0) reset_m();
                 if (kWide && kTeach) {
                     // Keep m unless the bound cannot rule out a logit above
                     // m + kSlack for some query of this block.
@@ -756,35 +759,43 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                     }
                 if (kTeach) {
                     kahan_add(l[qb], le[qb], ls0 + ls1);
-                } else if (kWide) {
-                    const float ln = tree_sum(P[qb], l[qb]);
-                    if (__builtin_amdgcn_ballot_w64(!(ln < INFINITY)) != 0) {
-                        reset_m();
-                        const float nm2 = -m[qb];
-#pragma unroll
-                        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                            for (int b = 0; b < 2; ++b) {
-                                u32x4 pk;
-#pragma unroll
-                                for (int j = 0; j < 4; ++j) {
-                                    f32x2 e;
-                                    e[0] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j], c, nm2));
-                                    e[1] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j + 1], c, nm2));
-                                    pk[j] = __builtin_bit_cast(uint32_t,
-                                                               __builtin_convertvector(e, f16x2));
-                                }
-                                P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
-                            }
-                        l[qb] = tree_sum(P[qb], l[qb]);
-                    } else {
-                        l[qb] = ln;
-                    }
-                } else {
-                    l[qb] = tree_sum(P[qb], l[qb]);
+                    if (qb == 0) mid();   // (the first block's S is dead)
                 }
-                if (qb == 0) mid();   // (after the first block, as in EXT mode)
             }
+            if (kTeach) return;
+            // WIDE: both blocks' fp16 row sums, then one overflow vote for
+            // the two (as in EXT mode); a block that overflowed moves m to
+            // its tile maximum and is taken again from its fp32 logits.
+            float ln[2];
+#pragma unroll
+            for (int qb = 0; qb < 2; ++qb) ln[qb] = tree_sum(P[qb], l[qb]);
+            if (__builtin_amdgcn_ballot_w64(!(ln[0] < INFINITY) || !(ln[1] < INFINITY)) != 0) {
+#pragma unroll
+                for (int qb = 0; qb < 2; ++qb) {
+                    if (__builtin_amdgcn_ballot_w64(!(ln[qb] < INFINITY)) == 0) continue;
+                    reset_m(qb);
+                    const float nm2 = -m[qb];
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int b = 0; b < 2; ++b) {
+                            u32x4 pk;
+#pragma unroll
+                            for (int j = 0; j < 4; ++j) {
+                                f32x2 e;
+                                e[0] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j], c, nm2));
+                                e[1] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j + 1], c, nm2));
+                                pk[j] = __builtin_bit_cast(uint32_t,
+                                                           __builtin_convertvector(e, f16x2));
+                            }
+                            P[qb][kb][b] = __builtin_bit_cast(f16x8, pk);
+                        }
+                    ln[qb] = tree_sum(P[qb], l[qb]);
+                }
+            }
+            l[0] = ln[0];
+            l[1] = ln[1];
+            mid();   // (S is dead)
         };
         const std::false_type body{};
         const std::true_type tail{};
