@@ -118,6 +118,36 @@ def test_block_full_size_sampled():
     check_update(out[rt], Xr, ref, "S=100 out")
 
 
+def test_block_element_offsets_past_2_32():
+    """N = 3053 x 1374 = 4,194,822 tokens: the FFN's 4096-wide hidden rows
+    pass 2^32 elements from token 2^20 on, the 1024-wide rows of X, Q, K, V
+    and the update from token 2^22.  Both stages on every token; sampled rows
+    on both sides of both boundaries and the last row."""
+    from paper_2609_23733_amd import vp
+    S, P = 3053, synth.TOKENS_PER_VIEW
+    N = S * P
+    log("block element offsets past 2^32: N=%d" % N)
+    wt = synth.make_block_weights((25, 0))
+    wd = {k: v.cuda() for k, v in wt.items()}
+    X = synth.make_block_input(S, P, key=(25, 0), device="cuda")
+    pos = synth.token_positions(S, P)
+    ws = torch.empty(vp.block_workspace_bytes(S, P), dtype=torch.uint8, device="cuda")
+    Q, K, V = vp.block_qkv(X, torch.from_numpy(pos).cuda(), wd, S, P, ws)
+    Y = synth.stored(synth.normal((N, D), synth.derive_seed(25, 0, 99), 0.1, "cuda"), "bf16")
+    out = vp.block_out(X, Y, wd, S, P, ws)
+    torch.cuda.synchronize()
+    edges = [2 ** 20 - 1, 2 ** 20, 2 ** 22 - 1, 2 ** 22, N - 2, N - 1]
+    rows = np.unique(np.concatenate([synth.sample_rows(N, 26, synth.derive_seed(25, 0, 20)),
+                                     np.array(edges)])).astype(np.int64)
+    rt = torch.from_numpy(rows).cuda()
+    Xr = X[rt].cpu()
+    rq, rk, rv = oracle.block_qkv(Xr, pos[rows], wt)
+    for nm, g, r in (("Q", Q, rq), ("K", K, rk), ("V", V, rv)):
+        check_y(g[rt].double().cpu().numpy(), r, "bf16", True, label="N=%d %s" % (N, nm))
+    ref, _ = oracle.block_out(Xr, Y[rt].cpu(), wt)
+    check_update(out[rt], Xr, ref, "N=%d out" % N)
+
+
 @pytest.mark.parametrize("dtype_note", ["bf16"])
 def test_whole_block(dtype_note):
     """qkv -> routed layer (router, modes, attention) -> out, against the

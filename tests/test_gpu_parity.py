@@ -386,6 +386,62 @@ def test_full_size_sharp(S, y_bf16):
     check_y(Yg, ref["Y"], "bf16", y_bf16, label="sharp S=%d" % S)
 
 
+def test_element_offsets_past_2_32():
+    """N = 3053 x 1374 = 4,194,822 tokens: element offsets token * 1024 + 64 h
+    + i pass 2^32 from token 2^22 on.  The last head runs FULL (the largest
+    offsets), head 14 SURR and head 13 MEAN; fp32 Y.  Sampled rows straddle
+    the boundary (tokens 2^22 - 1, 2^22 and the last one among them).  The
+    oracle sees one head at a time ([N, 1, d] slices): router state of the
+    three heads (Eq.1-3, Eq.5 context and value mean), the FULL head's rows,
+    the SURR head's rows (Eq.5-7 with the oracle's C_h) and the MEAN head's
+    rows."""
+    S, P = 3053, 1374
+    N = S * P
+    assert N * 16 * 64 > 2 ** 32
+    modes = np.array([1, 0] * 7 + [1, 2], np.uint8)
+    hf, hs, hm = 15, 14, 13
+    log("element offsets past 2^32: N=%d" % N)
+    x = synth.make_layer(S, P, dtype="bf16", key=(S, 5), modes=modes, qkv_device="cuda")
+    layer = run_gpu(x, y_dtype=torch.float32)
+    np.testing.assert_array_equal(layer.modes.cpu().numpy(), modes)
+    b = 2 ** 22
+    rows = np.unique(np.concatenate([
+        synth.sample_rows(N, 20, synth.derive_seed(S, 5, 20)),
+        np.array([0, b - 1, b, b + 1, N - 2, N - 1])])).astype(np.int64)
+    Yg = layer.Y[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    st = layer.state
+    ref = {}
+    for h in (hf, hs, hm):
+        sl = slice(h, h + 1)
+        Qh, Kh, Vh = (t[:, sl].float().cpu() for t in (x.Q, x.K, x.V))
+        qp = oracle.router_pool(Qh, x.W[sl], x.U[sl], x.w[sl])
+        s, C, mean = oracle.router_route(Kh, Vh, qp)
+        for name, g, r in (("q_pool", st.q_pool[h], qp[0]), ("ctx", st.ctx[h], C[0]),
+                           ("vmean", st.vmean[h], mean[0])):
+            g = g.cpu().numpy().astype(np.float64)
+            err = np.abs(g - r).max()
+            assert err <= 1e-4 * max(rms(r), 1e-30), (name, h, err, rms(r))
+        np.testing.assert_allclose(float(st.score[h]), s[0], rtol=1e-4)
+        if h == hf:
+            ref[h] = oracle.full_rows(Qh, Kh, Vh, 0, rows)
+        elif h == hs:
+            surr = {k: v[sl] for k, v in x.surr.items()}
+            ref[h] = oracle.surr_rows(Vh, C[0], surr, 0, rows)
+        else:
+            ref[h] = np.broadcast_to(mean[0], (rows.shape[0], 64))
+        del Qh, Kh, Vh
+    for h in (hf, hs, hm):
+        r = ref[h]
+        err = np.abs(Yg[:, h, :] - r)
+        bound = TOL["bf16"] * rms(r)
+        log("offsets past 2^32: head %d worst err/bound = %.3f" % (h, float(err.max() / bound)))
+        assert (err <= bound).all(), (h, float(err.max()), bound)
+    # MEAN rows are the head's value mean itself, wherever they lie
+    np.testing.assert_array_equal(
+        Yg[:, hm, :], np.broadcast_to(st.vmean[hm].cpu().numpy().astype(np.float64),
+                                      (rows.shape[0], 64)))
+
+
 # ------------------------------------ softmax reference point (FULL, bf16)
 
 C_LOG2 = 1.4426950408889634 / 8.0
