@@ -35,6 +35,47 @@ def _gpu():
     vp.load_library()
 
 
+def test_tome_element_offsets_past_2_32():
+    """N = 3053 x 1374 = 4,194,822 tokens at merging ratio 0.9: token rows of
+    [N, 16, 64] inputs pass 2^32 elements from token 2^22 on.  The plan is
+    checked as at S = 100 (64 sampled decisions against the oracle, rows and
+    member lists of every token exactly); merged rows whose members lie past
+    the boundary on a sample; the unmerged [N, 16, 64] output against the
+    merged rows it copies, bitwise."""
+    from paper_2609_23733_amd import vp
+    S, P = 3053, synth.TOKENS_PER_VIEW
+    N = S * P
+    M = int(0.9 * N)
+    log("tome element offsets past 2^32: N=%d M=%d" % (N, M))
+    K = synth.stored(synth.normal((N, 16, 64), synth.derive_seed(48, S, 0), 1.0, "cuda"), "bf16")
+    plan = run_plan(K, S, P, M)
+    Kc = K.cpu()
+    is_dst, _ = oracle.tome_split(S, P, M)
+    nsrc = int((~is_dst).sum())
+    sample = synth.sample_rows(nsrc, 64, synth.derive_seed(48, S, 1))
+    check_plan(Kc, S, P, M, plan, "N=%d" % N, srcs_sample=sample)
+    X = synth.stored(synth.normal((N, 16, 64), synth.derive_seed(48, S, 2), 1.0, "cuda"), "bf16")
+    Xm = vp.tome_merge(X, plan)
+    back = vp.tome_unmerge(Xm, plan)
+    torch.cuda.synchronize()
+    assert torch.equal(back, Xm[plan.row.long()])
+    rs = plan.row_start.cpu().numpy().astype(np.int64)
+    mem = plan.members.cpu().numpy().astype(np.int64)
+    row = plan.row.cpu().numpy().astype(np.int64)
+    high = np.unique(row[2 ** 22:])
+    pick = synth.sample_rows(high.shape[0], 24, synth.derive_seed(48, S, 3))
+    rows = np.unique(np.concatenate([high[pick], [row[2 ** 22 - 1], row[N - 1]]]))
+    toks = np.concatenate([mem[rs[r]:rs[r + 1]] for r in rows])
+    assert toks.max() >= 2 ** 22
+    lab = np.concatenate([np.full(rs[r + 1] - rs[r], i) for i, r in enumerate(rows)])
+    Xs = X[torch.from_numpy(toks).cuda()].cpu()
+    ref = oracle.tome_merge(Xs, lab, rows.shape[0])
+    g = Xm[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    bound = merged_bound(ref, rs[rows + 1] - rs[rows], float(Xs.float().abs().max()), True)
+    log("N=%d merge worst err/bound = %.3f" % (N, float((np.abs(g - ref) / bound).max())))
+    assert (np.abs(g - ref) <= bound).all()
+
+
 def run_plan(K, S, P, M):
     from paper_2609_23733_amd import vp
     plan = vp.TomePlan(S, P, M, want_best=True)
