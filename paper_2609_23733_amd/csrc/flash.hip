@@ -573,7 +573,7 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                         if (key >= N) S[0][kb][i] = S[1][kb][i] = -INFINITY;
                     }
             }
-            const float kbt = (kWide && kTeach) ? kmx[tr] : 0.f;
+            const float kbt = kTeach ? kmx[tr] : 0.f;
             if (kExt) {
                 // Exponentials in place (S <= kExtBound - m: finite in fp32),
                 // then fp16 packs and row sums; a query block whose weights
@@ -684,9 +684,10 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
                 for (int qb = 0; qb < 2; ++qb) l[qb] = tree_sum(P[qb], l[qb]);
                 return;
             }
-            // WIDE (not teacher): the segment's first tile sets m to its
-            // maximum before the weights; later tiles are taken against m and
-            // redone only on fp16 overflow (below).
+            // WIDE items and teacher instances from here on.  WIDE (not
+            // teacher): the segment's first tile sets m to its maximum before
+            // the weights; later tiles are taken against m and redone only on
+            // fp16 overflow (below).
             auto reset_m = [&](int qb) {
                 float mx = -INFINITY;
 #pragma unroll
@@ -703,13 +704,13 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 #pragma unroll
                     for (int i = 0; i < 16; ++i) O[qb][db][i] *= al;
             };
-            if (kWide && !kTeach && r == 0) {
+            if (!kTeach && r == 0) {
                 reset_m(0);
                 reset_m(1);
             }
 #pragma unroll
             for (int qb = 0; qb < 2; ++qb) {
-                if (kWide && kTeach) {
+                if (kTeach) {
                     // Keep m unless the bound cannot rule out a logit above
                     // m + kSlack for some query of this block.
                     if (__builtin_amdgcn_ballot_w64(qnc[qb] * kbt > m[qb] + kSlack) != 0) {
@@ -741,13 +742,8 @@ __global__ __launch_bounds__(512, 1) void k_flash_bf16(const bf16* __restrict__ 
 #pragma unroll
                         for (int j = 0; j < 4; ++j) {
                             f32x2 e;
-                            if (kWide) {
-                                e[0] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j], c, nm));
-                                e[1] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j + 1], c, nm));
-                            } else {
-                                e[0] = exp2f_fast(S[qb][kb][8 * b + 2 * j]);
-                                e[1] = exp2f_fast(S[qb][kb][8 * b + 2 * j + 1]);
-                            }
+                            e[0] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j], c, nm));
+                            e[1] = exp2f_fast(fmaf(S[qb][kb][8 * b + 2 * j + 1], c, nm));
                             pk[j] = __builtin_bit_cast(uint32_t,
                                                        __builtin_convertvector(e, f16x2));
                             if (kTeach) {
