@@ -31,15 +31,15 @@ __device__ __forceinline__ int full_head(const int32_t* buckets, int H, int slot
 constexpr int kLdsRow = 72;   // bf16 LDS row stride (144 B: 16-B aligned, bank-staggered)
 
 // ------------------------------------------------------------------------
-// K5a, K5b: the scale of each FULL head's packed values.  The attention
+// K5a: the scale of each FULL head's packed values.  The attention
 // kernels multiply fp16 weights with fp16 values; the gather stores
 // V_h 2^-e_h, with e_h chosen so that the head's largest |v| lies in
 // [2^14, 2^15), and the kernels multiply O by 2^e_h at the end (both scalings
 // exact).  Every bf16 value then fits fp16's range; values more than 2^29
 // below the head's largest land in fp16's subnormals (absolute error at most
 // 2^-40 of that largest value).
-// K5a: per (group of kVmaxTiles key tiles, FULL slot), max |v|;
-// K5b: per FULL slot, the maximum of those and vsc[slot] = (2^-e_h, 2^e_h).
+// K5a: per (group of kVmaxTiles key tiles, FULL slot), max |v|; the gather
+// (K5) reduces those per slot and records vsc[slot] = (2^-e_h, 2^e_h).
 // ------------------------------------------------------------------------
 constexpr int kVmaxTiles = 16;
 
@@ -80,25 +80,14 @@ __global__ __launch_bounds__(256) void k_vmax_partial(const bf16* __restrict__ V
     if (threadIdx.x == 0) vpart[(int64_t)slot * gridDim.x + blockIdx.x] = m;
 }
 
-__global__ __launch_bounds__(256) void k_vscale(const float* __restrict__ vpart, int nparts,
-                                                const int32_t* __restrict__ buckets, int H,
-                                                float* __restrict__ vsc) {
-    const int slot = blockIdx.x;
-    if (slot >= full_count(buckets, H)) return;
-    float m = 0.f;
-    for (int i = threadIdx.x; i < nparts; i += 256) m = fmaxf(m, vpart[(int64_t)slot * nparts + i]);
-    __shared__ float red[4];
-    m = block_max256(m, red);
-    if (threadIdx.x == 0) {
-        // An all-zero head keeps scale 1; an infinite value (NaN never wins
-        // fmaxf) keeps scale 1 too and reaches the output as it would in
-        // exact arithmetic.
-        int e = 0;
-        if (m > 0.f && m <= 3.4028235e38f) e = ilogbf(m) - 14;
-        e = e < -126 ? -126 : (e > 126 ? 126 : e);
-        vsc[2 * slot] = ldexpf(1.f, -e);
-        vsc[2 * slot + 1] = ldexpf(1.f, e);
-    }
+// Exponent e_h of the head's V scale 2^-e_h from its largest |v| (so that
+// max |v| 2^-e_h lies in [2^14, 2^15)).  An all-zero head keeps scale 1; an
+// infinite value (NaN never wins fmaxf) keeps scale 1 too and reaches the
+// output as it would in exact arithmetic.
+__device__ __forceinline__ int vscale_exponent(float m) {
+    int e = 0;
+    if (m > 0.f && m <= 3.4028235e38f) e = ilogbf(m) - 14;
+    return e < -126 ? -126 : (e > 126 ? 126 : e);
 }
 
 // ------------------------------------------------------------------------
@@ -114,7 +103,8 @@ __global__ __launch_bounds__(256) void k_vscale(const float* __restrict__ vpart,
 __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
                                                    const bf16* __restrict__ V,
                                                    const int32_t* __restrict__ buckets, int64_t N,
-                                                   int H, int nkt, const float* __restrict__ vsc,
+                                                   int H, int nkt, const float* __restrict__ vpart,
+                                                   int nvp, float* __restrict__ vsc,
                                                    f16* __restrict__ Vt, f16* __restrict__ Kh,
                                                    float* __restrict__ kmax) {
     const int slot = blockIdx.y, tile = blockIdx.x;
@@ -124,7 +114,6 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
     if (h < 0) return;
     __shared__ __attribute__((aligned(16))) f16 s[kD * kLdsRow];
     __shared__ float s_norm[4];
-    const float down = vsc[2 * slot];
     const int t = threadIdx.x;
     const int key = t >> 2, dseg = (t & 3) * 16;
     const int64_t row = (int64_t)tile * kBK + key;
@@ -133,6 +122,19 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
     bf16x8 a = load_bf16x8(V + off), b = load_bf16x8(V + off + 8);
     bf16x8 ka = load_bf16x8(K + off), kb = load_bf16x8(K + off + 8);
     if (!ok) a = b = ka = kb = zero_bf16x8();
+    // The head's V scale from the partial maxima (every workgroup of the
+    // head reduces the same values in the same order; the tile-0 one
+    // records the scale and its inverse for the attention kernels).
+    float vm = 0.f;
+    for (int i = t; i < nvp; i += 256) vm = fmaxf(vm, vpart[(int64_t)slot * nvp + i]);
+    vm = block_max256(vm, s_norm);
+    const int e = vscale_exponent(vm);
+    const float down = ldexpf(1.f, -e);
+    if (tile == 0 && t == 0) {
+        vsc[2 * slot] = down;
+        vsc[2 * slot + 1] = ldexpf(1.f, e);
+    }
+    __syncthreads();   // s_norm is reused below
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         s[(dseg + j) * kLdsRow + key] = (f16)(bf16_to_f32(a[j]) * down);
@@ -1385,11 +1387,9 @@ void launch_gather(const AttnArgs& a, hipStream_t st) {
     const int nvp = (int)flash_vmax_parts(a.N);
     hipLaunchKernelGGL(k_vmax_partial, dim3(nvp, a.H), dim3(256), 0, st, (const bf16*)a.V,
                        a.buckets, a.N, a.H, a.vpart);
-    hipLaunchKernelGGL(k_vscale, dim3(a.H), dim3(256), 0, st, (const float*)a.vpart, nvp,
-                       a.buckets, a.H, a.vsc);
     hipLaunchKernelGGL(k_gather_vt, dim3(nkt, a.H), dim3(256), 0, st, (const bf16*)a.K,
-                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (const float*)a.vsc,
-                       (f16*)a.vt, (f16*)a.kh, a.kmax);
+                       (const bf16*)a.V, a.buckets, a.N, a.H, nkt, (const float*)a.vpart, nvp,
+                       a.vsc, (f16*)a.vt, (f16*)a.kh, a.kmax);
 }
 
 void launch_flash(const AttnArgs& a, hipStream_t st) {
