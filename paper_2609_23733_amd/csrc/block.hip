@@ -200,9 +200,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     }
 }
 
-// B2a (W_O and FFN projections, T >= 256): persistent, one workgroup of 4
-// waves per CU, each wave a
-// 128 x 128 block of the tile with its 256 accumulators in AGPRs.  Workgroup b
+// B2a (W_O and FFN 2 projections, T >= 256): persistent, one workgroup of 4
+// waves per CU, each wave a 128 x 128 block of the tile with its 256
+// accumulators in AGPRs.  Workgroup b
 // takes tiles i G + slot(b), slot grouping the workgroups of an XCD, so the 32
 // tiles an XCD runs at once are 8 token tiles x 4 feature tiles.  A partial
 // last token tile reads rows T - 256 .. T - 1 (every read in bounds) and
@@ -235,9 +235,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
     __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
     __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
 
-    // All of a token tile's feature tiles in one group (FFN 1: 16, so an XCD's
-    // 32 tiles are 2 token tiles x 16 feature tiles; 3 % faster than groups
-    // of 4 there, and 2.6 % on QKV in B2b).
+    // All of a token tile's feature tiles in one group (with FFN 1 on this
+    // kernel, 16 feature tiles, so that an XCD's 32 tiles were 2 token tiles
+    // x 16 feature tiles, were 3 % faster than groups of 4; 2.6 % on QKV in
+    // B2b).
     auto tile_of = [&](int i, int& f0, int64_t& t0, int64_t& tl) {
         gemm_tile(i * G + slot, ntt, nft, f0, t0);
         tl = t0 + kGN <= g.T ? t0 : g.T - kGN;
@@ -363,7 +364,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
 // copy through registers one stage ahead, token rows past T reading row T - 1
 // (their outputs are never stored).  Used for the QKV projection, whose
 // rotary epilogue (16 sincos per token) the second wave on each SIMD helps
-// to hide (3-8 % faster than B2a at S = 100), and for T < 256.
+// to hide (3-8 % faster than B2a at S = 100), for FFN 1, whose GELU epilogue
+// it hides likewise (output stage 1 % faster), and for T < 256.
 template <int EPI>
 __global__ __launch_bounds__(512, 1) void k_gemm_w8(GemmArgs g) {
     const int nft = g.F / kGM;
@@ -439,7 +441,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_w8(GemmArgs g) {
 template <int EPI>
 static void gemm_launch(const GemmArgs& a, hipStream_t st) {
     const int total = (a.F / kGM) * (int)((a.T + kGN - 1) / kGN);
-    if constexpr (EPI != EPI_QKV) {
+    if constexpr (EPI == EPI_RESID) {
         if (a.T >= kGN) {
             hipLaunchKernelGGL(k_gemm<EPI>, dim3(total < kGemmWG ? total : kGemmWG), dim3(256), 0,
                                st, a);
