@@ -123,11 +123,20 @@ def stage_bytes(N, n_full, n_surr, n_mean, b_in, b_out):
             "linear": float(N) * D * (n_surr * (b_in + b_out) + n_mean * b_out)}
 
 
-def run_workload(S, n_full, steps, warmup, seed_key, dtype="bf16", sharp=False):
+WIDE_QK_SCALE = 1.3   # sharp Q and K scaled by this: item bounds near 30 log2 units
+
+
+def run_workload(S, n_full, steps, warmup, seed_key, dtype="bf16", sharp=False, wide=False):
+    """One layer configuration; `wide` scales the sharp Q and K so that every
+    FULL work item's logit bound exceeds the zero-reference window (running
+    reference points throughout the FULL stage)."""
     import torch
     from paper_2609_23733_amd import synth, vp
     x = synth.make_layer(S, P_TOKENS, dtype=dtype, n_full=n_full, key=seed_key,
-                         qkv_device="cuda", sharp=sharp)
+                         qkv_device="cuda", sharp=sharp or wide)
+    if wide:
+        x.Q = (x.Q.float() * WIDE_QK_SCALE).to(x.Q.dtype)
+        x.K = (x.K.float() * WIDE_QK_SCALE).to(x.K.dtype)
     ydt = torch.bfloat16 if dtype == "bf16" else torch.float32
     layer = vp.RoutedLayer(x, y_dtype=ydt)
     ms_step, stage = measure(layer, steps, warmup)
@@ -144,7 +153,9 @@ def run_workload(S, n_full, steps, warmup, seed_key, dtype="bf16", sharp=False):
     byt = stage_bytes(N, counts[2], counts[1], counts[0], b_in, b_out)
     gbs = {k: round(v / stage[k] / 1e6, 1) for k, v in byt.items() if v and stage[k] > 0}
     full_ms = stage["full"]
-    rec = dict(S=S, N=N, dtype=dtype, inputs="sharp N(0,1) Q/K" if sharp else "N(0,1/64)",
+    inputs = ("sharp N(0,1) Q/K x%g" % WIDE_QK_SCALE if wide else
+              "sharp N(0,1) Q/K" if sharp else "N(0,1/64)")
+    rec = dict(S=S, N=N, dtype=dtype, inputs=inputs,
                n_full=counts[2], n_surr=counts[1], n_mean=counts[0],
                ms=round(ms_step, 4), tflops=round(fl / ms_step / 1e9, 2),
                frac_peak=round(fl / ms_step / 1e9 / peak, 4),
@@ -539,7 +550,7 @@ def main():
                     help="skip the 24-layer routed stack at S=500")
     ap.add_argument("--stack", type=int, default=0, metavar="S",
                     help="also time a 24-block stack at S views (e.g. 500)")
-    ap.add_argument("--workload", default=None, metavar="S,NFULL[,sharp|f32]",
+    ap.add_argument("--workload", default=None, metavar="S,NFULL[,sharp|wide|f32]",
                     help="time only this workload and print its record (for profiling runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the "
@@ -565,9 +576,11 @@ def main():
     if args.workload:
         f = args.workload.split(",")
         S, nf = int(f[0]), int(f[1])
-        sharp, dt = "sharp" in f[2:], ("f32" if "f32" in f[2:] else "bf16")
-        rec, _, _ = run_workload(S, nf, args.steps, args.warmup, (S, 3 if sharp else 0),
-                                 dtype=dt, sharp=sharp)
+        sharp, wide = "sharp" in f[2:], "wide" in f[2:]
+        dt = "f32" if "f32" in f[2:] else "bf16"
+        rec, _, _ = run_workload(S, nf, args.steps, args.warmup,
+                                 (S, 3 if sharp or wide else 0), dtype=dt, sharp=sharp,
+                                 wide=wide)
         print(json.dumps(rec))
         return
 
@@ -601,14 +614,16 @@ def main():
     if not args.no_sweep:
         # S = 2 in fp32 (the fp32 FULL kernel against the fp32 matrix peak), the
         # other view counts and FULL-head counts, and S = 100 with sharp FULL
-        # heads (logit bounds past the zero-reference window: the running-
-        # reference-point path carries the FULL stage).
-        sweep = ((2, 8, "f32", False), (8, 8, "bf16", False), (32, 4, "bf16", False),
-                 (32, 16, "bf16", False), (100, 2, "bf16", False), (100, 8, "bf16", False),
-                 (100, 16, "bf16", False), (500, 4, "bf16", False), (100, 4, "bf16", True))
-        for S, nf, dt, sharp in sweep:
-            r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 3 if sharp else 0),
-                                     dtype=dt, sharp=sharp)
+        # heads (logit bounds past the zero-reference window: EXT items, whose
+        # reference point moves only on fp16 overflow) and with sharper ones
+        # (bounds past the EXT window too: WIDE items, running reference points).
+        sweep = ((2, 8, "f32", ""), (8, 8, "bf16", ""), (32, 4, "bf16", ""),
+                 (32, 16, "bf16", ""), (100, 2, "bf16", ""), (100, 8, "bf16", ""),
+                 (100, 16, "bf16", ""), (500, 4, "bf16", ""), (100, 4, "bf16", "sharp"),
+                 (100, 4, "bf16", "wide"))
+        for S, nf, dt, kind in sweep:
+            r, lyr, _ = run_workload(S, nf, args.steps, args.warmup, (S, 3 if kind else 0),
+                                     dtype=dt, sharp=kind == "sharp", wide=kind == "wide")
             by.append(r)
             del lyr
             torch.cuda.empty_cache()

@@ -386,6 +386,29 @@ def test_full_size_sharp(S, y_bf16):
     check_y(Yg, ref["Y"], "bf16", y_bf16, label="sharp S=%d" % S)
 
 
+def test_full_size_wide():
+    """S = 32 with sharp Q and K scaled by 1.3: every FULL work item's bound
+    (about 30 log2 units) exceeds the window of the zero-reference modes, so
+    the whole FULL stage runs with running reference points (WIDE items);
+    fp32 Y at the strict bar on 128 sampled rows, the last one among them."""
+    S = 32
+    log("full size wide S=%d" % S)
+    x = synth.make_layer(S, dtype="bf16", n_full=4, key=(S, 6), sharp=True, qkv_device="cuda")
+    x.Q = (x.Q.float() * 1.3).to(torch.bfloat16)
+    x.K = (x.K.float() * 1.3).to(torch.bfloat16)
+    b = item_bounds(x)
+    assert (b > EXT_BOUND).all(), b.min()
+    layer = run_gpu(x, y_dtype=torch.float32)
+    rows = synth.sample_rows(x.N, 128, synth.derive_seed(S, 6, 20))
+    ref = oracle_layer(x, rows=rows, full_rows_sel=rows)
+    check_router(layer, ref, oracle.RULE_ARGMAX)
+    Yg = layer.Y[torch.from_numpy(rows).cuda()].double().cpu().numpy()
+    for h in range(16):
+        if ref["modes"][h] == 2:
+            ref["Y"][:, h, :] = ref["Y_full_rows"][h]
+    check_y(Yg, ref["Y"], "bf16", False, label="wide S=%d" % S)
+
+
 def test_element_offsets_past_2_32():
     """N = 3053 x 1374 = 4,194,822 tokens: element offsets token * 1024 + 64 h
     + i pass 2^32 from token 2^22 on.  The last head runs FULL (the largest
@@ -474,7 +497,7 @@ def item_bounds(x):
 
 
 def test_zero_reference_overflow_moves():
-    """Logit bounds between 14 and 24 (zero reference point kept while the
+    """Logit bounds between 10 and 24 (zero reference point kept while the
     weights fit fp16), with one key per FULL head planted in tile 5 along
     that head's largest query, 20 log2 units above 0: that query's weights
     overflow fp16 mid-sequence and its reference point moves there."""
