@@ -181,8 +181,8 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 //
 // Softmax is invariant to the reference point subtracted from the logits
 // before exponentiation.  A work item (512 queries of one head) runs in one
-// of two modes, chosen from Cauchy-Schwarz bounds (|q . k| <= |q| max_j |k_j|)
-// before its first tile:
+// of three modes, chosen from Cauchy-Schwarz bounds (|q . k| <= |q| max_j
+// |k_j|) before its first tile:
 //  - FAST: every logit of the item lies within +-kFastBound in log2 units.
 //    The scale c = log2(e) / sqrt(d) is folded into Q (rounded to fp16,
 //    relative error 2^-11), S comes out of the MFMA in log2 units and the
@@ -207,6 +207,9 @@ __global__ __launch_bounds__(256) void k_gather_vt(const bf16* __restrict__ K,
 //    below m + kSlack, by its largest key norm, is exponentiated against m
 //    directly; otherwise the tile maximum is taken and m moves when the tile
 //    exceeds m + kSlack.)
+// In EXT and WIDE modes one wave-wide vote per tile, after both of a wave's
+// 32-query blocks are packed and summed, decides whether any of them
+// overflowed.
 // Row sums: the packed fp16 weights of a lane's 32 keys per tile are added
 // as a tree of packed fp16 adds (at most 32 weights of at most 2^10: no
 // overflow; relative error at most 5 * 2^-11), then into l in fp32.  The
