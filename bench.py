@@ -35,7 +35,7 @@ HEADS, D, L = 16, 64, 64
 # = 524305 KiB for 1 GiB read (x2.0) and WRITE_SIZE = 1048576 KiB for 1 GiB
 # written (x1.0).  Valid only for the kernel source it was measured on.
 FLASH_TRAFFIC = {
-    "source_sha256": "70b04b7536e5e299a925946f725f8a85c4d249f82dc319b971e22b2c891a8a08",
+    "source_sha256": "f98be6b14a04ba6c40fa84e0c8dce862feb05c74357ab2f902ba95c9f40c2df7",
     "S": 100, "n_full": 4,
     "fetch_kib": 1545636, "write_kib": 122449,
     "copy_fetch_kib": 524305, "copy_write_kib": 1048576, "copy_bytes": 1 << 30,

@@ -223,7 +223,9 @@ vp_status vp_routed_global_attention(const vp_shape *shape, const void *Q, const
  *                           every 64-key tile;
  *   vp_full_head_attention: exact softmax attention of every FULL head
  *                           (Algorithm 1, first branch); reads the packed
- *                           tiles the gather left in `ws`.  Results are
+ *                           tiles the gather left in `ws` (bf16) and keeps
+ *                           the partial results of work split over compute
+ *                           units there (both dtypes).  Results are
  *                           deterministic for a given device (the split of
  *                           work over its compute units is fixed);
  *   vp_linear_heads:        SURR (Eq.5-7, or surr->variant) and MEAN heads.

@@ -1225,22 +1225,31 @@ __global__ __launch_bounds__(256, 2) void k_flash_bf16_wide(const bf16* __restri
 // K6 (fp32): one workgroup = 4 waves x 32 queries; 32x32x2 fp32 MFMA.  S^T
 // output register r of lane-half hh holds key 8 (r / 4) + 4 hh + (r % 4) of
 // its 32-key block; the PV MFMA consumes one register per step, reading the
-// matching V row from LDS.
+// matching V row from LDS.  Small layers (few work items for the chip) split
+// each item's key tiles into two halves run by separate workgroups; each
+// half writes O (unnormalized, relative to its reference point m), l and m
+// per query, and K6d combines the two halves in order.
 // ------------------------------------------------------------------------
 constexpr int kBQ32 = 128;
 constexpr int kKRow32 = 65;   // odd stride: column reads are bank-conflict free
+constexpr int kRec32 = kD + 4;   // split record: O[64], l, m, 2 pad (16-byte aligned)
 
 __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ Q,
                                                       const float* __restrict__ K,
                                                       const float* __restrict__ V,
                                                       const int32_t* __restrict__ buckets,
                                                       int64_t N, int H, int nqt, int nkt, float c,
+                                                      int splits, float* __restrict__ part,
                                                       void* __restrict__ Y, int ydt) {
     const int nfull = full_count(buckets, H);
     const int active = nfull * nqt;
-    if ((int)blockIdx.x >= active) return;
-    const int L = xcd_remap(blockIdx.x, active);
+    if ((int)blockIdx.x >= active * splits) return;
+    const int Lx = xcd_remap(blockIdx.x, active * splits);
+    const int L = Lx / splits, half = Lx - L * splits;
     const int slot = L / nqt, qt = L - slot * nqt;
+    // key tiles [t0, t1) of the item (all of them unless split)
+    const int t0 = (int)((int64_t)half * nkt / splits);
+    const int t1 = (int)((int64_t)(half + 1) * nkt / splits);
     const int h = full_head(buckets, H, slot);
     if (h < 0) return;
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -1282,13 +1291,13 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
 
     f32x16 O[2] = {zero_f32x16(), zero_f32x16()};
     float m = -INFINITY, l = 0.f;
-    gload(0);
+    gload(t0);
     lstore(0);
     __syncthreads();
 
-    for (int t = 0; t < nkt; ++t) {
-        const int buf = t & 1;
-        if (t + 1 < nkt) gload(t + 1);
+    for (int t = t0; t < t1; ++t) {
+        const int buf = (t - t0) & 1;
+        if (t + 1 < t1) gload(t + 1);
         f32x16 S[2] = {zero_f32x16(), zero_f32x16()};
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
@@ -1340,11 +1349,26 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
         for (int db = 0; db < 2; ++db)
 #pragma unroll
             for (int r = 0; r < 16; ++r) O[db][r] = fmaf(O[db][r], al, Ot[db][r]);
-        if (t + 1 < nkt) lstore(buf ^ 1);
+        if (t + 1 < t1) lstore(buf ^ 1);
         __syncthreads();
     }
 
     const float lt = l + __shfl_xor(l, 32);
+    if (splits > 1) {
+        float* pr = part + ((int64_t)(L * 2 + half) * kBQ32 + wave * 32 + n) * kRec32;
+#pragma unroll
+        for (int db = 0; db < 2; ++db)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                *reinterpret_cast<float4*>(pr + db * 32 + 8 * g + 4 * hh) =
+                    make_float4(O[db][4 * g], O[db][4 * g + 1], O[db][4 * g + 2],
+                                O[db][4 * g + 3]);
+        if (hh == 0) {
+            pr[kD] = lt;
+            pr[kD + 1] = m;
+        }
+        return;
+    }
     const float inv = 1.f / lt;
     if (qok) {
 #pragma unroll
@@ -1366,6 +1390,57 @@ __global__ __launch_bounds__(256, 2) void k_flash_f32(const float* __restrict__ 
     }
 }
 
+// K6d: Y of the fp32 items that K6 split into two key halves: the halves' O
+// and l scaled to the larger reference point and added (half 0, then half
+// 1), then O / l.  Two workgroups of 256 threads per item, 4 threads per
+// query and 16 of its values each.
+__global__ __launch_bounds__(256) void k_flash_f32_combine(const int32_t* __restrict__ buckets,
+                                                           int64_t N, int H, int nqt,
+                                                           const float* __restrict__ part,
+                                                           void* __restrict__ Y, int ydt) {
+    const int nfull = full_count(buckets, H);
+    const int L = blockIdx.x >> 1;
+    if (L >= nfull * nqt) return;
+    const int slot = L / nqt, qt = L - slot * nqt;
+    const int h = full_head(buckets, H, slot);
+    if (h < 0) return;
+    const int qr = (blockIdx.x & 1) * 64 + (threadIdx.x >> 2), d0 = (threadIdx.x & 3) * 16;
+    const int64_t qi = (int64_t)qt * kBQ32 + qr;
+    if (qi >= N) return;
+    const float* r0 = part + ((int64_t)(L * 2) * kBQ32 + qr) * kRec32;
+    const float* r1 = r0 + (int64_t)kBQ32 * kRec32;
+    const float m0 = r0[kD + 1], m1 = r1[kD + 1];
+    const float mt = fmaxf(m0, m1);
+    const float w0 = exp2f_fast(m0 - mt), w1 = exp2f_fast(m1 - mt);
+    const float inv = 1.f / fmaf(r1[kD], w1, r0[kD] * w0);
+    float y[16];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const float4 a = *reinterpret_cast<const float4*>(r0 + d0 + 4 * k);
+        const float4 b = *reinterpret_cast<const float4*>(r1 + d0 + 4 * k);
+        y[4 * k] = fmaf(b.x, w1, a.x * w0) * inv;
+        y[4 * k + 1] = fmaf(b.y, w1, a.y * w0) * inv;
+        y[4 * k + 2] = fmaf(b.z, w1, a.z * w0) * inv;
+        y[4 * k + 3] = fmaf(b.w, w1, a.w * w0) * inv;
+    }
+    const int64_t yo = (qi * H + h) * kD + d0;
+    if (ydt == DT_BF16) {
+#pragma unroll
+        for (int k8 = 0; k8 < 2; ++k8) {
+            bf16x8 o;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) o[k] = (bf16)y[8 * k8 + k];
+            *reinterpret_cast<bf16x8*>(reinterpret_cast<bf16*>(Y) + yo + 8 * k8) = o;
+        }
+    } else {
+        float* yp = reinterpret_cast<float*>(Y) + yo;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            *reinterpret_cast<float4*>(yp + 4 * k) =
+                make_float4(y[4 * k], y[4 * k + 1], y[4 * k + 2], y[4 * k + 3]);
+    }
+}
+
 // ------------------------------------------------------------------ launchers
 
 int flash_q_tile(int dtype) { return dtype == DT_BF16 ? kBQ16 : kBQ32; }
@@ -1378,6 +1453,19 @@ int flash_stream_groups(int64_t N, int H) {
 
 size_t flash_part_bytes(int64_t N, int H) {
     return (size_t)2 * flash_stream_groups(N, H) * kPartFloats * sizeof(float);
+}
+
+// fp32 layers: two key halves per work item while the items alone would
+// leave the chip short of waves (at most 2 workgroups per CU of them), and
+// the workspace for the halves' records.
+int flash_f32_splits(int64_t N, int H) {
+    const int64_t nqt = (N + kBQ32 - 1) / kBQ32, nkt = (N + kBK - 1) / kBK;
+    return nqt * H <= 2 * kStreamWG && nkt >= 2 ? 2 : 1;
+}
+size_t flash_f32_part_bytes(int64_t N, int H) {
+    if (flash_f32_splits(N, H) == 1) return 0;
+    const int64_t nqt = (N + kBQ32 - 1) / kBQ32;
+    return (size_t)H * nqt * 2 * kBQ32 * kRec32 * sizeof(float);
 }
 
 int64_t flash_vmax_parts(int64_t N) {
@@ -1415,10 +1503,15 @@ void launch_flash(const AttnArgs& a, hipStream_t st) {
                            dim3(nqt * a.H), dim3(256), 0, st, (const bf16*)a.Q, (const bf16*)a.K,
                            (const f16*)a.vt, (const float*)a.kmax, (const float*)a.vsc, a.buckets,
                            a.N, a.H, nqt, nkt, c, a.qflag, nqf, a.Y, a.ydt, a.off);
-    } else
-        hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H), dim3(256), 0, st, (const float*)a.Q,
-                           (const float*)a.K, (const float*)a.V, a.buckets, a.N, a.H, nqt, nkt,
-                           c, a.Y, a.ydt);
+    } else {
+        const int splits = flash_f32_splits(a.N, a.H);
+        hipLaunchKernelGGL(k_flash_f32, dim3(nqt * a.H * splits), dim3(256), 0, st,
+                           (const float*)a.Q, (const float*)a.K, (const float*)a.V, a.buckets,
+                           a.N, a.H, nqt, nkt, c, splits, a.part, a.Y, a.ydt);
+        if (splits > 1)
+            hipLaunchKernelGGL(k_flash_f32_combine, dim3(nqt * a.H * 2), dim3(256), 0, st,
+                               a.buckets, a.N, a.H, nqt, (const float*)a.part, a.Y, a.ydt);
+    }
 }
 
 }  // namespace vp

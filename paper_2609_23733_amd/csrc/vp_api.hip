@@ -72,7 +72,8 @@ bool make_layout(const vp_shape* s, Layout* L) {
     if (s->dtype == VP_BF16)
         off = align_up(off + (size_t)s->H * cdiv(N, vp::flash_q_tile(VP_BF16)) * sizeof(int32_t));
     L->off_fpart = off;
-    if (s->dtype == VP_BF16) off = align_up(off + vp::flash_part_bytes(N, (int)s->H));
+    off = align_up(off + (s->dtype == VP_BF16 ? vp::flash_part_bytes(N, (int)s->H)
+                                              : vp::flash_f32_part_bytes(N, (int)s->H)));
     L->off_lpart = off;
     off = align_up(off + (size_t)L->n3 * s->H * vp::kLinSums * sizeof(float));
     L->off_lsum = off;

@@ -160,6 +160,8 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st);
 int flash_q_tile(int dtype);
 int flash_stream_groups(int64_t N, int H);
 size_t flash_part_bytes(int64_t N, int H);
+int flash_f32_splits(int64_t N, int H);
+size_t flash_f32_part_bytes(int64_t N, int H);
 int64_t flash_vmax_parts(int64_t N);
 
 }  // namespace vp
