@@ -21,48 +21,84 @@ constexpr int kDm = 1024;   // model width D = 16 heads x 64
 // B1: LayerNorm over the D = 1024 features of each row of X (+ X2 when given,
 // added in fp32): mean and biased variance in fp32 (two passes over
 // registers), y = (x - mean) r g + b, r = 1 / sqrt(var + eps), rounded to
-// bf16.  One wave per row; lane l holds features 16 l ... 16 l + 15.
+// bf16.  One wave per kLnRows consecutive rows, g and b held in registers;
+// lane l holds features 8 l ... 8 l + 7 and 512 + 8 l ... 512 + 8 l + 7, so
+// each 16-byte load or store of a wave covers 1 KB of the row contiguously.
+// The next row's loads are issued before the current row is normalised.
 // ------------------------------------------------------------------------
+constexpr int kLnRows = 2;
+
+template <bool kAdd>
 __global__ __launch_bounds__(256) void k_layernorm(const bf16* __restrict__ X,
                                                    const bf16* __restrict__ X2, int64_t T,
                                                    const float* __restrict__ g,
                                                    const float* __restrict__ b, float eps,
                                                    bf16* __restrict__ Y) {
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= T) return;
-    const int lane = threadIdx.x & 63, c0 = 16 * lane;
-    const bf16* xr = X + row * kDm + c0;
-    const bf16x8 a = load_bf16x8(xr), bb = load_bf16x8(xr + 8);
-    float x[16];
+    const int64_t row0 =
+        ((int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6)) * kLnRows;
+    if (row0 >= T) return;
+    const int lane = threadIdx.x & 63, c0 = 8 * lane, c1 = kDm / 2 + 8 * lane;
+    float gg[16], bv[16];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-        x[j] = bf16_to_f32(a[j]);
-        x[8 + j] = bf16_to_f32(bb[j]);
+        gg[j] = g[c0 + j];
+        gg[8 + j] = g[c1 + j];
+        bv[j] = b[c0 + j];
+        bv[8 + j] = b[c1 + j];
     }
-    if (X2) {
-        const bf16* x2 = X2 + row * kDm + c0;
-        const bf16x8 a2 = load_bf16x8(x2), b2 = load_bf16x8(x2 + 8);
+    const int nr = T - row0 < kLnRows ? (int)(T - row0) : kLnRows;
+    constexpr int kV = kAdd ? 4 : 2;
+    auto load = [&](int64_t row, bf16x8 (&v)[kV]) {
+        const bf16* xr = X + row * kDm;
+        v[0] = load_bf16x8(xr + c0);
+        v[1] = load_bf16x8(xr + c1);
+        if constexpr (kAdd) {
+            const bf16* x2 = X2 + row * kDm;
+            v[2] = load_bf16x8(x2 + c0);
+            v[3] = load_bf16x8(x2 + c1);
+        }
+    };
+    auto norm = [&](int64_t row, const bf16x8 (&v)[kV]) {
+        float x[16];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            x[j] += bf16_to_f32(a2[j]);
-            x[8 + j] += bf16_to_f32(b2[j]);
+            x[j] = bf16_to_f32(v[0][j]);
+            x[8 + j] = bf16_to_f32(v[1][j]);
+            if constexpr (kAdd) {
+                x[j] += bf16_to_f32(v[2][j]);
+                x[8 + j] += bf16_to_f32(v[3][j]);
+            }
         }
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s += x[j];
+        const float mean = wave_sum(s) * (1.f / kDm);
+        float q = 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) q = fmaf(x[j] - mean, x[j] - mean, q);
+        const float r = rsqrtf(wave_sum(q) * (1.f / kDm) + eps);
+        float y[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) y[j] = fmaf((x[j] - mean) * r, gg[j], bv[j]);
+        bf16* yr = Y + row * kDm;
+        *reinterpret_cast<bf16x8*>(yr + c0) =
+            pack_bf16x8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]);
+        *reinterpret_cast<bf16x8*>(yr + c1) =
+            pack_bf16x8(y[8], y[9], y[10], y[11], y[12], y[13], y[14], y[15]);
+    };
+    // Straight-line over kLnRows rows with two register sets, each row's loads
+    // issued one row ahead of its use.  Rows past the last are the last row
+    // again (the same values stored twice; Y never aliases X or X2), so no
+    // branch sits around the loads and each wait covers only the row in use.
+    auto rowi = [&](int i) { return row0 + (i < nr ? i : nr - 1); };
+    bf16x8 v[2][kV];
+    load(rowi(0), v[0]);
+#pragma unroll
+    for (int i = 0; i < kLnRows; ++i) {
+        if (i + 1 < kLnRows) load(rowi(i + 1), v[(i + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch ahead of the row's arithmetic
+        norm(rowi(i), v[i & 1]);
     }
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) s += x[j];
-    const float mean = wave_sum(s) * (1.f / kDm);
-    float q = 0.f;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) q = fmaf(x[j] - mean, x[j] - mean, q);
-    const float r = rsqrtf(wave_sum(q) * (1.f / kDm) + eps);
-    float y[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) y[j] = fmaf((x[j] - mean) * r, g[c0 + j], b[c0 + j]);
-    bf16* yr = Y + row * kDm + c0;
-    *reinterpret_cast<bf16x8*>(yr) = pack_bf16x8(y[0], y[1], y[2], y[3], y[4], y[5], y[6], y[7]);
-    *reinterpret_cast<bf16x8*>(yr + 8) =
-        pack_bf16x8(y[8], y[9], y[10], y[11], y[12], y[13], y[14], y[15]);
 }
 
 // ------------------------------------------------------------------------
@@ -465,8 +501,11 @@ static void gemm(int epi, const GemmArgs& a, hipStream_t st) {
 
 static void layernorm(const bf16* X, const bf16* X2, int64_t T, const float* g, const float* b,
                       float eps, bf16* Y, hipStream_t st) {
-    hipLaunchKernelGGL(k_layernorm, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, st, X, X2, T, g,
-                       b, eps, Y);
+    const dim3 grid((unsigned)((T + 4 * kLnRows - 1) / (4 * kLnRows)));
+    if (X2)
+        hipLaunchKernelGGL(k_layernorm<true>, grid, dim3(256), 0, st, X, X2, T, g, b, eps, Y);
+    else
+        hipLaunchKernelGGL(k_layernorm<false>, grid, dim3(256), 0, st, X, X2, T, g, b, eps, Y);
 }
 
 void launch_block_qkv(const BlockArgs& a, hipStream_t st) {
