@@ -119,7 +119,9 @@ __global__ __launch_bounds__(256) void k_layernorm(const bf16* __restrict__ X,
 constexpr int kGM = 256, kGN = 256, kGK = 64, kGRow = 72;
 constexpr int kGemmWG = 256;   // persistent workgroups: one per CU
 
-enum { EPI_QKV = 0, EPI_GELU = 1, EPI_RESID = 2 };
+// EPI_RESID: ls (acc + bias) + res + res2, either residual may be null;
+// EPI_RESID2: the same with both residuals given.
+enum { EPI_QKV = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_RESID2 = 3 };
 
 struct GemmArgs {
     const bf16* W;        // [F, Kd]
@@ -127,9 +129,9 @@ struct GemmArgs {
     const float* bias;    // [F]
     int64_t T;
     int F, Kd;
-    bf16* out;            // GELU: [T, F]; RESID: [T, F]
-    const bf16 *res, *res2;   // RESID: residuals [T, F] (either may be null)
-    const float* ls;      // RESID: LayerScale [F]
+    bf16* out;            // GELU, RESID, RESID2: [T, F]
+    const bf16 *res, *res2;   // RESID: residuals [T, F] (either may be null); RESID2: both
+    const float* ls;      // RESID, RESID2: LayerScale [F]
     bf16 *q, *k, *v;      // QKV: [T, D] each
     const int32_t* pos;   // QKV: [T, 2] (row, column)
     float log2_base;      // QKV: log2 of the rotary base
@@ -204,6 +206,26 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
                 if (EPI == EPI_GELU) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) v[r] = gelu(v[r]);
+                } else if (EPI == EPI_RESID2) {   // ls (acc + bias) + res + res2, in fp32
+                    // Both residuals are read with no branch around the loads,
+                    // so the reads of the four feature groups are in flight
+                    // together (a null test per read waits for each one).
+                    float base[16];
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        const int f = fbase + 8 * gq + 4 * hh;
+                        const bf16x4 r1 = *reinterpret_cast<const bf16x4*>(g.res + t * g.F + f);
+                        const bf16x4 r2 = *reinterpret_cast<const bf16x4*>(g.res2 + t * g.F + f);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) base[4 * gq + i] = (float)r1[i] + (float)r2[i];
+                    }
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        const int f = fbase + 8 * gq + 4 * hh;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            v[4 * gq + i] = fmaf(g.ls[f + i], v[4 * gq + i], base[4 * gq + i]);
+                    }
                 } else {   // ls (acc + bias) + res + res2, summed in fp32
 #pragma unroll
                     for (int gq = 0; gq < 4; ++gq) {
@@ -477,7 +499,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_w8(GemmArgs g) {
 template <int EPI>
 static void gemm_launch(const GemmArgs& a, hipStream_t st) {
     const int total = (a.F / kGM) * (int)((a.T + kGN - 1) / kGN);
-    if constexpr (EPI == EPI_RESID) {
+    if constexpr (EPI == EPI_RESID || EPI == EPI_RESID2) {
         if (a.T >= kGN) {
             hipLaunchKernelGGL(k_gemm<EPI>, dim3(total < kGemmWG ? total : kGemmWG), dim3(256), 0,
                                st, a);
@@ -495,6 +517,8 @@ static void gemm(int epi, const GemmArgs& a, hipStream_t st) {
         gemm_launch<EPI_QKV>(a, st);
     else if (epi == EPI_GELU)
         gemm_launch<EPI_GELU>(a, st);
+    else if (epi == EPI_RESID2 && a.res && a.res2)
+        gemm_launch<EPI_RESID2>(a, st);
     else
         gemm_launch<EPI_RESID>(a, st);
 }
@@ -530,7 +554,7 @@ void launch_block_out(const BlockArgs& a, hipStream_t st) {
     // X_out = X + A + LS_2 (H W_fc2^T + b_fc2)
     g.W = a.w_fc2; g.X = a.hid; g.bias = a.b_fc2; g.F = kDm; g.Kd = 4 * kDm;
     g.res = a.X; g.res2 = a.xa; g.ls = a.ls2; g.out = a.Xout;
-    gemm(EPI_RESID, g, st);
+    gemm(EPI_RESID2, g, st);
 }
 
 }  // namespace vp
