@@ -165,6 +165,18 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     // 256); Q and K are rotated, the first 32 features of each 64 by the row
     // coordinate and the next 32 by the column coordinate.
     const bool rotate = EPI == EPI_QKV && (f0 + 128 * wm) / kDm < 2;
+    // The 8-wave kernel (NTB = 2) reads the wave's 64 bias values once, with
+    // one wait, for all its tokens; the persistent kernel, whose registers are
+    // full, reads them per 32 x 32 block.
+    constexpr bool kHoist = NTB == 2;
+    float bias[4][16];
+    if constexpr (kHoist) {
+#pragma unroll
+        for (int fb = 0; fb < 4; ++fb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                bias[fb][r] = g.bias[f0 + 128 * wm + 32 * fb + 8 * (r >> 2) + 4 * hh + (r & 3)];
+    }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
         const int64_t t = tl + tok0 + 32 * tb + n;
@@ -186,7 +198,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
             float v[16];
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                v[r] = acc[fb][tb][r] + g.bias[fbase + 8 * (r >> 2) + 4 * hh + (r & 3)];
+                v[r] = acc[fb][tb][r] +
+                       (kHoist ? bias[fb][r] : g.bias[fbase + 8 * (r >> 2) + 4 * hh + (r & 3)]);
             bf16* dst;
             if (EPI == EPI_QKV) {
                 const int which = fbase / kDm, fin = fbase - which * kDm;
