@@ -177,6 +177,21 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
             for (int r = 0; r < 16; ++r)
                 bias[fb][r] = g.bias[f0 + 128 * wm + 32 * fb + 8 * (r >> 2) + 4 * hh + (r & 3)];
     }
+    // The wave's output tensor, chosen once with a wave-uniform index (an index
+    // in vector registers made the compiler read the pointer from the
+    // argument block per 32 x 32 block and wait for it before each store).
+    const int which = EPI == EPI_QKV ? __builtin_amdgcn_readfirstlane((f0 + 128 * wm) / kDm) : 0;
+    bf16* const qkv_out = which == 0 ? g.q : (which == 1 ? g.k : g.v);
+    // Rotary positions of all the wave's tokens, read before the first is
+    // used (rows past T - 1 read row T - 1 and are not stored).
+    int2 pos[NTB];
+    if (rotate) {
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) {
+            const int64_t t = tl + tok0 + 32 * tb + n;
+            pos[tb] = *reinterpret_cast<const int2*>(g.pos + 2 * (t < g.T ? t : g.T - 1));
+        }
+    }
 #pragma unroll
     for (int tb = 0; tb < NTB; ++tb) {
         const int64_t t = tl + tok0 + 32 * tb + n;
@@ -185,7 +200,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
         // row coordinate, half 1 the column coordinate
         float rs[2][8], rc[2][8];
         if (rotate) {
-            const int2 p = *reinterpret_cast<const int2*>(g.pos + 2 * t);
+            const int2 p = pos[tb];
 #pragma unroll
             for (int r = 0; r < 8; ++r) {
                 __sincosf((float)p.x * omega[r], &rs[0][r], &rc[0][r]);
@@ -202,7 +217,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
                        (kHoist ? bias[fb][r] : g.bias[fbase + 8 * (r >> 2) + 4 * hh + (r & 3)]);
             bf16* dst;
             if (EPI == EPI_QKV) {
-                const int which = fbase / kDm, fin = fbase - which * kDm;
+                const int fin = fbase - which * kDm;
                 if (rotate) {   // Q, K: rotate the planes (j, j + 16) of this half
                     const int half = (fin & 32) ? 1 : 0;   // fb & 1
 #pragma unroll
@@ -213,7 +228,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
                         v[r + 8] = u * sn + w * cs;
                     }
                 }
-                dst = (which == 0 ? g.q : (which == 1 ? g.k : g.v)) + t * kDm + fin;
+                dst = qkv_out + t * kDm + fin;
             } else {
                 dst = g.out + t * g.F + fbase;
                 if (EPI == EPI_GELU) {
