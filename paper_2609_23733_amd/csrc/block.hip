@@ -152,7 +152,7 @@ __device__ __forceinline__ void gemm_tile(int L, int ntt, int group, int& f0, in
 template <int EPI, int NTB>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4][NTB], int f0,
                                               int64_t t0, int64_t tl, int wm, int tok0, int n,
-                                              int hh) {
+                                              int hh, const float* sbl = nullptr) {
     float omega[8];   // rotary frequencies of features j = 8 (r / 4) + 4 hh + r % 4, r < 8
     if (EPI == EPI_QKV) {
 #pragma unroll
@@ -167,7 +167,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     const bool rotate = EPI == EPI_QKV && (f0 + 128 * wm) / kDm < 2;
     // The 8-wave kernel (NTB = 2) reads the wave's 64 bias values once, with
     // one wait, for all its tokens; the persistent kernel, whose registers are
-    // full, reads them per 32 x 32 block.
+    // full, reads the tile's bias and LayerScale from LDS (sbl: 256 bias values,
+    // then 256 LayerScale values, for features f0 ...) per 32 x 32 block.
     constexpr bool kHoist = NTB == 2;
     float bias[4][16];
     if constexpr (kHoist) {
@@ -196,6 +197,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
     for (int tb = 0; tb < NTB; ++tb) {
         const int64_t t = tl + tok0 + 32 * tb + n;
         if (t < t0 || t >= g.T) continue;
+        // An offset the compiler cannot see through, so the LDS reads of
+        // bias and LayerScale stay in each block instead of being hoisted out
+        // of the token loop (128 values per lane held across it spill).
+        int lo = -f0;
+        if (sbl) asm volatile("" : "+v"(lo));
         // (sin, cos) of this token's angles, once per token: half 0 takes the
         // row coordinate, half 1 the column coordinate
         float rs[2][8], rc[2][8];
@@ -214,7 +220,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
 #pragma unroll
             for (int r = 0; r < 16; ++r)
                 v[r] = acc[fb][tb][r] +
-                       (kHoist ? bias[fb][r] : g.bias[fbase + 8 * (r >> 2) + 4 * hh + (r & 3)]);
+                       (kHoist ? bias[fb][r]
+                               : sbl ? sbl[fbase + lo + 8 * (r >> 2) + 4 * hh + (r & 3)]
+                                     : g.bias[fbase + 8 * (r >> 2) + 4 * hh + (r & 3)]);
             bf16* dst;
             if (EPI == EPI_QKV) {
                 const int fin = fbase - which * kDm;
@@ -252,7 +260,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
                         const int f = fbase + 8 * gq + 4 * hh;
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
-                            v[4 * gq + i] = fmaf(g.ls[f + i], v[4 * gq + i], base[4 * gq + i]);
+                            v[4 * gq + i] = fmaf(sbl ? sbl[kGM + f + lo + i] : g.ls[f + i],
+                                                 v[4 * gq + i], base[4 * gq + i]);
                     }
                 } else {   // ls (acc + bias) + res + res2, summed in fp32
 #pragma unroll
@@ -271,7 +280,8 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, f32x16 (&acc)[4
                         }
 #pragma unroll
                         for (int i = 0; i < 4; ++i)
-                            v[4 * gq + i] = fmaf(g.ls[f + i], v[4 * gq + i], base[i]);
+                            v[4 * gq + i] = fmaf(sbl ? sbl[kGM + f + lo + i] : g.ls[f + i],
+                                                 v[4 * gq + i], base[i]);
                     }
                 }
             }
@@ -320,6 +330,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
 
     __shared__ __attribute__((aligned(16))) bf16 sW[2][kGM * kGRow];
     __shared__ __attribute__((aligned(16))) bf16 sX[2][kGN * kGRow];
+    __shared__ __attribute__((aligned(16))) float sBL[2 * kGM];   // the tile's bias, LayerScale
 
     // All of a token tile's feature tiles in one group (with FFN 1 on this
     // kernel, 16 feature tiles, so that an XCD's 32 tiles were 2 token tiles
@@ -435,7 +446,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm(GemmArgs g) {
         int f0;
         int64_t t0, tl;
         tile_of(i, f0, t0, tl);
-        gemm_epilogue<EPI, 4>(g, acc, f0, t0, tl, wm, 128 * wn, n, hh);
+        // The tile's bias and LayerScale through LDS: one read and one wait per
+        // thread, then one barrier, instead of a read and a wait per 32 x 32
+        // block.  The previous tile's epilogue finished reading sBL before the
+        // barriers of this tile's stages.
+        sBL[tid] = g.bias[f0 + tid];
+        sBL[kGM + tid] = g.ls[f0 + tid];
+        __syncthreads();
+        gemm_epilogue<EPI, 4>(g, acc, f0, t0, tl, wm, 128 * wn, n, hh, sBL);
 #pragma unroll
         for (int fb = 0; fb < 4; ++fb)
 #pragma unroll
