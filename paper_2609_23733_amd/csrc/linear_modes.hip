@@ -39,12 +39,14 @@ constexpr int kW = 72;           // bf16 LDS row stride
 // hidden units arrive eight-consecutive per lane-half, the K order of the
 // second MFMA.
 // ------------------------------------------------------------------------
-template <int ACT>
+// kAddV: the identity added (y = v + Eq.7), an instance of its own so that
+// the Eq.7 instance carries none of its registers.
+template <int ACT, bool kAddV>
 __global__ __launch_bounds__(256, 4) void k_surrogate_bf16(
     const bf16* __restrict__ V, const uint8_t* __restrict__ modes, const float* __restrict__ ctx,
     const bf16* __restrict__ gw1, const float* __restrict__ gb1, const bf16* __restrict__ gw2,
     const float* __restrict__ gb2, const bf16* __restrict__ dw1, const float* __restrict__ db1,
-    const bf16* __restrict__ dw2, const float* __restrict__ db2, int add_v, int64_t N, int H,
+    const bf16* __restrict__ dw2, const float* __restrict__ db2, int64_t N, int H,
     int rows, void* __restrict__ Y, int ydt) {
     const int h = blockIdx.y;
     if (modes[h] != MODE_SURR) return;
@@ -160,6 +162,17 @@ __global__ __launch_bounds__(256, 4) void k_surrogate_bf16(
             }
         }
         if (ok) {
+            // The token's 8 value groups, read together before the first is
+            // used (one wait, not one per group).
+            bf16x4 vin[2][4];
+            if constexpr (kAddV) {
+#pragma unroll
+                for (int db = 0; db < 2; ++db)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g)
+                        vin[db][g] = *reinterpret_cast<const bf16x4*>(
+                            V + (tok * H + h) * kD + 32 * db + 8 * g + 4 * hh);
+            }
 #pragma unroll
             for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -173,10 +186,9 @@ __global__ __launch_bounds__(256, 4) void k_surrogate_bf16(
                         y[i] = sC[d] + gam * (D[db][4 * g + i] + sB2d[d]);
                     }
                     const int64_t off = (tok * H + h) * kD + d0;
-                    if (add_v) {   // identity added: y = v + Eq.7
-                        const bf16x4 v = *reinterpret_cast<const bf16x4*>(V + off);
+                    if constexpr (kAddV) {   // identity added: y = v + Eq.7
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) y[i] += (float)v[i];
+                        for (int i = 0; i < 4; ++i) y[i] += (float)vin[db][g][i];
                     }
                     if (ydt == DT_BF16) {
                         bf16x4 v;
@@ -603,10 +615,11 @@ void launch_linear_heads(const AttnArgs& a, hipStream_t st) {
         const int add_v = v == SURR_ADD_IDENTITY;
         if (a.dtype == DT_BF16)
         {
-            auto* kern = a.act == 1 ? k_surrogate_bf16<1> : k_surrogate_bf16<0>;
+            auto* kern = add_v ? (a.act == 1 ? k_surrogate_bf16<1, true> : k_surrogate_bf16<0, true>)
+                               : (a.act == 1 ? k_surrogate_bf16<1, false> : k_surrogate_bf16<0, false>);
             hipLaunchKernelGGL(kern, dim3(nbs, a.H), dim3(256), 0, st, (const bf16*)a.V, a.modes, C,
                                (const bf16*)a.g_w1, a.g_b1, (const bf16*)a.g_w2, a.g_b2,
-                               (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2, add_v,
+                               (const bf16*)a.d_w1, a.d_b1, (const bf16*)a.d_w2, a.d_b2,
                                a.N, a.H, rows, a.Y, a.ydt);
         }
         else {
